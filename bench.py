@@ -1,0 +1,200 @@
+#!/usr/bin/env python3
+"""Benchmark: dense bf16 GEMM C = A*B (fp32 accumulate, fp32 out), 8192^3, one GPU.
+
+One step is one call of xgemm_run on the 8192 x 8192 x 8192 bf16 workload
+(entries uniform on [-1, 1], seed 2), inputs already resident in HBM.  Prints
+one JSON line.  ``value`` is the whole-job throughput over the K timed steps,
+bracketed by device synchronisation; ``roofline.achieved`` uses the average
+duration of the GEMM kernel from HIP events recorded on the stream the kernel
+is launched on.  The paper's own protocol (5 warm-up + 100 timed iterations,
+mean of the inter-quartile range; Section 6) is reported beside it.
+
+Usage: python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--workload NAME]
+       [--no-cpu-baseline] [--no-comparator] [--copy-calibration BYTES]
+"""
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2516.6, "fp16": 2516.6}  # MI355X dense MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+METRIC = "GEMM TFLOP/s and % of MI355X dense MFMA peak (bf16, 8192³) on 1 GPU"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters_%s.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2609_16389_amd", "csrc", "*"))):
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload: str):
+    """HBM bytes per launch from committed rocprofv3 --pmc counters, or None
+    if there are none or the kernel sources changed since they were taken."""
+    path = COUNTERS_FILE % workload
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, A, B, budget_s: float = 12.0):
+    """The oracle, untuned, on a bounded sample: the first R rows of C."""
+    import oracle
+    oracle.build(force=False)
+    cores = oracle.thread_count()
+    t0 = time.perf_counter()
+    oracle.gemm_rows(A, B, w.dtype, np.arange(8))
+    t_probe = time.perf_counter() - t0
+    rows = int(min(w.M, max(8, 8 * budget_s / max(t_probe, 1e-3))))
+    t0 = time.perf_counter()
+    oracle.gemm_rows(A, B, w.dtype, np.arange(rows))
+    t = time.perf_counter() - t0
+    flops = 2.0 * rows * w.N * w.K
+    return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": "rows 0..%d of C (%d x %d outputs, K=%d) of the %s workload, fp64, including "
+                      "decoding B; %.1f s" % (rows - 1, rows, w.N, w.K, w.name, t)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="gemm8192_bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-comparator", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0,
+                    help="also run a plain device copy of this many bytes (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this GEMM is not sharded across GPUs "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_16389_amd import workloads as wl
+    from paper_2609_16389_amd import xgemm as xg
+
+    w = wl.WORKLOADS[args.workload]
+    print("bench: workload %s M=%d N=%d K=%d %s" % (w.name, w.M, w.N, w.K, w.dtype), file=sys.stderr, flush=True)
+    A_bits, B_bits = wl.workload_inputs(w)
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float16
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    A = torch.from_numpy(A_bits.view(np.int16)).to(dev).view(tdt)
+    B = torch.from_numpy(B_bits.view(np.int16)).to(dev).view(tdt)
+    C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    h = xg.handle(0)
+    code = xg.XGEMM_BF16 if w.dtype == "bf16" else xg.XGEMM_FP16
+    cfg = xg.xgemm_select_config(w.M, w.N, w.K, code, torch.cuda.get_device_properties(dev).multi_processor_count)
+
+    def step():
+        rc = xg.xgemm_run(h, w.M, w.N, w.K, A.data_ptr(), w.K, B.data_ptr(), w.N, C.data_ptr(), w.N,
+                          code, stream.cuda_stream)
+        if rc != xg.XGEMM_OK:
+            raise xg.XgemmError(rc, xg.xgemm_last_error(h))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print("bench: warmup done", file=sys.stderr, flush=True)
+
+    # timed region: exactly K steps, bracketed by synchronisation; per-step
+    # HIP events on the launch stream give the kernel durations
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)]) * 1e-3  # seconds
+    print("bench: timed %d steps in %.3f s" % (args.steps, wall), file=sys.stderr, flush=True)
+
+    flops = float(w.flops)
+    ms_per_step = wall / args.steps * 1e3
+    value = flops * args.steps / wall / 1e12
+    avg_kernel = float(per.mean())
+    achieved = flops / avg_kernel / 1e12
+    srt = np.sort(per)
+    q = len(srt) // 4
+    iqr_mean = float(srt[q:len(srt) - q].mean()) if len(srt) >= 4 else float(srt.mean())
+    peak = PEAK_TFLOPS[w.dtype]
+
+    if args.copy_calibration:
+        n = args.copy_calibration // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+
+    comparator = None
+    if not args.no_comparator:
+        # torch.matmul (hipBLASLt) on the same inputs, bf16/fp16 output; context only
+        for _ in range(3):
+            torch.matmul(A, B)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(20):
+            torch.matmul(A, B)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) * 1e-3 / 20
+        comparator = {"name": "torch.matmul (hipBLASLt), 16-bit output", "tflops": round(flops / t / 1e12, 1)}
+
+    traffic = stored_traffic(w.name)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded uniform[-1,1], seed %d)" % w.seed if w.dist == "uniform"
+                else "synthetic (seeded normal(0,%g), seed %d)" % (w.param, w.seed),
+        "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "out": "fp32",
+                   "tile": cfg.tile, "split_k": cfg.split_k},
+        "pct_of_peak": round(100.0 * value / peak, 2),
+        "paper_protocol_iqr_mean_tflops": round(flops / iqr_mean / 1e12, 2),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4),
+                     "traffic": traffic},
+        "comparator": comparator,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("bench: cpu baseline (oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, A_bits, B_bits)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

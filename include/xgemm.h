@@ -1,0 +1,159 @@
+/*
+ * xgemm: dense matrix multiply C = A * B on an AMD Instinct MI355X (gfx950).
+ *
+ * A is M x K and B is K x N, both stored as 16-bit floating point (bfloat16 or
+ * IEEE binary16, the same type for both); C is M x N in fp32.  Products are
+ * accumulated in fp32 on the matrix (MFMA) units.  All matrices are row-major:
+ *
+ *     A[i][k] = A[i * lda + k]     B[k][j] = B[k * ldb + j]     C[i][j] = C[i * ldc + j]
+ *
+ * with leading dimensions counted in elements.  This is the plain sequential
+ * GEMM the paper starts every schedule from (Introduction; Section 2.3, chain
+ * of equivalence): C[i][j] = sum over k of A[i][k] * B[k][j].  The call
+ * overwrites C (no alpha/beta).  The kernels the paper builds from it, a
+ * non-split and a split-k GEMM (Section 6), correspond here to split_k = 1
+ * and split_k > 1.
+ *
+ * Accuracy contract: for every (i, j),
+ *     |C[i][j] - exact| <= 1e-4 * sum_k |A[i][k] * B[k][j]|
+ * where "exact" is the real-number result on the stored input values.
+ *
+ * Error behaviour: every entry point returns an xgemm_status.  Nothing is
+ * enqueued on a stream when a call fails; no entry point aborts or throws.
+ * Memory ownership: A, B and C are device pointers owned by the caller; the
+ * library never frees them nor keeps them past the call.  The library owns
+ * only the handle and the split-k workspace inside it.
+ */
+#ifndef XGEMM_H
+#define XGEMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct xgemm_ctx *xgemm_handle_t;
+
+/* Storage type of A and B. */
+enum xgemm_dtype {
+    XGEMM_BF16 = 0, /* bfloat16: 1 sign, 8 exponent (bias 127), 7 fraction bits */
+    XGEMM_FP16 = 1  /* IEEE binary16: 1 sign, 5 exponent (bias 15), 10 fraction bits */
+};
+
+enum xgemm_status {
+    XGEMM_OK = 0,
+    XGEMM_ERR_INVALID_ARG = 1, /* bad size, leading dimension, pointer, dtype or config */
+    XGEMM_ERR_UNSUPPORTED = 2, /* the current device is not a gfx950 GPU */
+    XGEMM_ERR_ALLOC = 3,       /* the split-k workspace could not be allocated */
+    XGEMM_ERR_HIP = 4          /* a HIP runtime call failed; see xgemm_last_error */
+};
+
+/* Output-tile shapes the kernels are built for (rows x columns of C per workgroup). */
+enum xgemm_tile {
+    XGEMM_TILE_256x256 = 0,
+    XGEMM_TILE_256x128 = 1,
+    XGEMM_TILE_128x128 = 2,
+    XGEMM_TILE_COUNT = 3
+};
+
+/*
+ * A launch configuration.  The paper tries, per problem size, the non-split
+ * kernel and split-k factors 1, 2, 4, 8 and 16 and keeps the fastest
+ * (Section 6); here the selector picks one from the problem shape and the
+ * device's compute-unit count, and xgemm_run_config lets a caller force one.
+ */
+typedef struct xgemm_config {
+    int32_t tile;    /* an xgemm_tile value */
+    int32_t split_k; /* number of K partitions, 1 .. 64; > 1 uses the workspace */
+    int32_t group_m; /* tile rows per group in the launch order, 1 .. 64 (L2 locality) */
+    int32_t reserved; /* must be 0 */
+} xgemm_config;
+
+/*
+ * Create a handle bound to the calling thread's current HIP device.  Caches
+ * the device's compute-unit count and architecture; allocates no device
+ * memory.  Returns XGEMM_ERR_UNSUPPORTED if the device is not gfx950,
+ * XGEMM_ERR_HIP if no device is usable, XGEMM_ERR_INVALID_ARG if out is NULL.
+ * The caller owns *out and releases it with xgemm_destroy.
+ */
+int xgemm_create(xgemm_handle_t *out);
+
+/*
+ * Release a handle and its workspace.  NULL is accepted (no-op).  Work that
+ * uses the handle's workspace must have completed (synchronize the stream
+ * first).
+ */
+int xgemm_destroy(xgemm_handle_t h);
+
+/*
+ * C = A * B, row-major, enqueued asynchronously on `stream` (a hipStream_t;
+ * NULL means the default stream).  C is complete once the stream has been
+ * synchronized.  Arguments:
+ *   M, N, K      sizes, each >= 0.  M == 0 or N == 0: no-op.  K == 0: C is
+ *                set to zero (the empty sum).
+ *   A, lda       device pointer to M x K values, lda >= K
+ *   B, ldb       device pointer to K x N values, ldb >= N
+ *   C, ldc       device pointer to M x N floats, ldc >= N; C must not overlap
+ *                A or B
+ *   dtype        XGEMM_BF16 or XGEMM_FP16 (applies to A and B)
+ * A pointer may be NULL only when its matrix has no elements.  Aligned fast
+ * path: A, B, C 16-byte aligned, lda and ldb multiples of 8, ldc a multiple of
+ * 4; any other alignment is still correct, through a slower element-wise
+ * path.  Sizes are limited to M, N, K < 2^31 with every matrix addressable in
+ * 64-bit element offsets.  A handle holds one workspace: calls that share a
+ * handle must be ordered on one stream.
+ */
+int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
+              const void *A, int64_t lda, const void *B, int64_t ldb,
+              float *C, int64_t ldc, int dtype, void *stream);
+
+/*
+ * As xgemm_run, with the launch configuration forced to *cfg (validated:
+ * XGEMM_ERR_INVALID_ARG for an unknown tile, a split_k or group_m out of
+ * range, or a non-zero reserved field).  Results agree with xgemm_run within
+ * the accuracy contract; only the summation grouping differs.
+ */
+int xgemm_run_config(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
+                     const void *A, int64_t lda, const void *B, int64_t ldb,
+                     float *C, int64_t ldc, int dtype, void *stream,
+                     const xgemm_config *cfg);
+
+/*
+ * The configuration xgemm_run would use for this problem on a device with
+ * `cu_count` compute units (host-only; touches no GPU).  Returns
+ * XGEMM_ERR_INVALID_ARG for negative sizes, an unknown dtype, cu_count < 1 or
+ * out == NULL.
+ */
+int xgemm_select_config(int64_t M, int64_t N, int64_t K, int dtype, int cu_count,
+                        xgemm_config *out);
+
+/*
+ * Workgroup tile of a tile id: rows (bm), columns (bn), K step (bk) and
+ * threads per workgroup.  Host-only.  XGEMM_ERR_INVALID_ARG for an unknown id
+ * or a NULL output pointer.
+ */
+int xgemm_tile_info(int tile, int *bm, int *bn, int *bk, int *threads);
+
+/*
+ * Bytes of split-k workspace a configuration needs for an M x N output
+ * (0 when split_k == 1).  Host-only.  Returns 0 for invalid arguments.
+ */
+size_t xgemm_workspace_bytes(int64_t M, int64_t N, const xgemm_config *cfg);
+
+/* Static description of a status code; never NULL. */
+const char *xgemm_strerror(int status);
+
+/*
+ * Detail of the last failure recorded on a handle (e.g. the HIP error text),
+ * or "" if none.  The string is owned by the handle and valid until the next
+ * call on it.  NULL handle: a static string.
+ */
+const char *xgemm_last_error(xgemm_handle_t h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XGEMM_H */

@@ -1,0 +1,212 @@
+"""ctypes binding for libxgemm (include/xgemm.h).
+
+Argument marshalling only: every entry point forwards to the HIP library with
+the same name, and all arithmetic runs in its kernels.  Torch tensors are used
+for device memory and streams; ``gemm`` reads their pointers, strides and the
+current stream and calls ``xgemm_run``.  There is no fallback path: if
+``libxgemm.so`` is missing the import of this module fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libxgemm.so")
+_HEADER = os.path.join(os.path.dirname(_PKG), "include", "xgemm.h")
+
+XGEMM_BF16 = 0
+XGEMM_FP16 = 1
+
+XGEMM_OK = 0
+XGEMM_ERR_INVALID_ARG = 1
+XGEMM_ERR_UNSUPPORTED = 2
+XGEMM_ERR_ALLOC = 3
+XGEMM_ERR_HIP = 4
+
+XGEMM_TILE_256x256 = 0
+XGEMM_TILE_256x128 = 1
+XGEMM_TILE_128x128 = 2
+XGEMM_TILE_COUNT = 3
+
+
+class xgemm_config(ctypes.Structure):
+    _fields_ = [("tile", ctypes.c_int32), ("split_k", ctypes.c_int32),
+                ("group_m", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+    def __repr__(self):
+        return "xgemm_config(tile=%d, split_k=%d, group_m=%d)" % (self.tile, self.split_k, self.group_m)
+
+
+class XgemmError(RuntimeError):
+    def __init__(self, status: int, detail: str = ""):
+        self.status = status
+        msg = "xgemm error %d (%s)" % (status, xgemm_strerror(status))
+        if detail:
+            msg += ": " + detail
+        super().__init__(msg)
+
+
+if not os.path.exists(_LIB_PATH):
+    raise ImportError("libxgemm.so is not built (%s); run __graft_entry__.build() or "
+                      "python -m paper_2609_16389_amd.build" % _LIB_PATH)
+
+lib = ctypes.CDLL(_LIB_PATH)
+
+_i64, _i32, _p = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
+_handle_t = ctypes.c_void_p
+
+lib.xgemm_create.argtypes = [ctypes.POINTER(_handle_t)]
+lib.xgemm_create.restype = _i32
+lib.xgemm_destroy.argtypes = [_handle_t]
+lib.xgemm_destroy.restype = _i32
+lib.xgemm_run.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p]
+lib.xgemm_run.restype = _i32
+lib.xgemm_run_config.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p,
+                                 ctypes.POINTER(xgemm_config)]
+lib.xgemm_run_config.restype = _i32
+lib.xgemm_select_config.argtypes = [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(xgemm_config)]
+lib.xgemm_select_config.restype = _i32
+lib.xgemm_tile_info.argtypes = [_i32] + [ctypes.POINTER(ctypes.c_int)] * 4
+lib.xgemm_tile_info.restype = _i32
+lib.xgemm_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(xgemm_config)]
+lib.xgemm_workspace_bytes.restype = ctypes.c_size_t
+lib.xgemm_strerror.argtypes = [_i32]
+lib.xgemm_strerror.restype = ctypes.c_char_p
+lib.xgemm_last_error.argtypes = [_handle_t]
+lib.xgemm_last_error.restype = ctypes.c_char_p
+
+
+def header_functions(path: str = _HEADER):
+    """Names of the functions include/xgemm.h declares."""
+    text = open(path).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(xgemm_[a-z_]+)\s*\(", text)))
+
+
+# ---------------------------------------------------------------------------
+# same-name wrappers (raw status codes, as the C ABI)
+# ---------------------------------------------------------------------------
+
+def xgemm_create() -> int:
+    """Returns a handle (an int address); raises XgemmError on failure."""
+    h = _handle_t()
+    rc = lib.xgemm_create(ctypes.byref(h))
+    if rc != XGEMM_OK:
+        raise XgemmError(rc)
+    return h.value
+
+
+def xgemm_destroy(h) -> int:
+    return lib.xgemm_destroy(h)
+
+
+def xgemm_run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream) -> int:
+    return lib.xgemm_run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream)
+
+
+def xgemm_run_config(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream, cfg) -> int:
+    return lib.xgemm_run_config(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream,
+                                ctypes.byref(cfg) if cfg is not None else None)
+
+
+def xgemm_select_config(M, N, K, dtype, cu_count) -> xgemm_config:
+    cfg = xgemm_config()
+    rc = lib.xgemm_select_config(M, N, K, dtype, cu_count, ctypes.byref(cfg))
+    if rc != XGEMM_OK:
+        raise XgemmError(rc)
+    return cfg
+
+
+def xgemm_tile_info(tile):
+    vals = [ctypes.c_int() for _ in range(4)]
+    rc = lib.xgemm_tile_info(tile, *[ctypes.byref(v) for v in vals])
+    if rc != XGEMM_OK:
+        raise XgemmError(rc)
+    return tuple(v.value for v in vals)  # (bm, bn, bk, threads)
+
+
+def xgemm_workspace_bytes(M, N, cfg) -> int:
+    return int(lib.xgemm_workspace_bytes(M, N, ctypes.byref(cfg)))
+
+
+def xgemm_strerror(status: int) -> str:
+    return lib.xgemm_strerror(status).decode()
+
+
+def xgemm_last_error(h) -> str:
+    return lib.xgemm_last_error(h).decode()
+
+
+# ---------------------------------------------------------------------------
+# torch convenience layer (marshalling only)
+# ---------------------------------------------------------------------------
+
+_handles = {}
+
+
+def handle(device_index: int | None = None):
+    """A per-device handle owned by this module (created on first use)."""
+    import torch
+    if device_index is None:
+        device_index = torch.cuda.current_device()
+    h = _handles.get(device_index)
+    if h is None:
+        with torch.cuda.device(device_index):
+            h = xgemm_create()
+        _handles[device_index] = h
+    return h
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return XGEMM_BF16
+    if t.dtype == torch.float16:
+        return XGEMM_FP16
+    raise TypeError("A and B must be bfloat16 or float16 tensors, got %s" % t.dtype)
+
+
+def _ld(t) -> int:
+    if t.dim() != 2:
+        raise ValueError("expected a 2-D tensor")
+    if t.shape[1] > 1 and t.stride(1) != 1:
+        raise ValueError("rows must be contiguous (stride(1) == 1)")
+    if t.shape[0] <= 1:
+        return max(t.shape[1], t.stride(0))
+    return t.stride(0)
+
+
+def gemm(A, B, out=None, config: xgemm_config | None = None, stream=None):
+    """C = A @ B with fp32 output, through xgemm_run (or xgemm_run_config).
+
+    A: (M, K) and B: (K, N) bfloat16/float16 CUDA tensors of one dtype with
+    contiguous rows; out: optional (M, N) float32 tensor with contiguous rows.
+    Enqueued on ``stream`` (default: torch's current stream).
+    """
+    import torch
+    if A.dtype != B.dtype:
+        raise TypeError("A and B must have the same dtype")
+    dtype = _dtype_code(A)
+    M, K = A.shape
+    K2, N = B.shape
+    if K2 != K:
+        raise ValueError("inner dimensions differ: %d vs %d" % (K, K2))
+    if not (A.is_cuda and B.is_cuda) or A.device != B.device:
+        raise ValueError("A and B must be on the same GPU")
+    if out is None:
+        out = torch.empty((M, N), dtype=torch.float32, device=A.device)
+    if out.dtype != torch.float32 or tuple(out.shape) != (M, N) or out.device != A.device:
+        raise ValueError("out must be a float32 (M, N) tensor on A's device")
+    s = stream if stream is not None else torch.cuda.current_stream(A.device)
+    h = handle(A.device.index)
+    args = (h, M, N, K, A.data_ptr() or None, _ld(A), B.data_ptr() or None, _ld(B),
+            out.data_ptr() or None, _ld(out), dtype, s.cuda_stream)
+    if config is None:
+        rc = xgemm_run(*args)
+    else:
+        rc = xgemm_run_config(*args, config)
+    if rc != XGEMM_OK:
+        raise XgemmError(rc, xgemm_last_error(h))
+    return out

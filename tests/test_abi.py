@@ -1,0 +1,81 @@
+"""The C-ABI library: it loads, exports what the header declares, and its
+host-only entry points (configuration selection, tile info, argument checks)
+behave as documented.  No GPU work is launched here."""
+import ctypes
+import math
+
+import pytest
+
+from paper_2609_16389_amd import workloads as wl
+from paper_2609_16389_amd import xgemm as xg
+
+
+def test_every_header_function_is_exported():
+    names = xg.header_functions()
+    assert "xgemm_create" in names and "xgemm_run" in names and "xgemm_destroy" in names
+    for n in names:
+        assert hasattr(xg.lib, n), "libxgemm.so does not export %s" % n
+
+
+def test_strerror_codes():
+    for code in range(5):
+        assert xg.xgemm_strerror(code) not in ("", "unknown status")
+    assert xg.xgemm_strerror(99) == "unknown status"
+
+
+def test_null_handle_is_invalid_argument():
+    assert xg.xgemm_run(None, 1, 1, 1, None, 1, None, 1, None, 1, xg.XGEMM_BF16, None) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.xgemm_destroy(None) == xg.XGEMM_OK
+    assert xg.xgemm_last_error(None) == "no handle"
+    assert xg.lib.xgemm_create(None) == xg.XGEMM_ERR_INVALID_ARG
+
+
+def test_tile_info():
+    seen = set()
+    for t in range(xg.XGEMM_TILE_COUNT):
+        bm, bn, bk, threads = xg.xgemm_tile_info(t)
+        assert bm % 32 == 0 and bn % 32 == 0 and bk % 16 == 0 and threads % 64 == 0
+        # two LDS stages fit in 160 KiB
+        assert 2 * (bm + bn) * bk * 2 <= 160 * 1024
+        seen.add((bm, bn))
+    assert len(seen) == xg.XGEMM_TILE_COUNT
+    with pytest.raises(xg.XgemmError):
+        xg.xgemm_tile_info(xg.XGEMM_TILE_COUNT)
+
+
+@pytest.mark.parametrize("name", sorted(wl.WORKLOADS))
+def test_selector_on_workloads(name):
+    w = wl.WORKLOADS[name]
+    dt = xg.XGEMM_BF16 if w.dtype == "bf16" else xg.XGEMM_FP16
+    cfg = xg.xgemm_select_config(w.M, w.N, w.K, dt, 256)
+    assert 0 <= cfg.tile < xg.XGEMM_TILE_COUNT and 1 <= cfg.split_k <= 16 and cfg.group_m >= 1
+    bm, bn, bk, _ = xg.xgemm_tile_info(cfg.tile)
+    tiles = math.ceil(w.M / bm) * math.ceil(w.N / bn)
+    # every split has a non-empty K range
+    chunk = math.ceil(math.ceil(w.K / cfg.split_k) / bk) * bk
+    assert chunk * (cfg.split_k - 1) < w.K
+    if name == "skinny1024x1024x65536_bf16":
+        # 1024 x 1024 has too few output tiles to fill 256 CUs without splitting K
+        assert cfg.split_k > 1 and tiles * cfg.split_k >= 128
+    if name == "gemm8192_bf16":
+        assert cfg.split_k == 1 and (bm, bn) == (256, 256)
+
+
+def test_selector_rejects_bad_arguments():
+    cfg = xg.xgemm_config()
+    assert xg.lib.xgemm_select_config(-1, 1, 1, 0, 256, ctypes.byref(cfg)) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.lib.xgemm_select_config(1, 1, 1, 7, 256, ctypes.byref(cfg)) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.lib.xgemm_select_config(1, 1, 1, 0, 0, ctypes.byref(cfg)) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.lib.xgemm_select_config(1, 1, 1, 0, 256, None) == xg.XGEMM_ERR_INVALID_ARG
+
+
+def test_workspace_bytes():
+    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, reserved=0)
+    assert xg.xgemm_workspace_bytes(1024, 1024, cfg) == 0
+    cfg.split_k = 16
+    assert xg.xgemm_workspace_bytes(1024, 1024, cfg) == 16 * 1024 * 1024 * 4
+    assert xg.xgemm_workspace_bytes(10, 5, cfg) == 16 * 10 * 8 * 4  # rows padded to 4 floats
+    cfg.reserved = 1
+    assert xg.xgemm_workspace_bytes(10, 5, cfg) == 0
+    cfg.reserved, cfg.tile = 0, 99
+    assert xg.xgemm_workspace_bytes(10, 5, cfg) == 0

@@ -1,0 +1,284 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Bar: |C_gpu - C_ref| <= 1e-4 * sum_k |a_ik b_kj| elementwise, no NaN; and
+bit-for-bit equality where the exact result is representable and every
+partial sum is exact in fp32 (small integers, identity, permutations).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import (CODE, check_close, check_exact, config, empty_out, run_gpu, to_device)
+from paper_2609_16389_amd import workloads as wl
+from paper_2609_16389_amd import xgemm as xg
+
+pytestmark = pytest.mark.gpu
+
+TILES = list(range(xg.XGEMM_TILE_COUNT))
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _oracle_built():
+    oracle.build(force=False)
+
+
+def _case(M, N, K, dtype, seed, dist="uniform"):
+    A, B = wl.make_inputs(M, N, K, dtype, dist, seed)
+    C_ref, S = oracle.gemm(A, B, dtype)
+    return A, B, C_ref, S
+
+
+# ---------------------------------------------------------------------------
+# small and ragged shapes, every tile, both dtypes
+# ---------------------------------------------------------------------------
+
+RAGGED = [(1, 1, 1), (17, 33, 65), (64, 64, 64), (255, 257, 129), (300, 520, 200),
+          (513, 129, 1000), (1000, 1000, 1000)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("shape", RAGGED, ids=lambda s: "x".join(map(str, s)))
+def test_ragged_default_config(dtype, shape):
+    M, N, K = shape
+    A, B, C_ref, S = _case(M, N, K, dtype, seed=M * 7 + N)
+    check_close(run_gpu(A, B, dtype), C_ref, S, "default %s %s" % (dtype, shape))
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("shape", [(256, 256, 256), (255, 257, 129), (520, 300, 700)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_every_tile(tile, shape):
+    M, N, K = shape
+    for dtype in ("bf16", "fp16"):
+        A, B, C_ref, S = _case(M, N, K, dtype, seed=tile + 11)
+        check_close(run_gpu(A, B, dtype, config=config(tile)), C_ref, S, "tile %d %s" % (tile, dtype))
+
+
+def test_workload_256_fp16_full():
+    """The 256^3 fp16 workload (uniform[-1,1], seed 0), every element."""
+    w = wl.WORKLOADS["gemm256_fp16"]
+    A, B = wl.workload_inputs(w)
+    C_ref, S = oracle.gemm(A, B, w.dtype)
+    check_close(run_gpu(A, B, w.dtype), C_ref, S, w.name)
+
+
+# ---------------------------------------------------------------------------
+# split-k (the paper tries split factors 1, 2, 4, 8, 16)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("split", [1, 2, 4, 8, 16])
+@pytest.mark.parametrize("tile", TILES)
+def test_split_k_factors(split, tile):
+    M, N, K = 384, 320, 4100  # K not a multiple of the K step
+    A, B, C_ref, S = _case(M, N, K, "bf16", seed=split)
+    check_close(run_gpu(A, B, "bf16", config=config(tile, split)), C_ref, S,
+                "tile %d split %d" % (tile, split))
+
+
+@pytest.mark.parametrize("split", [2, 16])
+def test_split_k_integer_exact(split):
+    M, N, K = 200, 136, 2048
+    A, B = wl.make_int_inputs(M, N, K, "fp16", seed=split)
+    C_ref, _ = oracle.gemm(A, B, "fp16")
+    check_exact(run_gpu(A, B, "fp16", config=config(xg.XGEMM_TILE_128x128, split)), C_ref)
+
+
+# ---------------------------------------------------------------------------
+# exact cases
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("shape", [(128, 128, 128), (333, 260, 1111), (512, 768, 2048)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_small_integers_bit_exact(dtype, shape):
+    M, N, K = shape
+    A, B = wl.make_int_inputs(M, N, K, dtype, seed=K)
+    C_ref, _ = oracle.gemm(A, B, dtype)
+    for tile in TILES:
+        check_exact(run_gpu(A, B, dtype, config=config(tile)), C_ref, "tile %d" % tile)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_identity_bit_exact(dtype):
+    M, K = 300, 264
+    A, _ = wl.make_inputs(M, 1, K, dtype, "normal", seed=3)
+    I = wl.to_bits(np.eye(K), dtype)
+    C_ref, _ = oracle.gemm(A, I, dtype)
+    check_exact(run_gpu(A, I, dtype), C_ref, "A*I")
+    I_M = wl.to_bits(np.eye(M), dtype)
+    C_ref2, _ = oracle.gemm(I_M, A, dtype)
+    check_exact(run_gpu(I_M, A, dtype), C_ref2, "I*A")
+
+
+def test_permutation_bit_exact():
+    rng = np.random.default_rng(5)
+    M, K = 256, 512
+    A, _ = wl.make_inputs(M, 1, K, "bf16", "uniform", seed=8)
+    P = np.zeros((K, K))
+    P[np.arange(K), rng.permutation(K)] = 1.0
+    Pb = wl.to_bits(P, "bf16")
+    C_ref, _ = oracle.gemm(A, Pb, "bf16")
+    check_exact(run_gpu(A, Pb, "bf16"), C_ref, "A*P")
+
+
+def test_fp16_subnormals():
+    # every A entry subnormal, B powers of two: each product exact in fp32
+    rng = np.random.default_rng(6)
+    M, N, K = 128, 96, 256
+    A = rng.integers(1, 1024, size=(M, K)).astype(np.uint16) | (rng.integers(0, 2, size=(M, K)) << 15).astype(np.uint16)
+    B = wl.to_bits(2.0 ** rng.integers(-2, 8, size=(K, N)), "fp16")
+    C_ref, S = oracle.gemm(A, B, "fp16")
+    C = run_gpu(A, B, "fp16")
+    check_close(C, C_ref, S, "subnormal")
+    assert np.count_nonzero(C) > 0.9 * C.size
+
+
+# ---------------------------------------------------------------------------
+# layouts, alignment, degenerate sizes
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_padded_leading_dimensions(dtype):
+    M, N, K = 260, 300, 200
+    A, B, C_ref, S = _case(M, N, K, dtype, seed=21)
+    out = empty_out(M, N, ldc=N + 12)
+    C = run_gpu(A, B, dtype, lda=K + 24, ldb=N + 8, out=out)
+    check_close(C, C_ref, S, "padded ld")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_unaligned_pointers_and_odd_leading_dimensions(dtype):
+    M, N, K = 131, 77, 95
+    A, B, C_ref, S = _case(M, N, K, dtype, seed=22)
+    out = empty_out(M, N, ldc=N + 1, offset=1)
+    C = run_gpu(A, B, dtype, lda=K + 3, ldb=N + 1, offset=1, out=out)
+    check_close(C, C_ref, S, "unaligned")
+
+
+def test_output_padding_untouched():
+    M, N, K = 64, 40, 64
+    A, B, C_ref, S = _case(M, N, K, "bf16", seed=23)
+    out = empty_out(M, N, ldc=N + 8, fill=123.0)
+    run_gpu(A, B, "bf16", out=out)
+    full = out.as_strided((M, N + 8), (N + 8, 1)).cpu().numpy()
+    assert np.all(full[:, N:] == 123.0)
+    check_close(full[:, :N], C_ref, S)
+
+
+def test_zero_k_gives_zero():
+    A = torch.empty((5, 0), dtype=torch.bfloat16, device="cuda")
+    B = torch.empty((0, 7), dtype=torch.bfloat16, device="cuda")
+    out = empty_out(5, 7, fill=9.0)
+    xg.gemm(A, B, out=out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 0)
+
+
+def test_empty_m_or_n_is_noop():
+    A = torch.ones((0, 16), dtype=torch.float16, device="cuda")
+    B = torch.ones((16, 8), dtype=torch.float16, device="cuda")
+    assert xg.gemm(A, B).shape == (0, 8)
+    A2 = torch.ones((4, 16), dtype=torch.float16, device="cuda")
+    B2 = torch.ones((16, 0), dtype=torch.float16, device="cuda")
+    assert xg.gemm(A2, B2).shape == (4, 0)
+    torch.cuda.synchronize()
+
+
+def test_invalid_arguments_on_gpu():
+    h = xg.handle()
+    A = torch.zeros((4, 4), dtype=torch.bfloat16, device="cuda")
+    C = torch.zeros((4, 4), dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream().cuda_stream
+    a, c = A.data_ptr(), C.data_ptr()
+    assert xg.xgemm_run(h, 4, 4, 4, a, 3, a, 4, c, 4, 0, s) == xg.XGEMM_ERR_INVALID_ARG  # lda < K
+    assert xg.xgemm_run(h, 4, 4, 4, a, 4, a, 4, c, 3, 0, s) == xg.XGEMM_ERR_INVALID_ARG  # ldc < N
+    assert xg.xgemm_run(h, 4, 4, 4, a, 4, a, 4, c, 4, 5, s) == xg.XGEMM_ERR_INVALID_ARG  # dtype
+    assert xg.xgemm_run(h, -1, 4, 4, a, 4, a, 4, c, 4, 0, s) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.xgemm_run(h, 4, 4, 4, None, 4, a, 4, c, 4, 0, s) == xg.XGEMM_ERR_INVALID_ARG
+    bad = config(xg.XGEMM_TILE_COUNT)
+    assert xg.xgemm_run_config(h, 4, 4, 4, a, 4, a, 4, c, 4, 0, s, bad) == xg.XGEMM_ERR_INVALID_ARG
+    bad = config(0, split=0)
+    assert xg.xgemm_run_config(h, 4, 4, 4, a, 4, a, 4, c, 4, 0, s, bad) == xg.XGEMM_ERR_INVALID_ARG
+    torch.cuda.synchronize()
+    assert torch.all(C == 0)  # nothing was enqueued
+
+
+def test_own_handle_lifecycle_and_stream():
+    h = xg.xgemm_create()
+    try:
+        M, N, K = 200, 300, 400
+        A, B, C_ref, S = _case(M, N, K, "fp16", seed=31)
+        dA, dB = to_device(A, "fp16"), to_device(B, "fp16")
+        C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        st = torch.cuda.Stream()
+        with torch.cuda.stream(st):
+            rc = xg.xgemm_run_config(h, M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, C.data_ptr(), N,
+                                     xg.XGEMM_FP16, st.cuda_stream, config(xg.XGEMM_TILE_256x256, 4))
+            assert rc == xg.XGEMM_OK, xg.xgemm_last_error(h)
+        st.synchronize()
+        check_close(C.cpu().numpy(), C_ref, S, "own handle")
+    finally:
+        assert xg.xgemm_destroy(h) == xg.XGEMM_OK
+
+
+def test_run_to_run_deterministic():
+    M, N, K = 512, 512, 8192
+    A, B = wl.make_inputs(M, N, K, "bf16", "normal", seed=41)
+    for cfg in (None, config(xg.XGEMM_TILE_128x128, 8)):
+        c1 = run_gpu(A, B, "bf16", config=cfg)
+        c2 = run_gpu(A, B, "bf16", config=cfg)
+        assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+
+
+def test_transpose_identity():
+    M, N, K = 320, 192, 640
+    A, B, C_ref, S = _case(M, N, K, "bf16", seed=51)
+    Ct = run_gpu(np.ascontiguousarray(B.T), np.ascontiguousarray(A.T), "bf16")
+    check_close(Ct.T, C_ref, S, "(B^T A^T)^T")
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads in the configuration the benchmark times; outputs
+# sampled (whole rows, whole columns, scattered entries) and checked one by
+# one against the oracle
+# ---------------------------------------------------------------------------
+
+BIG = ["gemm4096_bf16", "gemm8192_bf16", "proj16384x5120x4096_fp16", "proj4096x14336x4096_fp16",
+       "skinny1024x1024x65536_bf16"]
+
+
+@pytest.mark.parametrize("name", BIG)
+def test_full_size_workload_sampled(name):
+    w = wl.WORKLOADS[name]
+    A, B = wl.workload_inputs(w)
+    C = run_gpu(A, B, w.dtype)
+    rng = np.random.default_rng(1234)
+    rows = np.unique(np.concatenate([[0, w.M - 1], rng.integers(0, w.M, 6)]))
+    Cr, Sr = oracle.gemm_rows(A, B, w.dtype, rows)
+    check_close(C[rows], Cr, Sr, "%s rows" % name)
+    cols = np.unique(np.concatenate([[0, w.N - 1], rng.integers(0, w.N, 6)]))
+    ri = np.repeat(np.arange(w.M), cols.size)
+    ci = np.tile(cols, w.M)
+    c, s = oracle.gemm_entries(A, B, w.dtype, ri, ci)
+    check_close(C[ri, ci].reshape(w.M, cols.size), c.reshape(w.M, cols.size), s.reshape(w.M, cols.size),
+                "%s cols" % name)
+    ri = rng.integers(0, w.M, 4096)
+    ci = rng.integers(0, w.N, 4096)
+    c, s = oracle.gemm_entries(A, B, w.dtype, ri, ci)
+    check_close(C[ri, ci][None], c[None], s[None], "%s entries" % name)
+
+
+def test_full_size_8192_integer_exact_sampled():
+    """8192^3 with integer entries in [-8, 8]: every partial sum is an integer
+    below 2^24, so the fp32 result must equal the oracle exactly."""
+    M = N = K = 8192
+    A, B = wl.make_int_inputs(M, N, K, "bf16", seed=2)
+    C = run_gpu(A, B, "bf16")
+    rng = np.random.default_rng(99)
+    rows = rng.integers(0, M, 4)
+    Cr, _ = oracle.gemm_rows(A, B, "bf16", rows)
+    check_exact(C[rows], Cr, "int rows")
+    ri, ci = rng.integers(0, M, 4096), rng.integers(0, N, 4096)
+    c, _ = oracle.gemm_entries(A, B, "bf16", ri, ci)
+    check_exact(C[ri, ci][None], c[None], "int entries")
