@@ -58,10 +58,14 @@ def cpu_baseline(w, A, B, budget_s: float = 12.0):
     import oracle
     oracle.build(force=False)
     cores = oracle.thread_count()
+    # two probes separate the per-call cost (decoding B) from the per-row cost
     t0 = time.perf_counter()
-    oracle.gemm_rows(A, B, w.dtype, np.arange(8))
-    t_probe = time.perf_counter() - t0
-    rows = int(min(w.M, max(8, 8 * budget_s / max(t_probe, 1e-3))))
+    oracle.gemm_rows(A, B, w.dtype, np.arange(cores))
+    t1 = time.perf_counter()
+    oracle.gemm_rows(A, B, w.dtype, np.arange(4 * cores))
+    t2 = time.perf_counter()
+    per_row = max((t2 - t1) - (t1 - t0), 1e-4) / (3 * cores)
+    rows = int(min(w.M, max(cores, budget_s / per_row)))
     t0 = time.perf_counter()
     oracle.gemm_rows(A, B, w.dtype, np.arange(rows))
     t = time.perf_counter() - t0

@@ -48,6 +48,11 @@ class XgemmError(RuntimeError):
         super().__init__(msg)
 
 
+# torch ships its own HIP runtime with the same soname as the system one.  It
+# must be loaded first so that libxgemm.so binds to it: one runtime per
+# process, so that torch's device memory and streams are valid here.
+import torch  # noqa: E402,F401
+
 if not os.path.exists(_LIB_PATH):
     raise ImportError("libxgemm.so is not built (%s); run __graft_entry__.build() or "
                       "python -m paper_2609_16389_amd.build" % _LIB_PATH)

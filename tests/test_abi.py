@@ -79,3 +79,19 @@ def test_workspace_bytes():
     assert xg.xgemm_workspace_bytes(10, 5, cfg) == 0
     cfg.reserved, cfg.tile = 0, 99
     assert xg.xgemm_workspace_bytes(10, 5, cfg) == 0
+
+
+def test_single_hip_runtime_in_process():
+    """libxgemm.so must bind to the HIP runtime torch loaded, not a second copy,
+    whatever the import order (torch's device pointers and streams belong to
+    its runtime)."""
+    import subprocess
+    import sys
+    code = ("import ctypes, sys; sys.path.insert(0, %r)\n"
+            "import paper_2609_16389_amd.xgemm\n"
+            "import torch\n"
+            "maps = open('/proc/self/maps').read().split('\\n')\n"
+            "libs = sorted({l.split()[-1] for l in maps if 'libamdhip64' in l})\n"
+            "print(len(libs), libs)\n") % xg._PKG.rsplit("/", 1)[0]
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, check=True).stdout
+    assert out.startswith("1 "), out
