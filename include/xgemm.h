@@ -136,6 +136,23 @@ int xgemm_select_config(int64_t M, int64_t N, int64_t K, int dtype, int cu_count
  */
 int xgemm_tile_info(int tile, int *bm, int *bn, int *bk, int *threads);
 
+/* Kernel families (see xgemm_kernel_family). */
+enum xgemm_kernel_family_id {
+    XGEMM_KERNEL_GENERAL = 0,   /* any shape and alignment; element-wise edge handling */
+    XGEMM_KERNEL_PIPELINED = 1  /* direct global-to-LDS loads, multi-stage LDS pipeline */
+};
+
+/*
+ * Which kernel family xgemm_run_config would launch for these arguments
+ * (host-only; A and B are only inspected for their alignment).  The
+ * pipelined family needs A and B 16-byte aligned, lda and ldb multiples of
+ * 8, N a multiple of 8, K a multiple of 32 and at least 128 K values in
+ * every split; everything else runs on the general family.  Returns -1 for
+ * M, N or K <= 0, leading dimensions too small, or an invalid cfg.
+ */
+int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                        const void *B, int64_t ldb, const xgemm_config *cfg);
+
 /*
  * Bytes of split-k workspace a configuration needs for an M x N output
  * (0 when split_k == 1).  Host-only.  Returns 0 for invalid arguments.

@@ -24,6 +24,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 namespace xgemm_dev {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -317,6 +319,276 @@ gemm_kernel(GemmParams p)
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const int col = n0 + wn * TN + j * 32 + q * 8 + (lane >> 5) * 4;
+                f32x4 v;
+                v.x = acc[i][j][4 * q + 0];
+                v.y = acc[i][j][4 * q + 1];
+                v.z = acc[i][j][4 * q + 2];
+                v.w = acc[i][j][4 * q + 3];
+                if (vec_store) {
+                    *(f32x4 *)(Cb + (int64_t)row * ldc + col) = v;
+                } else if (row < p.M) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (col + e < p.N)
+                            Cb[(int64_t)row * ldc + col + e] = v[e];
+                }
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Pipelined kernel for 16-byte aligned operands with K a multiple of BK.
+//
+// Global -> LDS without registers: each wave issues 16-byte direct-to-LDS
+// loads (a lane's 16 bytes land at LDS base + 16 * lane), so the LDS layout
+// is chosen by which global chunk each lane fetches.  STAGES K steps are in
+// flight at once.  Fragments:
+//   A  (BM x BK, k contiguous, rows of BK*2 bytes): ds_read_b128 of 8
+//      consecutive k of one row; 16-byte chunk c of row r is stored at slot
+//      c ^ ((r >> 2) & 3), so 16 consecutive rows read at one logical chunk
+//      cover all 16 slots of a 256-byte bank window;
+//   B  (BK x BN, n contiguous as in memory, rows of BN*2 bytes):
+//      ds_read_b64_tr_b16 -- within each group of 16 lanes, lane i receives
+//      element (i % 4) of the 8 bytes addressed by lane 4e + i / 4 as its
+//      element e, which turns a 4 (k) x 16 (n) block into the k-packed
+//      MFMA operand; 64-byte block b of row k is stored at block
+//      b ^ (k & 3) so the four rows of one read fall in different banks.
+// M and N edges: rows and columns beyond the matrix are clamped to the last
+// valid one (they only feed outputs that are never stored).
+//
+// Schedule of K step t (fragment buffers alternate between K sub-steps):
+//   read fragments of the last sub-step of t         (LDS stage t)
+//   MFMAs of the other sub-steps of t
+//   wait: own fragment reads done, own loads of stage t+1 landed; barrier
+//   issue direct loads of step t+STAGES into stage t (now free)
+//   read fragments of sub-step 0 of t+1               (LDS stage t+1)
+//   MFMAs of the last sub-step of t
+// ---------------------------------------------------------------------------
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+
+// 16 bytes per lane from global (scalar base + per-lane byte offset) to LDS
+// at lds_addr + 16 * lane.  Issued as inline assembly so that the compiler's
+// wait insertion does not treat it as a pending LDS write (it would otherwise
+// wait for every such load before each LDS read); the kernels place their
+// own vmcnt waits.
+__device__ __forceinline__ void lds_load16(const void *gbase, uint32_t voff, uint32_t lds_addr)
+{
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(gbase), "{m0}"(lds_addr) : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_address(const void *p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char *)p;
+}
+
+__device__ __forceinline__ v4i16 ds_read_tr16(const char *p)
+{
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4i16 *)p);
+}
+
+// s_waitcnt with only vmcnt constrained (gfx9 encoding: vmcnt bits 3:0 and
+// 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+__device__ __forceinline__ void wait_lgkmcnt0()
+{
+    __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));
+}
+
+// Workgroup barrier that the compiler may not move memory accesses across;
+// it adds no waits of its own (they are explicit at each use).
+__device__ __forceinline__ void barrier_only()
+{
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT>
+__global__ void __launch_bounds__(WGM * WGN * 64, 1)
+gemm_kernel_dma(GemmParams p)
+{
+    constexpr int NW = WGM * WGN;
+    constexpr int TM = BM / WGM, TN = BN / WGN;
+    constexpr int FM = TM / 32, FN = TN / 32;
+    constexpr int KS = BK / 16;                  // MFMA k sub-steps per K step
+    constexpr int A_ROWB = BK * 2;
+    constexpr int B_ROWB = BN * 2;
+    constexpr int A_BYTES = BM * A_ROWB;
+    constexpr int B_BYTES = BK * B_ROWB;
+    constexpr int STAGE = A_BYTES + B_BYTES;
+    constexpr int A_LD = A_BYTES / 1024 / NW;    // direct loads per wave per K step
+    constexpr int B_LD = B_BYTES / 1024 / NW;
+    constexpr int LD = A_LD + B_LD;
+    constexpr int A_ROWS_PER_LD = 1024 / A_ROWB; // tile rows one load instruction fills
+    constexpr int B_ROWS_PER_LD = 1024 / B_ROWB;
+    static_assert(BK == 32, "A layout assumes 64-byte rows");
+    static_assert(BN % 32 == 0 && B_ROWB <= 1024 && 1024 % B_ROWB == 0, "B layout");
+    static_assert(A_LD * NW * 1024 == A_BYTES && B_LD * NW * 1024 == B_BYTES, "load split");
+    static_assert(KS >= 2 && STAGES >= 2 && STAGES * STAGE <= 160 * 1024, "pipeline shape");
+    static_assert((STAGES - 1) * LD < 64, "vmcnt range");
+
+    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
+
+    int tm, tn, ks;
+    map_tile(p, tm, tn, ks);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kbeg = ks * p.k_chunk;
+    const int kend = min(p.K, kbeg + p.k_chunk);
+    const int nk = kend > kbeg ? (kend - kbeg) / BK : 0;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WGM, wn = wave / WGM;
+    const int64_t lda = p.lda, ldb = p.ldb;
+
+    // --- per-lane byte offsets of the direct loads (relative to the tile) ---
+    uint32_t a_goff[A_LD], b_goff[B_LD];
+    const int mmax = p.M - 1 - m0;               // last valid tile row
+    const int nmax = ((p.N - 1) / 8) * 8 - n0;   // last valid 8-column chunk
+#pragma unroll
+    for (int j = 0; j < A_LD; ++j) {
+        const int r = (wave * A_LD + j) * A_ROWS_PER_LD + lane / 4;
+        const int c = (lane & 3) ^ ((r >> 2) & 3);
+        a_goff[j] = (uint32_t)((min(r, mmax) * lda + c * 8) * 2);
+    }
+#pragma unroll
+    for (int j = 0; j < B_LD; ++j) {
+        const int k = (wave * B_LD + j) * B_ROWS_PER_LD + lane / (B_ROWB / 16);
+        const int q = lane % (B_ROWB / 16);          // physical 16-byte chunk in the row
+        const int lb = (q >> 2) ^ (k & 3);           // logical 64-byte block
+        const int n = lb * 32 + (q & 3) * 8;
+        b_goff[j] = (uint32_t)((k * ldb + min(n, nmax)) * 2);
+    }
+
+    auto issue_loads = [&](int kstep, int stage) {
+        const int k0 = kbeg + kstep * BK;
+        const uint16_t *Ab = p.A + (int64_t)m0 * lda + k0;
+        const uint16_t *Bb = p.B + (int64_t)k0 * ldb + n0;
+        const uint32_t sA = lds_address(smem) + stage * STAGE;
+        const uint32_t sB = sA + A_BYTES;
+#pragma unroll
+        for (int j = 0; j < A_LD; ++j)
+            lds_load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
+#pragma unroll
+        for (int j = 0; j < B_LD; ++j)
+            lds_load16(Bb, b_goff[j], sB + (wave * B_LD + j) * 1024);
+    };
+
+    // --- fragment addressing ---
+    const int l32 = lane & 31;
+    const int g = lane >> 5;                      // k half of the MFMA operand
+    // A: row wm*TM + i*32 + l32, logical chunk 2*kk + g
+    const int a_x = g ^ ((l32 >> 2) & 3);
+    const int a_lane = (wm * TM + l32) * A_ROWB;
+    // B: rows kk*16 + 8g + 4c + s/4, columns wn*TN + j*32 + 16h + 4(s%4)
+    const int s16 = lane & 15;
+    const int h = (lane >> 4) & 1;
+    const int t4 = s16 >> 2;                      // equals row & 3
+    const int b_lane = (8 * g + t4) * B_ROWB + 32 * h + 8 * (s16 & 3);
+    const int b_blk0 = wn * (TN / 32);
+
+    f32x16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e)
+                acc[i][j][e] = 0.0f;
+
+    u32x4 fa[2][FM], fb[2][FN];
+
+    auto read_frags = [&](int stage, int kk, int buf) {
+        const char *sA = smem + stage * STAGE + a_lane + (((2 * kk) ^ a_x) << 4);
+        const char *sB = smem + stage * STAGE + A_BYTES + kk * 16 * B_ROWB + b_lane;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+            fa[buf][i] = *(const u32x4 *)(sA + i * 32 * A_ROWB);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const char *pb = sB + (((b_blk0 + j) ^ t4) << 6);
+            const v4i16 lo = ds_read_tr16(pb);
+            const v4i16 hi = ds_read_tr16(pb + 4 * B_ROWB);
+            u32x4 v;
+            v.x = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1));
+            v.y = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3));
+            v.z = __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 0, 1));
+            v.w = __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 2, 3));
+            fb[buf][j] = v;
+        }
+    };
+
+    auto mfmas = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                acc[i][j] = mfma32<DT>(fb[buf][j], fa[buf][i], acc[i][j]);
+    };
+
+    // One K step.  LOAD: issue the direct loads of step t + STAGES.  WAIT:
+    // number of this wave's load groups allowed in flight once step t + 1
+    // has landed (-1: step t is the last one, nothing to wait for).
+    auto kstep = [&]<bool LOAD, int WAIT>(int t) {
+        const int stage = t % STAGES;
+        // sub-steps 0 .. KS-2, prefetching the next one's fragments
+#pragma unroll
+        for (int kk = 0; kk < KS - 1; ++kk) {
+            read_frags(stage, kk + 1, (kk + 1) & 1);
+            mfmas(kk & 1);
+        }
+        // stage t fully read by this wave; stage t+1 landed for this wave
+        wait_lgkmcnt0();
+        if constexpr (WAIT >= 0)
+            wait_vmcnt<WAIT * LD>();
+        barrier_only();
+        if constexpr (LOAD)
+            issue_loads(t + STAGES, stage);
+        if constexpr (WAIT >= 0)
+            read_frags((t + 1) % STAGES, 0, 0);
+        mfmas((KS - 1) & 1);
+    };
+
+    // The host launches this kernel only when every split has at least
+    // STAGES K steps.
+    if (nk >= STAGES) {
+        // prologue: fill every stage, wait for stage 0
+#pragma unroll
+        for (int t = 0; t < STAGES; ++t)
+            issue_loads(t, t);
+        wait_vmcnt<(STAGES - 1) * LD>();
+        barrier_only();
+        read_frags(0, 0, 0);
+        // steady state: every step issues the loads of step t + STAGES
+        for (int t = 0; t < nk - STAGES; ++t)
+            kstep.template operator()<true, STAGES - 2>(t);
+        // the last STAGES steps: no more loads, exact waits
+        [&]<int... I>(std::integer_sequence<int, I...>) {
+            (kstep.template operator()<false, (I + 1 < STAGES ? STAGES - 2 - I : -1)>(nk - STAGES + I), ...);
+        }(std::make_integer_sequence<int, STAGES>{});
+    }
+
+    // epilogue (same accumulator layout as gemm_kernel)
+    float *Cb = p.C + (int64_t)ks * p.split_stride;
+    const int64_t ldc = p.ldc;
+    const bool vec_store = p.vec_c && (m0 + BM <= p.M) && (n0 + BN <= p.N);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int row = m0 + wm * TM + i * 32 + l32;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int col = n0 + wn * TN + j * 32 + q * 8 + g * 4;
                 f32x4 v;
                 v.x = acc[i][j][4 * q + 0];
                 v.y = acc[i][j][4 * q + 1];

@@ -124,12 +124,46 @@ hipError_t launch_gemm(int dtype, const GemmParams &p, int grid, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t launch_tile(int tile, int dtype, const GemmParams &p, int grid, hipStream_t s)
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN>
+hipError_t launch_dma(int dtype, const GemmParams &p, int grid, hipStream_t s)
+{
+    if (dtype == XGEMM_BF16)
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 0>), dim3(grid),
+                           dim3(WGM * WGN * 64), 0, s, p);
+    else
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 1>), dim3(grid),
+                           dim3(WGM * WGN * 64), 0, s, p);
+    return hipGetLastError();
+}
+
+// K step and LDS stages of the pipelined (direct-to-LDS) kernels.
+constexpr int kDmaBK = 32;
+constexpr int kDmaStages = 4;
+
+// The pipelined kernels need 16-byte aligned A and B with lda, ldb multiples
+// of 8, N a multiple of 8 (whole 16-byte chunks of B rows), K a multiple of
+// their K step, at least kDmaStages K steps in every split, and per-tile byte
+// offsets that fit in 32 bits.
+bool dma_eligible(const GemmParams &p, int bm)
+{
+    const int64_t last = (int64_t)p.K - (int64_t)(p.split - 1) * p.k_chunk;
+    const int64_t min_steps = (p.k_chunk < last ? p.k_chunk : last) / kDmaBK;
+    return p.vec_ab && p.N % 8 == 0 && p.K % kDmaBK == 0 && min_steps >= kDmaStages &&
+           (int64_t)bm * p.lda * 2 < ((int64_t)1 << 32) && (int64_t)kDmaBK * p.ldb * 2 < ((int64_t)1 << 32);
+}
+
+hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int grid, hipStream_t s)
 {
     switch (tile) {
-    case XGEMM_TILE_256x256: return launch_gemm<256, 256, 64, 2, 2>(dtype, p, grid, s);
-    case XGEMM_TILE_256x128: return launch_gemm<256, 128, 64, 2, 2>(dtype, p, grid, s);
-    case XGEMM_TILE_128x128: return launch_gemm<128, 128, 64, 2, 2>(dtype, p, grid, s);
+    case XGEMM_TILE_256x256:
+        return dma ? launch_dma<256, 256, kDmaBK, kDmaStages, 2, 2>(dtype, p, grid, s)
+                   : launch_gemm<256, 256, 64, 2, 2>(dtype, p, grid, s);
+    case XGEMM_TILE_256x128:
+        return dma ? launch_dma<256, 128, kDmaBK, kDmaStages, 2, 2>(dtype, p, grid, s)
+                   : launch_gemm<256, 128, 64, 2, 2>(dtype, p, grid, s);
+    case XGEMM_TILE_128x128:
+        return dma ? launch_dma<128, 128, kDmaBK, kDmaStages, 2, 2>(dtype, p, grid, s)
+                   : launch_gemm<128, 128, 64, 2, 2>(dtype, p, grid, s);
     default: return hipErrorInvalidValue;
     }
 }
@@ -152,6 +186,69 @@ int check_args(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int
                  span_c = (double)M * (double)ldc;
     if (span_a > 9.0e18 || span_b > 9.0e18 || span_c > 9.0e18)
         return XGEMM_ERR_INVALID_ARG;
+    return XGEMM_OK;
+}
+
+// Everything about a launch that follows from the arguments on the host.
+struct Plan {
+    GemmParams p;
+    int tile;
+    int split;
+    int64_t grid;
+    bool dma;       // pipelined direct-to-LDS kernel (else the general one)
+    size_t ws;      // split-k workspace bytes
+    int64_t ldw;    // workspace row stride (floats)
+};
+
+// Plan a launch for K > 0 and M, N > 0 with configuration cfg.  Device
+// pointers are only inspected for their alignment.
+int make_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+              const float *C, int64_t ldc, const xgemm_config &cfg, Plan *out)
+{
+    const TileShape &t = kTiles[cfg.tile];
+    // drop trailing splits that would have no K range
+    int split = cfg.split_k;
+    int64_t kc = split_chunk(K, split, t.bk);
+    while (split > 1 && kc * (split - 1) >= K) {
+        --split;
+        kc = split_chunk(K, split, t.bk);
+    }
+    const int64_t tiles_m = cdiv(M, t.bm), tiles_n = cdiv(N, t.bn);
+    const int64_t grid = tiles_m * tiles_n * split;
+    if (grid > 0x7fffffff)
+        return XGEMM_ERR_INVALID_ARG;
+
+    GemmParams &p = out->p;
+    p.A = (const uint16_t *)A;
+    p.B = (const uint16_t *)B;
+    p.lda = lda;
+    p.ldb = ldb;
+    p.M = (int)M;
+    p.N = (int)N;
+    p.K = (int)K;
+    p.k_chunk = (int)kc;
+    p.split = split;
+    p.tiles_m = (int)tiles_m;
+    p.tiles_n = (int)tiles_n;
+    p.group_m = cfg.group_m;
+    p.vec_ab = ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 8 == 0) && (ldb % 8 == 0);
+    out->ldw = cdiv(N, 4) * 4;
+    if (split == 1) {
+        p.C = (float *)C;
+        p.ldc = ldc;
+        p.split_stride = 0;
+        p.vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
+    } else {
+        p.C = nullptr;  // the workspace, filled in at launch
+        p.ldc = out->ldw;
+        p.split_stride = M * out->ldw;
+        p.vec_c = 1;
+    }
+    out->tile = cfg.tile;
+    out->split = split;
+    out->grid = grid;
+    out->dma = dma_eligible(p, t.bm);
+    out->ws = workspace_bytes(M, N, split);
     return XGEMM_OK;
 }
 
@@ -185,22 +282,12 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
         cfg = *forced;
     else
         select_config(M, N, K, h->cu_count, &cfg);
-    const TileShape &t = kTiles[cfg.tile];
-    // drop trailing splits that would have no K range
-    int split = cfg.split_k;
-    int64_t kc = split_chunk(K, split, t.bk);
-    while (split > 1 && kc * (split - 1) >= K) {
-        --split;
-        kc = split_chunk(K, split, t.bk);
-    }
+    Plan plan;
+    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, &plan);
+    if (rc != XGEMM_OK)
+        return rc;
 
-    const int64_t tiles_m = cdiv(M, t.bm), tiles_n = cdiv(N, t.bn);
-    const int64_t grid64 = tiles_m * tiles_n * split;
-    if (grid64 > 0x7fffffff)
-        return XGEMM_ERR_INVALID_ARG;
-
-    const size_t ws = workspace_bytes(M, N, split);
-    if (ws > h->ws_bytes) {
+    if (plan.ws > h->ws_bytes) {
         // the old workspace may still be in use by work on this stream
         if (h->workspace) {
             e = hipStreamSynchronize(s);
@@ -212,54 +299,30 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
             h->workspace = nullptr;
             h->ws_bytes = 0;
         }
-        e = hipMalloc(&h->workspace, ws);
+        e = hipMalloc(&h->workspace, plan.ws);
         if (e != hipSuccess) {
             h->workspace = nullptr;
             (void)hipGetLastError();
             set_error(h, "hipMalloc workspace", e);
             return XGEMM_ERR_ALLOC;
         }
-        h->ws_bytes = ws;
+        h->ws_bytes = plan.ws;
     }
+    if (plan.split > 1)
+        plan.p.C = (float *)h->workspace;
 
-    GemmParams p;
-    p.A = (const uint16_t *)A;
-    p.B = (const uint16_t *)B;
-    p.lda = lda;
-    p.ldb = ldb;
-    p.M = (int)M;
-    p.N = (int)N;
-    p.K = (int)K;
-    p.k_chunk = (int)kc;
-    p.split = split;
-    p.tiles_m = (int)tiles_m;
-    p.tiles_n = (int)tiles_n;
-    p.group_m = cfg.group_m;
-    p.vec_ab = ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 8 == 0) && (ldb % 8 == 0);
-    const int64_t ldw = cdiv(N, 4) * 4;
-    if (split == 1) {
-        p.C = C;
-        p.ldc = ldc;
-        p.split_stride = 0;
-        p.vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
-    } else {
-        p.C = (float *)h->workspace;
-        p.ldc = ldw;
-        p.split_stride = M * ldw;
-        p.vec_c = 1;
-    }
-    e = launch_tile(cfg.tile, dtype, p, (int)grid64, s);
+    e = launch_tile(plan.tile, plan.dma, dtype, plan.p, (int)plan.grid, s);
     if (e != hipSuccess) {
         set_error(h, "gemm launch", e);
         return XGEMM_ERR_HIP;
     }
-    if (split > 1) {
+    if (plan.split > 1) {
         const int64_t nvec = M * cdiv(N, 4);
         const int grid = (int)(cdiv(nvec, 256) < 8192 ? cdiv(nvec, 256) : 8192);
         const int vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
         hipLaunchKernelGGL(xgemm_dev::splitk_reduce, dim3(grid), dim3(256), 0, s,
-                           (const float *)h->workspace, (int64_t)(M * ldw), ldw, split, C, ldc,
-                           (int)M, (int)N, vec_c);
+                           (const float *)h->workspace, (int64_t)(M * plan.ldw), plan.ldw, plan.split, C,
+                           ldc, (int)M, (int)N, vec_c);
         e = hipGetLastError();
         if (e != hipSuccess) {
             set_error(h, "split-k reduce launch", e);
@@ -347,6 +410,19 @@ int xgemm_tile_info(int tile, int *bm, int *bn, int *bk, int *threads)
     *bk = kTiles[tile].bk;
     *threads = kTiles[tile].threads;
     return XGEMM_OK;
+}
+
+int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
+                        int64_t ldb, const xgemm_config *cfg)
+{
+    if (!valid_config(cfg) || M <= 0 || N <= 0 || K <= 0 || M >= kMaxDim || N >= kMaxDim || K >= kMaxDim ||
+        lda < K || ldb < N)
+        return -1;
+    Plan plan;
+    // C's alignment does not affect the choice
+    if (make_plan(M, N, K, A, lda, B, ldb, nullptr, N, *cfg, &plan) != XGEMM_OK)
+        return -1;
+    return plan.dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
 }
 
 size_t xgemm_workspace_bytes(int64_t M, int64_t N, const xgemm_config *cfg)

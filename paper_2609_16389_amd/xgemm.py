@@ -30,6 +30,9 @@ XGEMM_TILE_256x128 = 1
 XGEMM_TILE_128x128 = 2
 XGEMM_TILE_COUNT = 3
 
+XGEMM_KERNEL_GENERAL = 0
+XGEMM_KERNEL_PIPELINED = 1
+
 
 class xgemm_config(ctypes.Structure):
     _fields_ = [("tile", ctypes.c_int32), ("split_k", ctypes.c_int32),
@@ -75,6 +78,8 @@ lib.xgemm_select_config.argtypes = [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER
 lib.xgemm_select_config.restype = _i32
 lib.xgemm_tile_info.argtypes = [_i32] + [ctypes.POINTER(ctypes.c_int)] * 4
 lib.xgemm_tile_info.restype = _i32
+lib.xgemm_kernel_family.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, ctypes.POINTER(xgemm_config)]
+lib.xgemm_kernel_family.restype = _i32
 lib.xgemm_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(xgemm_config)]
 lib.xgemm_workspace_bytes.restype = ctypes.c_size_t
 lib.xgemm_strerror.argtypes = [_i32]
@@ -130,6 +135,10 @@ def xgemm_tile_info(tile):
     if rc != XGEMM_OK:
         raise XgemmError(rc)
     return tuple(v.value for v in vals)  # (bm, bn, bk, threads)
+
+
+def xgemm_kernel_family(M, N, K, A, lda, B, ldb, cfg) -> int:
+    return lib.xgemm_kernel_family(M, N, K, A, lda, B, ldb, ctypes.byref(cfg))
 
 
 def xgemm_workspace_bytes(M, N, cfg) -> int:

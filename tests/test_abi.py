@@ -95,3 +95,25 @@ def test_single_hip_runtime_in_process():
             "print(len(libs), libs)\n") % xg._PKG.rsplit("/", 1)[0]
     out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, check=True).stdout
     assert out.startswith("1 "), out
+
+
+def test_kernel_family_rules():
+    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, reserved=0)
+    al = 1 << 20  # a 16-byte aligned stand-in address (only alignment is inspected)
+    fam = lambda M, N, K, a=al, lda=None, b=al, ldb=None, c=cfg: xg.xgemm_kernel_family(
+        M, N, K, a, K if lda is None else lda, b, N if ldb is None else ldb, c)
+    P, G = xg.XGEMM_KERNEL_PIPELINED, xg.XGEMM_KERNEL_GENERAL
+    assert fam(8192, 8192, 8192) == P
+    assert fam(1000, 1000, 1024) == P          # ragged M and N, N % 8 == 0
+    assert fam(1000, 1001, 1024) == G          # N % 8 != 0
+    assert fam(1000, 1000, 1000) == G          # K % 32 != 0
+    assert fam(1000, 1000, 96) == G            # fewer than 4 K steps
+    assert fam(1000, 1000, 1024, a=al + 2) == G  # misaligned A
+    assert fam(1000, 1000, 1024, lda=1028) == G  # lda % 8 != 0
+    assert fam(1000, 1000, 1024, ldb=1004) == G  # ldb % 8 != 0
+    cfg16 = xg.xgemm_config(tile=0, split_k=16, group_m=4, reserved=0)
+    assert fam(1024, 1024, 65536, c=cfg16) == P
+    assert fam(1024, 1024, 1024, c=cfg16) == G   # 64-element splits are too short
+    assert fam(0, 8, 32) == -1
+    bad = xg.xgemm_config(tile=7, split_k=1, group_m=4, reserved=0)
+    assert fam(8, 8, 32, c=bad) == -1

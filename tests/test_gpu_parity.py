@@ -64,13 +64,55 @@ def test_workload_256_fp16_full():
 
 
 # ---------------------------------------------------------------------------
+# the pipelined (direct-to-LDS) kernels: ragged M, N a multiple of 8
+# ---------------------------------------------------------------------------
+
+def _family(M, N, K, cfg):
+    return xg.xgemm_kernel_family(M, N, K, 1 << 20, K, 1 << 20, N, cfg)
+
+
+PIPE_SHAPES = [(256, 256, 128), (1000, 1000, 1024), (255, 264, 512), (777, 136, 4096), (64, 520, 160)]
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("shape", PIPE_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_pipelined_shapes(tile, shape):
+    M, N, K = shape
+    assert _family(M, N, K, config(tile)) == xg.XGEMM_KERNEL_PIPELINED
+    for dtype in ("bf16", "fp16"):
+        A, B, C_ref, S = _case(M, N, K, dtype, seed=M + tile)
+        check_close(run_gpu(A, B, dtype, config=config(tile)), C_ref, S,
+                    "pipelined tile %d %s %s" % (tile, dtype, shape))
+
+
+@pytest.mark.parametrize("split", [1, 2, 4, 8, 16])
+@pytest.mark.parametrize("tile", TILES)
+def test_pipelined_split_k(split, tile):
+    M, N, K = 384, 320, 8192
+    assert _family(M, N, K, config(tile, split)) == xg.XGEMM_KERNEL_PIPELINED
+    A, B, C_ref, S = _case(M, N, K, "bf16", seed=split + 100)
+    check_close(run_gpu(A, B, "bf16", config=config(tile, split)), C_ref, S,
+                "pipelined tile %d split %d" % (tile, split))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_pipelined_integer_bit_exact(dtype):
+    M, N, K = 520, 264, 2048
+    A, B = wl.make_int_inputs(M, N, K, dtype, seed=77)
+    C_ref, _ = oracle.gemm(A, B, dtype)
+    for tile in TILES:
+        assert _family(M, N, K, config(tile)) == xg.XGEMM_KERNEL_PIPELINED
+        check_exact(run_gpu(A, B, dtype, config=config(tile)), C_ref, "pipelined tile %d" % tile)
+
+
+# ---------------------------------------------------------------------------
 # split-k (the paper tries split factors 1, 2, 4, 8, 16)
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("split", [1, 2, 4, 8, 16])
 @pytest.mark.parametrize("tile", TILES)
 def test_split_k_factors(split, tile):
-    M, N, K = 384, 320, 4100  # K not a multiple of the K step
+    M, N, K = 384, 320, 4100  # K not a multiple of 32: the general kernel
     A, B, C_ref, S = _case(M, N, K, "bf16", seed=split)
     check_close(run_gpu(A, B, "bf16", config=config(tile, split)), C_ref, S,
                 "tile %d split %d" % (tile, split))
