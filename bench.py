@@ -11,6 +11,15 @@ mean of the inter-quartile range; Section 6) is reported beside it.
 
 Usage: python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--workload NAME]
        [--no-cpu-baseline] [--no-comparator] [--copy-calibration BYTES]
+       python bench.py --summarize-counters DIR [--workload NAME]   (CPU only)
+
+Counters: run this script under ``rocprofv3 --pmc`` (one pass per counter
+group, with --copy-calibration 1073741824 on the FETCH_SIZE and WRITE_SIZE
+passes), then ``--summarize-counters`` on the output directory writes
+profiles/counters_<workload>.json.  The HBM byte counters are scaled by what
+they read for a plain 1 GiB device copy (known traffic: 1 GiB read, 1 GiB
+written).  The bench line reports the summary while the kernel sources still
+hash to the value recorded in it.
 """
 from __future__ import annotations
 
@@ -53,6 +62,64 @@ def stored_traffic(workload: str):
     return d.get("hbm_bytes_per_launch")
 
 
+def stored_counters(workload: str):
+    path = COUNTERS_FILE % workload
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return d
+
+
+def summarize_counters(directory: str, workload: str) -> str:
+    """rocprofv3 --pmc CSV output -> profiles/counters_<workload>.json."""
+    import csv
+    import statistics
+    vals, names, durs = {}, {}, {}
+    for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                k = r["Kernel_Name"]
+                vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                durs.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    gemm = [k for k in vals if "gemm_kernel" in k]
+    copy = [k for k in vals if "copyBuffer" in k or "copy_kernel" in k]
+    if not gemm:
+        raise SystemExit("no GEMM kernel in %s" % directory)
+    k = max(gemm, key=lambda n: len(durs[n]))
+    med = {c: statistics.median(v) for c, v in vals[k].items()}
+    out = {"kernel": k, "workload": workload, "kernel_source_sha256": kernel_source_hash(),
+           "dispatches": len(durs[k]) // max(1, len(vals[k])), "median_duration_ns": statistics.median(durs[k]),
+           "counters_median": med}
+    fetch_scale = write_scale = None
+    if copy:
+        cm = {c: statistics.median(v) for c, v in vals[copy[0]].items()}
+        gib_kib = 1024.0 * 1024.0
+        if cm.get("FETCH_SIZE"):
+            fetch_scale = gib_kib / cm["FETCH_SIZE"]
+        if cm.get("WRITE_SIZE"):
+            write_scale = gib_kib / cm["WRITE_SIZE"]
+        out["copy_calibration"] = {"kernel": copy[0], "bytes": 1 << 30, "counters_median": cm,
+                                   "fetch_scale": fetch_scale, "write_scale": write_scale}
+    if fetch_scale and write_scale and "FETCH_SIZE" in med and "WRITE_SIZE" in med:
+        out["hbm_bytes_per_launch"] = 1024.0 * (med["FETCH_SIZE"] * fetch_scale + med["WRITE_SIZE"] * write_scale)
+        out["hbm_read_bytes_per_launch"] = 1024.0 * med["FETCH_SIZE"] * fetch_scale
+        out["hbm_write_bytes_per_launch"] = 1024.0 * med["WRITE_SIZE"] * write_scale
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in med and "GRBM_GUI_ACTIVE" in med:
+        # GRBM_GUI_ACTIVE is summed over the 8 XCDs; 1024 SIMDs in all
+        per_xcd = med["GRBM_GUI_ACTIVE"] / 8.0
+        out["mfma_busy_pct"] = 100.0 * med["SQ_VALU_MFMA_BUSY_CYCLES"] / (per_xcd * 1024.0)
+        out["clock_ghz"] = per_xcd / out["median_duration_ns"]
+    if "SQ_LDS_BANK_CONFLICT" in med and "SQ_LDS_IDX_ACTIVE" in med:
+        out["lds_bank_conflict_pct"] = 100.0 * med["SQ_LDS_BANK_CONFLICT"] / max(1.0, med["SQ_LDS_IDX_ACTIVE"])
+    path = COUNTERS_FILE % workload
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+    return path
+
+
 def cpu_baseline(w, A, B, budget_s: float = 12.0):
     """The oracle, untuned, on a bounded sample: the first R rows of C."""
     import oracle
@@ -85,7 +152,13 @@ def main():
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="also run a plain device copy of this many bytes (counter calibration)")
+    ap.add_argument("--summarize-counters", metavar="DIR", default=None,
+                    help="write profiles/counters_<workload>.json from rocprofv3 --pmc output and exit")
     args = ap.parse_args()
+
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters, args.workload))
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this GEMM is not sharded across GPUs "
@@ -170,6 +243,7 @@ def main():
         comparator = {"name": "torch.matmul (hipBLASLt), 16-bit output", "tflops": round(flops / t / 1e12, 1)}
 
     traffic = stored_traffic(w.name)
+    counters = stored_counters(w.name)
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -192,6 +266,9 @@ def main():
                      "frac": round(achieved / peak, 4),
                      "traffic": traffic},
         "comparator": comparator,
+        "counters": None if counters is None else {
+            k: counters.get(k) for k in ("mfma_busy_pct", "clock_ghz", "lds_bank_conflict_pct",
+                                         "hbm_read_bytes_per_launch", "hbm_write_bytes_per_launch")},
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

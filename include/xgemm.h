@@ -146,7 +146,7 @@ enum xgemm_kernel_family_id {
  * Which kernel family xgemm_run_config would launch for these arguments
  * (host-only; A and B are only inspected for their alignment).  The
  * pipelined family needs A and B 16-byte aligned, lda and ldb multiples of
- * 8, N a multiple of 8, K a multiple of 32 and at least 128 K values in
+ * 8, N a multiple of 8, K a multiple of 64 and at least 192 K values in
  * every split; everything else runs on the general family.  Returns -1 for
  * M, N or K <= 0, leading dimensions too small, or an invalid cfg.
  */

@@ -346,8 +346,8 @@ gemm_kernel(GemmParams p)
 // flight at once.  Fragments:
 //   A  (BM x BK, k contiguous, rows of BK*2 bytes): ds_read_b128 of 8
 //      consecutive k of one row; 16-byte chunk c of row r is stored at slot
-//      c ^ ((r >> 2) & 3), so 16 consecutive rows read at one logical chunk
-//      cover all 16 slots of a 256-byte bank window;
+//      c ^ aswz(r) (see aswz), so 16 consecutive rows read at one logical
+//      chunk cover all 16 slots of a 256-byte bank window;
 //   B  (BK x BN, n contiguous as in memory, rows of BN*2 bytes):
 //      ds_read_b64_tr_b16 -- within each group of 16 lanes, lane i receives
 //      element (i % 4) of the 8 bytes addressed by lane 4e + i / 4 as its
@@ -411,6 +411,21 @@ __device__ __forceinline__ void barrier_only()
     asm volatile("" ::: "memory");
 }
 
+// Fence for the compiler's instruction scheduler: nothing moves across it,
+// so the code order between fences is the issue order.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Chunk swizzle of the A tile for rows of ROWB bytes (4 or 8 chunks): with
+// 64-byte rows, four rows share a 256-byte bank window and rows r, r+4,
+// r+8, r+12 get distinct slots; with 128-byte rows, two rows share a window
+// and rows of one parity within 16 get distinct slots.
+template <int ROWB>
+__device__ __forceinline__ int aswz(int r)
+{
+    static_assert(ROWB == 64 || ROWB == 128, "A row size");
+    return ROWB == 64 ? ((r >> 2) & 3) : ((r >> 1) & 7);
+}
+
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT>
 __global__ void __launch_bounds__(WGM * WGN * 64, 1)
 gemm_kernel_dma(GemmParams p)
@@ -429,7 +444,7 @@ gemm_kernel_dma(GemmParams p)
     constexpr int LD = A_LD + B_LD;
     constexpr int A_ROWS_PER_LD = 1024 / A_ROWB; // tile rows one load instruction fills
     constexpr int B_ROWS_PER_LD = 1024 / B_ROWB;
-    static_assert(BK == 32, "A layout assumes 64-byte rows");
+    static_assert(BK == 32 || BK == 64, "A rows of 64 or 128 bytes");
     static_assert(BN % 32 == 0 && B_ROWB <= 1024 && 1024 % B_ROWB == 0, "B layout");
     static_assert(A_LD * NW * 1024 == A_BYTES && B_LD * NW * 1024 == B_BYTES, "load split");
     static_assert(KS >= 2 && STAGES >= 2 && STAGES * STAGE <= 160 * 1024, "pipeline shape");
@@ -456,8 +471,8 @@ gemm_kernel_dma(GemmParams p)
     const int nmax = ((p.N - 1) / 8) * 8 - n0;   // last valid 8-column chunk
 #pragma unroll
     for (int j = 0; j < A_LD; ++j) {
-        const int r = (wave * A_LD + j) * A_ROWS_PER_LD + lane / 4;
-        const int c = (lane & 3) ^ ((r >> 2) & 3);
+        const int r = (wave * A_LD + j) * A_ROWS_PER_LD + lane / (A_ROWB / 16);
+        const int c = (lane % (A_ROWB / 16)) ^ aswz<A_ROWB>(r);
         a_goff[j] = (uint32_t)((min(r, mmax) * lda + c * 8) * 2);
     }
 #pragma unroll
@@ -487,7 +502,7 @@ gemm_kernel_dma(GemmParams p)
     const int l32 = lane & 31;
     const int g = lane >> 5;                      // k half of the MFMA operand
     // A: row wm*TM + i*32 + l32, logical chunk 2*kk + g
-    const int a_x = g ^ ((l32 >> 2) & 3);
+    const int a_x = g ^ aswz<A_ROWB>(l32);
     const int a_lane = (wm * TM + l32) * A_ROWB;
     // B: rows kk*16 + 8g + 4c + s/4, columns wn*TN + j*32 + 16h + 4(s%4)
     const int s16 = lane & 15;
@@ -507,32 +522,46 @@ gemm_kernel_dma(GemmParams p)
 
     u32x4 fa[2][FM], fb[2][FN];
 
-    auto read_frags = [&](int stage, int kk, int buf) {
+    auto read_A = [&](int stage, int kk, int buf, int i) {
         const char *sA = smem + stage * STAGE + a_lane + (((2 * kk) ^ a_x) << 4);
-        const char *sB = smem + stage * STAGE + A_BYTES + kk * 16 * B_ROWB + b_lane;
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-            fa[buf][i] = *(const u32x4 *)(sA + i * 32 * A_ROWB);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const char *pb = sB + (((b_blk0 + j) ^ t4) << 6);
-            const v4i16 lo = ds_read_tr16(pb);
-            const v4i16 hi = ds_read_tr16(pb + 4 * B_ROWB);
-            u32x4 v;
-            v.x = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1));
-            v.y = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3));
-            v.z = __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 0, 1));
-            v.w = __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 2, 3));
-            fb[buf][j] = v;
-        }
+        fa[buf][i] = *(const u32x4 *)(sA + i * 32 * A_ROWB);
     };
-
-    auto mfmas = [&](int buf) {
+    auto read_B = [&](int stage, int kk, int buf, int j) {
+        const char *pb = smem + stage * STAGE + A_BYTES + kk * 16 * B_ROWB + b_lane +
+                         (((b_blk0 + j) ^ t4) << 6);
+        const v4i16 lo = ds_read_tr16(pb);
+        const v4i16 hi = ds_read_tr16(pb + 4 * B_ROWB);
+        u32x4 v;
+        v.x = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1));
+        v.y = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3));
+        v.z = __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 0, 1));
+        v.w = __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 2, 3));
+        fb[buf][j] = v;
+    };
+    // The fragment reads of one sub-step as FM + FN units in the order the
+    // MFMAs below first need them: A0, B0 .. B(FN-1), A1 .. A(FM-1).
+    constexpr int NU = FM + FN;
+#ifndef XGEMM_READ_UNITS_PER_MFMA
+#define XGEMM_READ_UNITS_PER_MFMA 1
+#endif
+    constexpr int RPM = XGEMM_READ_UNITS_PER_MFMA;  // read units issued after each MFMA
+    auto read_unit = [&](int stage, int kk, int buf, int u) {
+        if (u == 0)
+            read_A(stage, kk, buf, 0);
+        else if (u <= FN)
+            read_B(stage, kk, buf, u - 1);
+        else
+            read_A(stage, kk, buf, u - FN);
+    };
+    auto read_frags = [&](int stage, int kk, int buf) {
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-            for (int j = 0; j < FN; ++j)
-                acc[i][j] = mfma32<DT>(fb[buf][j], fa[buf][i], acc[i][j]);
+        for (int u = 0; u < NU; ++u)
+            read_unit(stage, kk, buf, u);
+    };
+    // MFMA n of a sub-step, row-major over the (i, j) blocks.
+    auto mfma_n = [&](int buf, int n) {
+        const int i = n / FN, j = n % FN;
+        acc[i][j] = mfma32<DT>(fb[buf][j], fa[buf][i], acc[i][j]);
     };
 
     // One K step.  LOAD: issue the direct loads of step t + STAGES.  WAIT:
@@ -540,22 +569,57 @@ gemm_kernel_dma(GemmParams p)
     // has landed (-1: step t is the last one, nothing to wait for).
     auto kstep = [&]<bool LOAD, int WAIT>(int t) {
         const int stage = t % STAGES;
-        // sub-steps 0 .. KS-2, prefetching the next one's fragments
+        // sub-steps 0 .. KS-2: MFMAs of kk, each followed by one read unit of
+        // kk+1, in this order
 #pragma unroll
         for (int kk = 0; kk < KS - 1; ++kk) {
-            read_frags(stage, kk + 1, (kk + 1) & 1);
-            mfmas(kk & 1);
+#pragma unroll
+            for (int n = 0; n < FM * FN; ++n) {
+                mfma_n(kk & 1, n);
+#pragma unroll
+                for (int q = 0; q < RPM; ++q)
+                    if (n * RPM + q < NU)
+                        read_unit(stage, kk + 1, (kk + 1) & 1, n * RPM + q);
+                sched_fence();
+            }
         }
         // stage t fully read by this wave; stage t+1 landed for this wave
         wait_lgkmcnt0();
         if constexpr (WAIT >= 0)
             wait_vmcnt<WAIT * LD>();
         barrier_only();
-        if constexpr (LOAD)
-            issue_loads(t + STAGES, stage);
-        if constexpr (WAIT >= 0)
-            read_frags((t + 1) % STAGES, 0, 0);
-        mfmas((KS - 1) & 1);
+        sched_fence();
+        // last sub-step: its MFMAs, with the direct loads of step t+STAGES
+        // into the freed stage and the reads of step t+1's first sub-step
+        const int next = (t + 1) % STAGES;
+        const int k0 = kbeg + (t + STAGES) * BK;
+        const uint16_t *Ab = p.A + (int64_t)m0 * lda + k0;
+        const uint16_t *Bb = p.B + (int64_t)k0 * ldb + n0;
+        const uint32_t sA = lds_address(smem) + stage * STAGE;
+        const uint32_t sB = sA + A_BYTES;
+#pragma unroll
+        for (int n = 0; n < FM * FN; ++n) {
+            mfma_n((KS - 1) & 1, n);
+            if constexpr (WAIT >= 0) {
+#pragma unroll
+                for (int q = 0; q < RPM; ++q)
+                    if (n * RPM + q < NU)
+                        read_unit(next, 0, 0, n * RPM + q);
+            }
+            if constexpr (LOAD) {
+                // spread the LD loads over the MFMAs
+                constexpr int per = (LD + FM * FN - 1) / (FM * FN);
+#pragma unroll
+                for (int q = 0; q < per; ++q) {
+                    const int j = n * per + q;
+                    if (j < A_LD)
+                        lds_load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
+                    else if (j < LD)
+                        lds_load16(Bb, b_goff[j - A_LD], sB + (wave * B_LD + (j - A_LD)) * 1024);
+                }
+            }
+            sched_fence();
+        }
     };
 
     // The host launches this kernel only when every split has at least

@@ -136,19 +136,22 @@ hipError_t launch_dma(int dtype, const GemmParams &p, int grid, hipStream_t s)
     return hipGetLastError();
 }
 
-// K step and LDS stages of the pipelined (direct-to-LDS) kernels.
-constexpr int kDmaBK = 32;
-constexpr int kDmaStages = 4;
+// K step of the pipelined (direct-to-LDS) kernels; LDS stages per tile.
+constexpr int kDmaBK = 64;
+constexpr int kDmaStages256x256 = 2;  // 2 x 64 KiB
+constexpr int kDmaStages256x128 = 3;  // 3 x 48 KiB
+constexpr int kDmaStages128x128 = 2;  // 2 x 32 KiB, two workgroups per CU
+constexpr int kDmaMinStages = 3;
 
 // The pipelined kernels need 16-byte aligned A and B with lda, ldb multiples
 // of 8, N a multiple of 8 (whole 16-byte chunks of B rows), K a multiple of
-// their K step, at least kDmaStages K steps in every split, and per-tile byte
-// offsets that fit in 32 bits.
+// their K step, at least as many K steps in every split as the deepest
+// pipeline has stages, and per-tile byte offsets that fit in 32 bits.
 bool dma_eligible(const GemmParams &p, int bm)
 {
     const int64_t last = (int64_t)p.K - (int64_t)(p.split - 1) * p.k_chunk;
     const int64_t min_steps = (p.k_chunk < last ? p.k_chunk : last) / kDmaBK;
-    return p.vec_ab && p.N % 8 == 0 && p.K % kDmaBK == 0 && min_steps >= kDmaStages &&
+    return p.vec_ab && p.N % 8 == 0 && p.K % kDmaBK == 0 && min_steps >= kDmaMinStages &&
            (int64_t)bm * p.lda * 2 < ((int64_t)1 << 32) && (int64_t)kDmaBK * p.ldb * 2 < ((int64_t)1 << 32);
 }
 
@@ -156,13 +159,13 @@ hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int g
 {
     switch (tile) {
     case XGEMM_TILE_256x256:
-        return dma ? launch_dma<256, 256, kDmaBK, kDmaStages, 2, 2>(dtype, p, grid, s)
+        return dma ? launch_dma<256, 256, kDmaBK, kDmaStages256x256, 2, 2>(dtype, p, grid, s)
                    : launch_gemm<256, 256, 64, 2, 2>(dtype, p, grid, s);
     case XGEMM_TILE_256x128:
-        return dma ? launch_dma<256, 128, kDmaBK, kDmaStages, 2, 2>(dtype, p, grid, s)
+        return dma ? launch_dma<256, 128, kDmaBK, kDmaStages256x128, 2, 2>(dtype, p, grid, s)
                    : launch_gemm<256, 128, 64, 2, 2>(dtype, p, grid, s);
     case XGEMM_TILE_128x128:
-        return dma ? launch_dma<128, 128, kDmaBK, kDmaStages, 2, 2>(dtype, p, grid, s)
+        return dma ? launch_dma<128, 128, kDmaBK, kDmaStages128x128, 2, 2>(dtype, p, grid, s)
                    : launch_gemm<128, 128, 64, 2, 2>(dtype, p, grid, s);
     default: return hipErrorInvalidValue;
     }

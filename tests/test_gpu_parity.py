@@ -71,7 +71,7 @@ def _family(M, N, K, cfg):
     return xg.xgemm_kernel_family(M, N, K, 1 << 20, K, 1 << 20, N, cfg)
 
 
-PIPE_SHAPES = [(256, 256, 128), (1000, 1000, 1024), (255, 264, 512), (777, 136, 4096), (64, 520, 160)]
+PIPE_SHAPES = [(256, 256, 192), (1000, 1000, 1024), (255, 264, 512), (777, 136, 4096), (64, 520, 320)]
 
 
 @pytest.mark.parametrize("tile", TILES)
