@@ -564,13 +564,41 @@ gemm_kernel_dma(GemmParams p)
         acc[i][j] = mfma32<DT>(fb[buf][j], fa[buf][i], acc[i][j]);
     };
 
-    // One K step.  LOAD: issue the direct loads of step t + STAGES.  WAIT:
-    // number of this wave's load groups allowed in flight once step t + 1
-    // has landed (-1: step t is the last one, nothing to wait for).
-    auto kstep = [&]<bool LOAD, int WAIT>(int t) {
+    // Direct load j (0 .. LD-1) of K step u into LDS stage `stage`.
+    auto load_j = [&](int u, int stage, int j) {
+        const int k0 = kbeg + u * BK;
+        const uint32_t sA = lds_address(smem) + stage * STAGE;
+        if (j < A_LD) {
+            const uint16_t *Ab = p.A + (int64_t)m0 * lda + k0;
+            lds_load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
+        } else {
+            const uint16_t *Bb = p.B + (int64_t)k0 * ldb + n0;
+            lds_load16(Bb, b_goff[j - A_LD], sA + A_BYTES + (wave * B_LD + (j - A_LD)) * 1024);
+        }
+    };
+    // With three or more stages the loads of one K step are issued in two
+    // halves: the first after the barrier that frees their stage, the
+    // second during the next step's sub-steps before its barrier.  This
+    // spaces the direct loads one per few MFMAs (a burst of them fills the
+    // vector-memory queue and blocks the wave's MFMA issue) while each load
+    // still has about STAGES-2 K steps to land.  With two stages every load
+    // must be issued right after the barrier.
+    constexpr bool SPLIT = STAGES >= 3;
+    constexpr int H1 = SPLIT ? (LD + 1) / 2 : LD;   // loads issued after the barrier
+    constexpr int H2 = LD - H1;                      // loads issued before the next barrier
+    constexpr int STEP1 = H1 > 0 ? (FM * FN) / H1 > 0 ? (FM * FN) / H1 : 1 : 1;
+    constexpr int STEP2 = H2 > 0 ? ((KS - 1) * FM * FN) / H2 > 0 ? ((KS - 1) * FM * FN) / H2 : 1 : 1;
+
+    // One K step t.  LOAD1: issue the first half of step t+STAGES's loads
+    // (into stage t, freed by this step's barrier).  LOAD2: issue the second
+    // half of step t-1+STAGES's loads (into stage t-1).  WAIT: number of this
+    // wave's load groups allowed in flight once step t+1 has landed (-1: t
+    // is the last step).
+    auto kstep = [&]<bool LOAD1, bool LOAD2, int WAIT>(int t) {
         const int stage = t % STAGES;
+        const int prev = (t + STAGES - 1) % STAGES;
         // sub-steps 0 .. KS-2: MFMAs of kk, each followed by one read unit of
-        // kk+1, in this order
+        // kk+1 (and, spread out, the second-half loads), in this order
 #pragma unroll
         for (int kk = 0; kk < KS - 1; ++kk) {
 #pragma unroll
@@ -580,6 +608,11 @@ gemm_kernel_dma(GemmParams p)
                 for (int q = 0; q < RPM; ++q)
                     if (n * RPM + q < NU)
                         read_unit(stage, kk + 1, (kk + 1) & 1, n * RPM + q);
+                if constexpr (LOAD2) {
+                    const int gi = kk * FM * FN + n;
+                    if (gi % STEP2 == 0 && gi / STEP2 < H2)
+                        load_j(t - 1 + STAGES, prev, H1 + gi / STEP2);
+                }
                 sched_fence();
             }
         }
@@ -589,14 +622,10 @@ gemm_kernel_dma(GemmParams p)
             wait_vmcnt<WAIT * LD>();
         barrier_only();
         sched_fence();
-        // last sub-step: its MFMAs, with the direct loads of step t+STAGES
-        // into the freed stage and the reads of step t+1's first sub-step
+        // last sub-step: its MFMAs, with the first-half loads of step
+        // t+STAGES into the freed stage and the reads of step t+1's first
+        // sub-step
         const int next = (t + 1) % STAGES;
-        const int k0 = kbeg + (t + STAGES) * BK;
-        const uint16_t *Ab = p.A + (int64_t)m0 * lda + k0;
-        const uint16_t *Bb = p.B + (int64_t)k0 * ldb + n0;
-        const uint32_t sA = lds_address(smem) + stage * STAGE;
-        const uint32_t sB = sA + A_BYTES;
 #pragma unroll
         for (int n = 0; n < FM * FN; ++n) {
             mfma_n((KS - 1) & 1, n);
@@ -606,16 +635,12 @@ gemm_kernel_dma(GemmParams p)
                     if (n * RPM + q < NU)
                         read_unit(next, 0, 0, n * RPM + q);
             }
-            if constexpr (LOAD) {
-                // spread the LD loads over the MFMAs
-                constexpr int per = (LD + FM * FN - 1) / (FM * FN);
+            if constexpr (LOAD1) {
 #pragma unroll
-                for (int q = 0; q < per; ++q) {
-                    const int j = n * per + q;
-                    if (j < A_LD)
-                        lds_load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
-                    else if (j < LD)
-                        lds_load16(Bb, b_goff[j - A_LD], sB + (wave * B_LD + (j - A_LD)) * 1024);
+                for (int q = 0; q < (H1 + FM * FN - 1) / (FM * FN); ++q) {
+                    const int j = (H1 <= FM * FN) ? (n % STEP1 == 0 ? n / STEP1 : H1) : n * ((H1 + FM * FN - 1) / (FM * FN)) + q;
+                    if (j < H1)
+                        load_j(t + STAGES, stage, j);
                 }
             }
             sched_fence();
@@ -632,13 +657,23 @@ gemm_kernel_dma(GemmParams p)
         wait_vmcnt<(STAGES - 1) * LD>();
         barrier_only();
         read_frags(0, 0, 0);
-        // steady state: every step issues the loads of step t + STAGES
-        for (int t = 0; t < nk - STAGES; ++t)
-            kstep.template operator()<true, STAGES - 2>(t);
-        // the last STAGES steps: no more loads, exact waits
-        [&]<int... I>(std::integer_sequence<int, I...>) {
-            (kstep.template operator()<false, (I + 1 < STAGES ? STAGES - 2 - I : -1)>(nk - STAGES + I), ...);
-        }(std::make_integer_sequence<int, STAGES>{});
+        if (nk > STAGES) {
+            // step 0: the prologue issued all of step STAGES-1's loads
+            kstep.template operator()<true, false, STAGES - 2>(0);
+            // steady state
+            for (int t = 1; t < nk - STAGES; ++t)
+                kstep.template operator()<true, SPLIT, STAGES - 2>(t);
+            // the last STAGES steps: no more first halves, exact waits
+            kstep.template operator()<false, SPLIT, STAGES - 2>(nk - STAGES);
+            [&]<int... I>(std::integer_sequence<int, I...>) {
+                (kstep.template operator()<false, false, (I + 2 < STAGES ? STAGES - 3 - I : -1)>(nk - STAGES + 1 + I),
+                 ...);
+            }(std::make_integer_sequence<int, STAGES - 1>{});
+        } else {
+            [&]<int... I>(std::integer_sequence<int, I...>) {
+                (kstep.template operator()<false, false, (I + 1 < STAGES ? STAGES - 2 - I : -1)>(I), ...);
+            }(std::make_integer_sequence<int, STAGES>{});
+        }
     }
 
     // epilogue (same accumulator layout as gemm_kernel)
