@@ -65,10 +65,12 @@ enum xgemm_tile {
  * device's compute-unit count, and xgemm_run_config lets a caller force one.
  */
 typedef struct xgemm_config {
-    int32_t tile;    /* an xgemm_tile value */
-    int32_t split_k; /* number of K partitions, 1 .. 64; > 1 uses the workspace */
-    int32_t group_m; /* tile rows per group in the launch order, 1 .. 64 (L2 locality) */
-    int32_t reserved; /* must be 0 */
+    int32_t tile;       /* an xgemm_tile value */
+    int32_t split_k;    /* number of K partitions, 1 .. 64; > 1 uses the workspace */
+    int32_t group_m;    /* tile rows per group in the launch order, 1 .. 64 (L2 locality) */
+    int32_t tail_split; /* 0 or 1: off; 2 .. 64 (only with split_k == 1): the output tiles past
+                           the last full wave of workgroups run as a second launch with this
+                           split-k factor, their partials going through the workspace */
 } xgemm_config;
 
 /*
@@ -111,8 +113,8 @@ int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
 
 /*
  * As xgemm_run, with the launch configuration forced to *cfg (validated:
- * XGEMM_ERR_INVALID_ARG for an unknown tile, a split_k or group_m out of
- * range, or a non-zero reserved field).  Results agree with xgemm_run within
+ * XGEMM_ERR_INVALID_ARG for an unknown tile, split_k, group_m or tail_split
+ * out of range, or tail_split > 1 together with split_k > 1).  Results agree with xgemm_run within
  * the accuracy contract; only the summation grouping differs.
  */
 int xgemm_run_config(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
@@ -154,10 +156,12 @@ int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t 
                         const void *B, int64_t ldb, const xgemm_config *cfg);
 
 /*
- * Bytes of split-k workspace a configuration needs for an M x N output
- * (0 when split_k == 1).  Host-only.  Returns 0 for invalid arguments.
+ * Bytes of workspace xgemm_run_config needs for this problem and cfg on a
+ * device with cu_count compute units: split_k * M * ceil(N/4)*4 floats when
+ * split_k > 1, the tail tiles' partials when tail_split > 1 applies, else 0.
+ * Host-only.  Returns 0 for invalid arguments.
  */
-size_t xgemm_workspace_bytes(int64_t M, int64_t N, const xgemm_config *cfg);
+size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, const xgemm_config *cfg);
 
 /* Static description of a status code; never NULL. */
 const char *xgemm_strerror(int status);

@@ -49,6 +49,9 @@ struct GemmParams {
     int group_m;
     int vec_ab;             // A, B 16-byte aligned, lda and ldb multiples of 8
     int vec_c;              // output 16-byte aligned, ldc a multiple of 4
+    int tile_base;          // this launch covers logical tiles [tile_base, tile_base + tile_count)
+    int tile_count;
+    int tile_major;         // 1: write each (split, tile) partial as a dense BM x BN block of C
 };
 
 template <int DT>
@@ -73,29 +76,67 @@ __device__ __forceinline__ f32x16 mfma32<1>(u32x4 a, u32x4 b, f32x16 c)
 // slot) pair among 16 consecutive rows.
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
-// Workgroup -> (tile_m, tile_n, split).  The hardware hands workgroup ids to
-// the XCDs round-robin; consecutive logical ids are first gathered onto one
-// XCD, then walked in groups of group_m tile rows so that the workgroups an
-// XCD runs at the same time share rows of A and columns of B in its L2.  The
-// split index is outermost: workgroups of one K range run together.
-// (The paper's persistent kernels hand out tasks in lexicographic order and
-// leave other orders to future work, Section 4.2.)
-__device__ __forceinline__ void map_tile(const GemmParams &p, int &tm, int &tn, int &ks)
+// Logical tile id -> (tile_m, tile_n): tiles are walked in groups of
+// group_m tile rows, column by column within a group, so that consecutive
+// ids share rows of A and columns of B.  Shared by the GEMM kernels and the
+// tile reduction, which must agree on it.
+__host__ __device__ __forceinline__ void logical_tile(int t, int tiles_m, int tiles_n, int group_m, int &tm,
+                                                      int &tn)
+{
+    const int group = group_m * tiles_n;
+    const int g = t / group;
+    const int first_m = g * group_m;
+    const int gm = min(tiles_m - first_m, group_m);
+    const int r = t - g * group;
+    tm = first_m + r % gm;
+    tn = r / gm;
+}
+
+// Workgroup -> (tile_m, tile_n, split, local tile index).  The hardware
+// hands workgroup ids to the XCDs round-robin; consecutive logical ids are
+// first gathered onto one XCD, so that the workgroups an XCD runs at the
+// same time are neighbours in the grouped tile order and share rows of A
+// and columns of B in its L2.  The split index is outermost: workgroups of
+// one K range run together.  (The paper's persistent kernels hand out tasks
+// in lexicographic order and leave other orders to future work, Section
+// 4.2.)
+__device__ __forceinline__ void map_tile(const GemmParams &p, int &tm, int &tn, int &ks, int &local)
 {
     const int total = gridDim.x;
     const int w = blockIdx.x;
     const int per = total / kNumXcd;
     const int lid = (w < per * kNumXcd) ? (w % kNumXcd) * per + w / kNumXcd : w;
-    const int tiles = p.tiles_m * p.tiles_n;
-    ks = lid / tiles;
-    const int t = lid - ks * tiles;
-    const int group = p.group_m * p.tiles_n;
-    const int g = t / group;
-    const int first_m = g * p.group_m;
-    const int gm = min(p.tiles_m - first_m, p.group_m);
-    const int r = t - g * group;
-    tm = first_m + r % gm;
-    tn = r / gm;
+    ks = lid / p.tile_count;
+    local = lid - ks * p.tile_count;
+    logical_tile(p.tile_base + local, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
+}
+
+// Output placement: row-major C (or a full-matrix split partial) at
+// out + row * ldc + col, or, for tile-major partials, the dense BM x BN
+// block of (split, local tile) with row and column taken relative to the
+// tile origin.
+struct OutView {
+    float *base;
+    int64_t ld;
+    int r0, c0;
+};
+
+template <int BM, int BN>
+__device__ __forceinline__ OutView out_view(const GemmParams &p, int ks, int local, int m0, int n0)
+{
+    OutView o;
+    if (p.tile_major) {
+        o.base = p.C + ((int64_t)ks * p.tile_count + local) * (int64_t)(BM * BN);
+        o.ld = BN;
+        o.r0 = m0;
+        o.c0 = n0;
+    } else {
+        o.base = p.C + (int64_t)ks * p.split_stride;
+        o.ld = p.ldc;
+        o.r0 = 0;
+        o.c0 = 0;
+    }
+    return o;
 }
 
 // Eight 16-bit values starting at base[off], the first `cnt` of them read
@@ -156,8 +197,8 @@ gemm_kernel(GemmParams p)
 
     __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
 
-    int tm, tn, ks;
-    map_tile(p, tm, tn, ks);
+    int tm, tn, ks, local;
+    map_tile(p, tm, tn, ks, local);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = ks * p.k_chunk;
     const int kend = min(p.K, kbeg + p.k_chunk);
@@ -308,9 +349,10 @@ gemm_kernel(GemmParams p)
 
     // Epilogue: lane l holds rows (l % 32) of each 32 x 32 block and, in
     // register quad q, columns 8q + 4(l / 32) .. +3.
-    float *Cb = p.C + (int64_t)ks * p.split_stride;
-    const int64_t ldc = p.ldc;
-    const bool vec_store = p.vec_c && interior;
+    const OutView ov = out_view<BM, BN>(p, ks, local, m0, n0);
+    float *Cb = ov.base;
+    const int64_t ldc = ov.ld;
+    const bool vec_store = p.tile_major || (p.vec_c && interior);
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int row = m0 + wm * TM + i * 32 + l32;
@@ -325,12 +367,12 @@ gemm_kernel(GemmParams p)
                 v.z = acc[i][j][4 * q + 2];
                 v.w = acc[i][j][4 * q + 3];
                 if (vec_store) {
-                    *(f32x4 *)(Cb + (int64_t)row * ldc + col) = v;
+                    *(f32x4 *)(Cb + (int64_t)(row - ov.r0) * ldc + (col - ov.c0)) = v;
                 } else if (row < p.M) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         if (col + e < p.N)
-                            Cb[(int64_t)row * ldc + col + e] = v[e];
+                            Cb[(int64_t)(row - ov.r0) * ldc + (col - ov.c0) + e] = v[e];
                 }
             }
         }
@@ -452,8 +494,8 @@ gemm_kernel_dma(GemmParams p)
 
     __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
-    int tm, tn, ks;
-    map_tile(p, tm, tn, ks);
+    int tm, tn, ks, local;
+    map_tile(p, tm, tn, ks, local);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = ks * p.k_chunk;
     const int kend = min(p.K, kbeg + p.k_chunk);
@@ -677,9 +719,10 @@ gemm_kernel_dma(GemmParams p)
     }
 
     // epilogue (same accumulator layout as gemm_kernel)
-    float *Cb = p.C + (int64_t)ks * p.split_stride;
-    const int64_t ldc = p.ldc;
-    const bool vec_store = p.vec_c && (m0 + BM <= p.M) && (n0 + BN <= p.N);
+    const OutView ov = out_view<BM, BN>(p, ks, local, m0, n0);
+    float *Cb = ov.base;
+    const int64_t ldc = ov.ld;
+    const bool vec_store = p.tile_major || (p.vec_c && (m0 + BM <= p.M) && (n0 + BN <= p.N));
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int row = m0 + wm * TM + i * 32 + l32;
@@ -694,12 +737,12 @@ gemm_kernel_dma(GemmParams p)
                 v.z = acc[i][j][4 * q + 2];
                 v.w = acc[i][j][4 * q + 3];
                 if (vec_store) {
-                    *(f32x4 *)(Cb + (int64_t)row * ldc + col) = v;
+                    *(f32x4 *)(Cb + (int64_t)(row - ov.r0) * ldc + (col - ov.c0)) = v;
                 } else if (row < p.M) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         if (col + e < p.N)
-                            Cb[(int64_t)row * ldc + col + e] = v[e];
+                            Cb[(int64_t)(row - ov.r0) * ldc + (col - ov.c0) + e] = v[e];
                 }
             }
         }
@@ -732,6 +775,44 @@ splitk_reduce(const float *W, int64_t split_stride, int64_t ldw, int split,
             for (int e = 0; e < 4; ++e)
                 if (j + e < N)
                     c[e] = s[e];
+        }
+    }
+}
+
+// Tile-major split partials -> C: for each tile of the range [tile_base,
+// tile_base + tile_count), C[tile] = sum over p of W[p][tile], p ascending.
+// W holds split x tile_count dense BM x BN blocks.
+template <int BM, int BN>
+__global__ void __launch_bounds__(256)
+splitk_reduce_tiles(const float *W, int split, int tile_base, int tile_count, int tiles_m, int tiles_n,
+                    int group_m, float *C, int64_t ldc, int M, int N, int vec_c)
+{
+    constexpr int V = BM * BN / 4;  // float4 vectors per tile
+    const int64_t nvec = (int64_t)tile_count * V;
+    const int64_t pstride = (int64_t)tile_count * BM * BN;
+    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nvec;
+         t += (int64_t)gridDim.x * blockDim.x) {
+        const int local = (int)(t / V);
+        const int v = (int)(t - (int64_t)local * V);
+        const int r = v / (BN / 4), c = (v % (BN / 4)) * 4;
+        int tm, tn;
+        logical_tile(tile_base + local, tiles_m, tiles_n, group_m, tm, tn);
+        const int row = tm * BM + r, col = tn * BN + c;
+        if (row >= M || col >= N)
+            continue;
+        const float *w = W + (int64_t)local * BM * BN + (int64_t)r * BN + c;
+        f32x4 sum = *(const f32x4 *)w;
+        for (int q = 1; q < split; ++q) {
+            const f32x4 x = *(const f32x4 *)(w + q * pstride);
+            sum += x;
+        }
+        float *dst = C + (int64_t)row * ldc + col;
+        if (vec_c && col + 4 <= N) {
+            *(f32x4 *)dst = sum;
+        } else {
+            for (int e = 0; e < 4; ++e)
+                if (col + e < N)
+                    dst[e] = sum[e];
         }
     }
 }

@@ -49,7 +49,8 @@ void set_error(xgemm_ctx *h, const char *what, hipError_t e)
 bool valid_config(const xgemm_config *c)
 {
     return c && c->tile >= 0 && c->tile < XGEMM_TILE_COUNT && c->split_k >= 1 && c->split_k <= 64 &&
-           c->group_m >= 1 && c->group_m <= 64 && c->reserved == 0;
+           c->group_m >= 1 && c->group_m <= 64 && c->tail_split >= 0 && c->tail_split <= 64 &&
+           (c->tail_split <= 1 || c->split_k == 1);
 }
 
 // K elements each split covers: K / split rounded up to the K step, so that
@@ -61,11 +62,16 @@ int64_t split_chunk(int64_t K, int split, int bk)
 
 // Modelled cost of a configuration in units of MFMA-peak cycles of one CU:
 // the number of full waves of workgroups times the cycles one workgroup
-// needs at the tile's sustained rate, plus the split-k traffic through HBM.
+// needs at the tile's sustained rate, plus the split-k traffic.  The tile
+// efficiencies and the split-k byte rate were fitted to measured times of
+// the 4096^3, 16384x5120x4096, 4096x14336x4096 and 1024x1024x65536
+// problems on MI355X (the split partials are written in a burst at the
+// end of the main loop and read back by a separate kernel, which together
+// move about 1.5 KB per peak cycle).
 double model_cost(int64_t M, int64_t N, int64_t K, int cu_count, int tile, int split)
 {
     const TileShape &t = kTiles[tile];
-    static const double kTileEff[XGEMM_TILE_COUNT] = {1.0, 0.9, 0.75};
+    static const double kTileEff[XGEMM_TILE_COUNT] = {1.0, 0.85, 0.75};
     const int64_t tiles = cdiv(M, t.bm) * cdiv(N, t.bn);
     const int64_t kc = split_chunk(K, split, t.bk);
     const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
@@ -74,12 +80,52 @@ double model_cost(int64_t M, int64_t N, int64_t K, int cu_count, int tile, int s
     const double wg_cycles = 2.0 * t.bm * t.bn * (double)kc * t.wg_per_cu / 4096.0 / kTileEff[tile];
     double cost = (double)waves * wg_cycles;
     if (split > 1) {
-        // partials written once and read once, C written once; ~3.3 KB per
-        // cycle of HBM bandwidth (8 TB/s at 2.4 GHz), plus a launch
+        // partials written once and read once, C written once, plus a launch
         const double bytes = (2.0 * split + 1.0) * 4.0 * (double)M * (double)N;
-        cost += bytes / 3333.0 + 4000.0;
+        cost += bytes / 1500.0 + 4000.0;
     }
     return cost;
+}
+
+// Tile rows per group in the launch order.  Each XCD runs a contiguous
+// share of the logical tile ids; when eight whole tile rows fit in one
+// share, groups of eight keep an XCD's concurrent tiles square-ish across
+// the whole share, otherwise groups of four.
+int choose_group_m(int64_t tiles_m, int64_t tiles_n, int split)
+{
+    const int64_t share = tiles_m * tiles_n * split / xgemm_dev::kNumXcd;
+    return (tiles_n * 8 <= share && tiles_m >= 8) ? 8 : 4;
+}
+
+// Split-k factor for the tiles past the last full wave of workgroups (0:
+// run them unsplit).  A partial last wave leaves CUs idle for a whole tile
+// time; splitting those tiles' K ranges spreads them over the idle CUs at
+// the price of writing, reading and summing their partials.
+int choose_tail_split(int64_t M, int64_t N, int64_t K, int cu_count, int tile)
+{
+    const TileShape &t = kTiles[tile];
+    const int64_t tiles = cdiv(M, t.bm) * cdiv(N, t.bn);
+    const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
+    const int64_t tail = tiles % slots;
+    if (tiles <= slots || tail == 0)
+        return 0;
+    // Peak-rate cycles of one tile, at the kernel's sustained fraction of
+    // the peak (about 0.55 on MI355X with random data), against the
+    // partials' traffic at about 70% of HBM bandwidth (2.3 KB per cycle).
+    const double wg = 2.0 * t.bm * t.bn * (double)K * t.wg_per_cu / 4096.0 / 0.55;
+    double best = wg;  // the tail run unsplit: one more full tile time
+    int best_s = 0;
+    for (int s2 = 2; s2 <= 8; s2 *= 2) {
+        if (tail * s2 > slots || split_chunk(K, s2, t.bk) * (s2 - 1) >= K || K / s2 < 3 * t.bk)
+            break;
+        const double bytes = (2.0 * s2 + 1.0) * 4.0 * (double)tail * t.bm * t.bn;
+        const double c = wg / s2 + bytes / 2333.0 + 4000.0;
+        if (c < best * 0.95) {
+            best = c;
+            best_s = s2;
+        }
+    }
+    return best_s;
 }
 
 void select_config(int64_t M, int64_t N, int64_t K, int cu_count, xgemm_config *out)
@@ -98,10 +144,16 @@ void select_config(int64_t M, int64_t N, int64_t K, int cu_count, xgemm_config *
             }
         }
     }
+    const TileShape &t = kTiles[best_tile];
     out->tile = best_tile;
     out->split_k = best_split;
-    out->group_m = 4;
-    out->reserved = 0;
+    out->group_m = choose_group_m(cdiv(M, t.bm), cdiv(N, t.bn), best_split);
+    // The tail split is not chosen automatically: on MI355X a partial last
+    // wave runs at a higher clock (fewer busy CUs, less power), and the
+    // measured 4096 x 14336 x 4096 problem (3.5 waves) took 447 us with a
+    // 2-way tail split against 445 us without.  choose_tail_split's model is
+    // kept for callers that force the split through xgemm_run_config.
+    out->tail_split = 0;
 }
 
 size_t workspace_bytes(int64_t M, int64_t N, int split)
@@ -171,6 +223,27 @@ hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int g
     }
 }
 
+template <int BM, int BN>
+hipError_t launch_tile_reduce_t(const GemmParams &p, float *C, int64_t ldc, int vec_c, hipStream_t s)
+{
+    const int64_t nvec = (int64_t)p.tile_count * BM * BN / 4;
+    const int grid = (int)(cdiv(nvec, 256) < 8192 ? cdiv(nvec, 256) : 8192);
+    hipLaunchKernelGGL((xgemm_dev::splitk_reduce_tiles<BM, BN>), dim3(grid), dim3(256), 0, s, (const float *)p.C,
+                       p.split, p.tile_base, p.tile_count, p.tiles_m, p.tiles_n, p.group_m, C, ldc, p.M, p.N,
+                       vec_c);
+    return hipGetLastError();
+}
+
+hipError_t launch_tile_reduce(int tile, const GemmParams &p, float *C, int64_t ldc, int vec_c, hipStream_t s)
+{
+    switch (tile) {
+    case XGEMM_TILE_256x256: return launch_tile_reduce_t<256, 256>(p, C, ldc, vec_c, s);
+    case XGEMM_TILE_256x128: return launch_tile_reduce_t<256, 128>(p, C, ldc, vec_c, s);
+    case XGEMM_TILE_128x128: return launch_tile_reduce_t<128, 128>(p, C, ldc, vec_c, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 int check_args(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
                const void *B, int64_t ldb, const float *C, int64_t ldc, int dtype)
 {
@@ -192,66 +265,107 @@ int check_args(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int
     return XGEMM_OK;
 }
 
-// Everything about a launch that follows from the arguments on the host.
-struct Plan {
+// One kernel launch of a plan: a range of logical tiles, its split-k
+// factor and where its output goes.
+struct Segment {
     GemmParams p;
-    int tile;
-    int split;
     int64_t grid;
-    bool dma;       // pipelined direct-to-LDS kernel (else the general one)
-    size_t ws;      // split-k workspace bytes
-    int64_t ldw;    // workspace row stride (floats)
+    bool dma;    // pipelined direct-to-LDS kernel (else the general one)
+    int reduce;  // 0: writes C; 1: full-matrix partials + splitk_reduce; 2: tile partials + tile reduce
 };
 
-// Plan a launch for K > 0 and M, N > 0 with configuration cfg.  Device
-// pointers are only inspected for their alignment.
+// Everything about a call that follows from the arguments on the host.
+struct Plan {
+    int tile;
+    Segment seg[2];
+    int nseg;
+    size_t ws;      // workspace bytes
+    int64_t ldw;    // full-matrix workspace row stride (floats)
+};
+
+// K range per split with trailing empty splits dropped; returns the split.
+int trim_split(int64_t K, int split, int bk, int64_t *kc)
+{
+    *kc = split_chunk(K, split, bk);
+    while (split > 1 && *kc * (split - 1) >= K) {
+        --split;
+        *kc = split_chunk(K, split, bk);
+    }
+    return split;
+}
+
+// Plan a call for K > 0 and M, N > 0 with configuration cfg on a device
+// with cu_count CUs.  Device pointers are only inspected for alignment.
 int make_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
-              const float *C, int64_t ldc, const xgemm_config &cfg, Plan *out)
+              const float *C, int64_t ldc, const xgemm_config &cfg, int cu_count, Plan *out)
 {
     const TileShape &t = kTiles[cfg.tile];
-    // drop trailing splits that would have no K range
-    int split = cfg.split_k;
-    int64_t kc = split_chunk(K, split, t.bk);
-    while (split > 1 && kc * (split - 1) >= K) {
-        --split;
-        kc = split_chunk(K, split, t.bk);
-    }
     const int64_t tiles_m = cdiv(M, t.bm), tiles_n = cdiv(N, t.bn);
-    const int64_t grid = tiles_m * tiles_n * split;
-    if (grid > 0x7fffffff)
+    const int64_t tiles = tiles_m * tiles_n;
+    int64_t kc;
+    const int split = trim_split(K, cfg.split_k, t.bk, &kc);
+    if (tiles * split > 0x7fffffff || tiles * 8 > 0x7fffffff)
         return XGEMM_ERR_INVALID_ARG;
 
-    GemmParams &p = out->p;
-    p.A = (const uint16_t *)A;
-    p.B = (const uint16_t *)B;
-    p.lda = lda;
-    p.ldb = ldb;
-    p.M = (int)M;
-    p.N = (int)N;
-    p.K = (int)K;
-    p.k_chunk = (int)kc;
-    p.split = split;
-    p.tiles_m = (int)tiles_m;
-    p.tiles_n = (int)tiles_n;
-    p.group_m = cfg.group_m;
-    p.vec_ab = ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 8 == 0) && (ldb % 8 == 0);
-    out->ldw = cdiv(N, 4) * 4;
-    if (split == 1) {
-        p.C = (float *)C;
-        p.ldc = ldc;
-        p.split_stride = 0;
-        p.vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
-    } else {
-        p.C = nullptr;  // the workspace, filled in at launch
-        p.ldc = out->ldw;
-        p.split_stride = M * out->ldw;
-        p.vec_c = 1;
-    }
+    GemmParams base;
+    base.A = (const uint16_t *)A;
+    base.B = (const uint16_t *)B;
+    base.lda = lda;
+    base.ldb = ldb;
+    base.M = (int)M;
+    base.N = (int)N;
+    base.K = (int)K;
+    base.tiles_m = (int)tiles_m;
+    base.tiles_n = (int)tiles_n;
+    base.group_m = cfg.group_m;
+    base.vec_ab = ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 8 == 0) && (ldb % 8 == 0);
+    base.tile_base = 0;
+    base.tile_major = 0;
     out->tile = cfg.tile;
-    out->split = split;
-    out->grid = grid;
-    out->dma = dma_eligible(p, t.bm);
-    out->ws = workspace_bytes(M, N, split);
+    out->ldw = cdiv(N, 4) * 4;
+    out->ws = 0;
+    out->nseg = 0;
+
+    auto add = [&](int64_t first, int64_t count, int sp, int64_t kchunk, int reduce) {
+        Segment &g = out->seg[out->nseg++];
+        g.p = base;
+        g.p.tile_base = (int)first;
+        g.p.tile_count = (int)count;
+        g.p.split = sp;
+        g.p.k_chunk = (int)kchunk;
+        g.reduce = reduce;
+        if (reduce == 0) {
+            g.p.C = (float *)C;
+            g.p.ldc = ldc;
+            g.p.split_stride = 0;
+            g.p.vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
+        } else {
+            g.p.C = nullptr;  // the workspace, filled in at launch
+            g.p.ldc = reduce == 1 ? out->ldw : t.bn;
+            g.p.split_stride = reduce == 1 ? M * out->ldw : 0;
+            g.p.vec_c = 1;
+            g.p.tile_major = reduce == 2;
+        }
+        g.grid = count * sp;
+        g.dma = dma_eligible(g.p, t.bm);
+    };
+
+    if (split > 1) {
+        add(0, tiles, split, kc, 1);
+        out->ws = workspace_bytes(M, N, split);
+        return XGEMM_OK;
+    }
+    const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
+    int64_t kct = 0;
+    const int tail_split = cfg.tail_split >= 2 ? trim_split(K, cfg.tail_split, t.bk, &kct) : 1;
+    const int64_t tail = (tail_split >= 2 && tiles > slots) ? tiles % slots : 0;
+    if (tail > 0) {
+        add(0, tiles - tail, 1, kc, 0);
+        add(tiles - tail, tail, tail_split, kct, 2);
+        out->ws = (size_t)tail * tail_split * t.bm * t.bn * sizeof(float);
+    } else {
+        add(0, tiles, 1, kc, 0);
+    }
     return XGEMM_OK;
 }
 
@@ -286,7 +400,7 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     else
         select_config(M, N, K, h->cu_count, &cfg);
     Plan plan;
-    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, &plan);
+    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan);
     if (rc != XGEMM_OK)
         return rc;
 
@@ -311,25 +425,32 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
         }
         h->ws_bytes = plan.ws;
     }
-    if (plan.split > 1)
-        plan.p.C = (float *)h->workspace;
 
-    e = launch_tile(plan.tile, plan.dma, dtype, plan.p, (int)plan.grid, s);
-    if (e != hipSuccess) {
-        set_error(h, "gemm launch", e);
-        return XGEMM_ERR_HIP;
-    }
-    if (plan.split > 1) {
-        const int64_t nvec = M * cdiv(N, 4);
-        const int grid = (int)(cdiv(nvec, 256) < 8192 ? cdiv(nvec, 256) : 8192);
-        const int vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
-        hipLaunchKernelGGL(xgemm_dev::splitk_reduce, dim3(grid), dim3(256), 0, s,
-                           (const float *)h->workspace, (int64_t)(M * plan.ldw), plan.ldw, plan.split, C,
-                           ldc, (int)M, (int)N, vec_c);
-        e = hipGetLastError();
+    const int vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
+    for (int i = 0; i < plan.nseg; ++i) {
+        Segment &g = plan.seg[i];
+        if (g.reduce)
+            g.p.C = (float *)h->workspace;
+        e = launch_tile(plan.tile, g.dma, dtype, g.p, (int)g.grid, s);
         if (e != hipSuccess) {
-            set_error(h, "split-k reduce launch", e);
+            set_error(h, "gemm launch", e);
             return XGEMM_ERR_HIP;
+        }
+        if (g.reduce == 1) {
+            const int64_t nvec = M * cdiv(N, 4);
+            const int grid = (int)(cdiv(nvec, 256) < 8192 ? cdiv(nvec, 256) : 8192);
+            hipLaunchKernelGGL(xgemm_dev::splitk_reduce, dim3(grid), dim3(256), 0, s,
+                               (const float *)h->workspace, (int64_t)(M * plan.ldw), plan.ldw, g.p.split, C,
+                               ldc, (int)M, (int)N, vec_c);
+        } else if (g.reduce == 2) {
+            e = launch_tile_reduce(plan.tile, g.p, C, ldc, vec_c, s);
+        }
+        if (g.reduce) {
+            e = hipGetLastError();
+            if (e != hipSuccess) {
+                set_error(h, "split-k reduce launch", e);
+                return XGEMM_ERR_HIP;
+            }
         }
     }
     return XGEMM_OK;
@@ -422,17 +543,23 @@ int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t 
         lda < K || ldb < N)
         return -1;
     Plan plan;
-    // C's alignment does not affect the choice
-    if (make_plan(M, N, K, A, lda, B, ldb, nullptr, N, *cfg, &plan) != XGEMM_OK)
+    // C's alignment does not affect the choice; the tail split needs a CU count
+    if (make_plan(M, N, K, A, lda, B, ldb, nullptr, N, *cfg, 256, &plan) != XGEMM_OK)
         return -1;
-    return plan.dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
+    return plan.seg[0].dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
 }
 
-size_t xgemm_workspace_bytes(int64_t M, int64_t N, const xgemm_config *cfg)
+size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, const xgemm_config *cfg)
 {
-    if (!valid_config(cfg) || M < 0 || N < 0)
+    if (!valid_config(cfg) || M < 0 || N < 0 || K < 0 || cu_count < 1 || M >= kMaxDim || N >= kMaxDim ||
+        K >= kMaxDim)
         return 0;
-    return workspace_bytes(M, N, cfg->split_k);
+    if (M == 0 || N == 0 || K == 0)
+        return 0;
+    Plan plan;
+    if (make_plan(M, N, K, nullptr, K, nullptr, N, nullptr, N, *cfg, cu_count, &plan) != XGEMM_OK)
+        return 0;
+    return plan.ws;
 }
 
 const char *xgemm_strerror(int status)

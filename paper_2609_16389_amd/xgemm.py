@@ -36,10 +36,11 @@ XGEMM_KERNEL_PIPELINED = 1
 
 class xgemm_config(ctypes.Structure):
     _fields_ = [("tile", ctypes.c_int32), ("split_k", ctypes.c_int32),
-                ("group_m", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("group_m", ctypes.c_int32), ("tail_split", ctypes.c_int32)]
 
     def __repr__(self):
-        return "xgemm_config(tile=%d, split_k=%d, group_m=%d)" % (self.tile, self.split_k, self.group_m)
+        return "xgemm_config(tile=%d, split_k=%d, group_m=%d, tail_split=%d)" % (
+            self.tile, self.split_k, self.group_m, self.tail_split)
 
 
 class XgemmError(RuntimeError):
@@ -80,7 +81,7 @@ lib.xgemm_tile_info.argtypes = [_i32] + [ctypes.POINTER(ctypes.c_int)] * 4
 lib.xgemm_tile_info.restype = _i32
 lib.xgemm_kernel_family.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, ctypes.POINTER(xgemm_config)]
 lib.xgemm_kernel_family.restype = _i32
-lib.xgemm_workspace_bytes.argtypes = [_i64, _i64, ctypes.POINTER(xgemm_config)]
+lib.xgemm_workspace_bytes.argtypes = [_i64, _i64, _i64, _i32, ctypes.POINTER(xgemm_config)]
 lib.xgemm_workspace_bytes.restype = ctypes.c_size_t
 lib.xgemm_strerror.argtypes = [_i32]
 lib.xgemm_strerror.restype = ctypes.c_char_p
@@ -141,8 +142,8 @@ def xgemm_kernel_family(M, N, K, A, lda, B, ldb, cfg) -> int:
     return lib.xgemm_kernel_family(M, N, K, A, lda, B, ldb, ctypes.byref(cfg))
 
 
-def xgemm_workspace_bytes(M, N, cfg) -> int:
-    return int(lib.xgemm_workspace_bytes(M, N, ctypes.byref(cfg)))
+def xgemm_workspace_bytes(M, N, K, cu_count, cfg) -> int:
+    return int(lib.xgemm_workspace_bytes(M, N, K, cu_count, ctypes.byref(cfg)))
 
 
 def xgemm_strerror(status: int) -> str:

@@ -62,5 +62,5 @@ def check_exact(C_gpu: np.ndarray, C_ref: np.ndarray, what: str = ""):
                              % (what, int(bad.sum()), i, j, C_gpu[i, j], C_ref[i, j]))
 
 
-def config(tile, split=1, group_m=4):
-    return xg.xgemm_config(tile=tile, split_k=split, group_m=group_m, reserved=0)
+def config(tile, split=1, group_m=4, tail_split=0):
+    return xg.xgemm_config(tile=tile, split_k=split, group_m=group_m, tail_split=tail_split)

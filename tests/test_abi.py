@@ -70,15 +70,32 @@ def test_selector_rejects_bad_arguments():
 
 
 def test_workspace_bytes():
-    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, reserved=0)
-    assert xg.xgemm_workspace_bytes(1024, 1024, cfg) == 0
+    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0)
+    assert xg.xgemm_workspace_bytes(1024, 1024, 4096, 256, cfg) == 0
     cfg.split_k = 16
-    assert xg.xgemm_workspace_bytes(1024, 1024, cfg) == 16 * 1024 * 1024 * 4
-    assert xg.xgemm_workspace_bytes(10, 5, cfg) == 16 * 10 * 8 * 4  # rows padded to 4 floats
-    cfg.reserved = 1
-    assert xg.xgemm_workspace_bytes(10, 5, cfg) == 0
-    cfg.reserved, cfg.tile = 0, 99
-    assert xg.xgemm_workspace_bytes(10, 5, cfg) == 0
+    assert xg.xgemm_workspace_bytes(1024, 1024, 65536, 256, cfg) == 16 * 1024 * 1024 * 4
+    assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 16 * 10 * 8 * 4  # rows padded to 4 floats
+    cfg.tail_split = 2                      # tail split needs split_k == 1
+    assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 0
+    cfg.tail_split, cfg.tile = 0, 99
+    assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 0
+
+
+def test_tail_split_plan():
+    # 4096 x 14336 with 256 x 256 tiles: 896 tiles = 3 full waves of 256 + 128
+    w = wl.WORKLOADS["proj4096x14336x4096_fp16"]
+    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=2)
+    assert xg.xgemm_workspace_bytes(w.M, w.N, w.K, 256, cfg) == 128 * 2 * 256 * 256 * 4
+    # not chosen automatically (measured neutral on MI355X)
+    assert xg.xgemm_select_config(w.M, w.N, w.K, xg.XGEMM_FP16, 256).tail_split == 0
+    # whole waves (8192^3: 1024 tiles) need no tail split
+    w8 = wl.WORKLOADS["gemm8192_bf16"]
+    cfg8 = xg.xgemm_select_config(w8.M, w8.N, w8.K, xg.XGEMM_BF16, 256)
+    assert cfg8.tail_split == 0
+    assert xg.xgemm_workspace_bytes(w8.M, w8.N, w8.K, 256, cfg8) == 0
+    # fewer tiles than one wave: nothing to split
+    forced = xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=4)
+    assert xg.xgemm_workspace_bytes(1024, 1024, 4096, 256, forced) == 0
 
 
 def test_single_hip_runtime_in_process():
@@ -98,7 +115,7 @@ def test_single_hip_runtime_in_process():
 
 
 def test_kernel_family_rules():
-    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, reserved=0)
+    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0)
     al = 1 << 20  # a 16-byte aligned stand-in address (only alignment is inspected)
     fam = lambda M, N, K, a=al, lda=None, b=al, ldb=None, c=cfg: xg.xgemm_kernel_family(
         M, N, K, a, K if lda is None else lda, b, N if ldb is None else ldb, c)
@@ -112,9 +129,9 @@ def test_kernel_family_rules():
     assert fam(1000, 1000, 1024, a=al + 2) == G  # misaligned A
     assert fam(1000, 1000, 1024, lda=1028) == G  # lda % 8 != 0
     assert fam(1000, 1000, 1024, ldb=1004) == G  # ldb % 8 != 0
-    cfg16 = xg.xgemm_config(tile=0, split_k=16, group_m=4, reserved=0)
+    cfg16 = xg.xgemm_config(tile=0, split_k=16, group_m=4, tail_split=0)
     assert fam(1024, 1024, 65536, c=cfg16) == P
     assert fam(1024, 1024, 1024, c=cfg16) == G   # 64-element splits are too short
     assert fam(0, 8, 32) == -1
-    bad = xg.xgemm_config(tile=7, split_k=1, group_m=4, reserved=0)
+    bad = xg.xgemm_config(tile=7, split_k=1, group_m=4, tail_split=0)
     assert fam(8, 8, 32, c=bad) == -1

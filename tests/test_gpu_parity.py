@@ -126,6 +126,25 @@ def test_split_k_integer_exact(split):
     check_exact(run_gpu(A, B, "fp16", config=config(xg.XGEMM_TILE_128x128, split)), C_ref)
 
 
+@pytest.mark.parametrize("tail_split", [2, 4, 8])
+@pytest.mark.parametrize("shape", [(2304, 7936, 2048), (2300, 7930, 1000)], ids=lambda s: "x".join(map(str, s)))
+def test_tail_split(tail_split, shape):
+    """Tiles past the last full wave of 256 workgroups run as a second,
+    split-k launch whose tile partials are reduced into C."""
+    M, N, K = shape  # 9 x 31 = 279 tiles of 256 x 256: a tail of 23
+    A, B, C_ref, S = _case(M, N, K, "bf16", seed=tail_split)
+    cfg = config(xg.XGEMM_TILE_256x256, 1, 4, tail_split)
+    assert xg.xgemm_workspace_bytes(M, N, K, 256, cfg) == 23 * tail_split * 256 * 256 * 4
+    check_close(run_gpu(A, B, "bf16", config=cfg), C_ref, S, "tail split %d %s" % (tail_split, shape))
+
+
+def test_tail_split_integer_exact():
+    M, N, K = 2304, 7936, 1024
+    A, B = wl.make_int_inputs(M, N, K, "fp16", seed=12)
+    C_ref, _ = oracle.gemm(A, B, "fp16")
+    check_exact(run_gpu(A, B, "fp16", config=config(xg.XGEMM_TILE_256x256, 1, 4, 4)), C_ref, "tail split")
+
+
 # ---------------------------------------------------------------------------
 # exact cases
 # ---------------------------------------------------------------------------
