@@ -123,6 +123,25 @@ int xgemm_run_config(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
                      const xgemm_config *cfg);
 
 /*
+ * Strided batched product: for b = 0 .. batch-1,
+ *     C + b*stride_c  =  (A + b*stride_a) * (B + b*stride_b)
+ * each problem M x N x K as in xgemm_run (row-major, leading dimensions
+ * lda, ldb, ldc).  Strides are in elements; stride_a or stride_b may be 0
+ * (one A or B shared by every problem), but the outputs must not overlap:
+ * stride_c >= (M-1)*ldc + N when batch > 1.  batch == 0: no-op.  The
+ * paper's benchmarks include such batched products (its comparison uses a
+ * strided-batched vendor GEMM with batch count L, Section 6).  All problems
+ * run in one launch without split-k; 16-byte vector paths additionally
+ * need stride_a and stride_b multiples of 8 and stride_c a multiple of 4.
+ * Errors as xgemm_run, plus XGEMM_ERR_INVALID_ARG for negative batch or
+ * strides, overlapping outputs or batch > 2^31 - 1.
+ */
+int xgemm_run_strided_batched(xgemm_handle_t h, int64_t batch, int64_t M, int64_t N, int64_t K,
+                              const void *A, int64_t lda, int64_t stride_a,
+                              const void *B, int64_t ldb, int64_t stride_b,
+                              float *C, int64_t ldc, int64_t stride_c, int dtype, void *stream);
+
+/*
  * The configuration xgemm_run would use for this problem on a device with
  * `cu_count` compute units (host-only; touches no GPU).  Returns
  * XGEMM_ERR_INVALID_ARG for negative sizes, an unknown dtype, cu_count < 1 or

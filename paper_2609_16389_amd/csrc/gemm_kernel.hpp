@@ -52,6 +52,10 @@ struct GemmParams {
     int tile_base;          // this launch covers logical tiles [tile_base, tile_base + tile_count)
     int tile_count;
     int tile_major;         // 1: write each (split, tile) partial as a dense BM x BN block of C
+    int batch;              // independent problems; problem b uses A + b*stride_a, B + b*stride_b,
+    int64_t stride_a;       //   C + b*stride_c (elements); batched launches have split == 1
+    int64_t stride_b;
+    int64_t stride_c;
 };
 
 template <int DT>
@@ -100,15 +104,26 @@ __host__ __device__ __forceinline__ void logical_tile(int t, int tiles_m, int ti
 // one K range run together.  (The paper's persistent kernels hand out tasks
 // in lexicographic order and leave other orders to future work, Section
 // 4.2.)
-__device__ __forceinline__ void map_tile(const GemmParams &p, int &tm, int &tn, int &ks, int &local)
+// The batch index is outermost of all: the problems of a batch run one
+// after another across the grid.  Returns the workgroup's parameters with
+// A, B and C moved to its problem.
+__device__ __forceinline__ GemmParams map_tile(const GemmParams &p_in, int &tm, int &tn, int &ks, int &local)
 {
     const int total = gridDim.x;
     const int w = blockIdx.x;
     const int per = total / kNumXcd;
-    const int lid = (w < per * kNumXcd) ? (w % kNumXcd) * per + w / kNumXcd : w;
-    ks = lid / p.tile_count;
-    local = lid - ks * p.tile_count;
-    logical_tile(p.tile_base + local, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
+    int lid = (w < per * kNumXcd) ? (w % kNumXcd) * per + w / kNumXcd : w;
+    const int per_batch = p_in.tile_count * p_in.split;
+    const int b = lid / per_batch;
+    lid -= b * per_batch;
+    ks = lid / p_in.tile_count;
+    local = lid - ks * p_in.tile_count;
+    logical_tile(p_in.tile_base + local, p_in.tiles_m, p_in.tiles_n, p_in.group_m, tm, tn);
+    GemmParams p = p_in;
+    p.A += b * p_in.stride_a;
+    p.B += b * p_in.stride_b;
+    p.C += b * p_in.stride_c;
+    return p;
 }
 
 // Output placement: row-major C (or a full-matrix split partial) at
@@ -178,7 +193,7 @@ __device__ __forceinline__ u32x4 column8(const u32x4 (&v)[8], int c)
 
 template <int BM, int BN, int BK, int WGM, int WGN, int DT>
 __global__ void __launch_bounds__(WGM * WGN * 64)
-gemm_kernel(GemmParams p)
+gemm_kernel(GemmParams p_in)
 {
     constexpr int NT = WGM * WGN * 64;
     constexpr int TM = BM / WGM, TN = BN / WGN;   // wave tile
@@ -198,7 +213,7 @@ gemm_kernel(GemmParams p)
     __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
 
     int tm, tn, ks, local;
-    map_tile(p, tm, tn, ks, local);
+    const GemmParams p = map_tile(p_in, tm, tn, ks, local);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = ks * p.k_chunk;
     const int kend = min(p.K, kbeg + p.k_chunk);
@@ -470,7 +485,7 @@ __device__ __forceinline__ int aswz(int r)
 
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT>
 __global__ void __launch_bounds__(WGM * WGN * 64, 1)
-gemm_kernel_dma(GemmParams p)
+gemm_kernel_dma(GemmParams p_in)
 {
     constexpr int NW = WGM * WGN;
     constexpr int TM = BM / WGM, TN = BN / WGN;
@@ -495,7 +510,7 @@ gemm_kernel_dma(GemmParams p)
     __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
 
     int tm, tn, ks, local;
-    map_tile(p, tm, tn, ks, local);
+    const GemmParams p = map_tile(p_in, tm, tn, ks, local);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = ks * p.k_chunk;
     const int kend = min(p.K, kbeg + p.k_chunk);

@@ -128,15 +128,25 @@ int choose_tail_split(int64_t M, int64_t N, int64_t K, int cu_count, int tile)
     return best_s;
 }
 
+void select_config_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int cu_count, xgemm_config *out);
+
 void select_config(int64_t M, int64_t N, int64_t K, int cu_count, xgemm_config *out)
+{
+    select_config_batched(1, M, N, K, cu_count, out);
+}
+
+// The configuration for `batch` independent problems of one shape: the
+// batch multiplies the workgroups of a wave, and batched launches do not
+// split K.
+void select_config_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int cu_count, xgemm_config *out)
 {
     double best = 0.0;
     int best_tile = XGEMM_TILE_256x256, best_split = 1;
     for (int tile = 0; tile < XGEMM_TILE_COUNT; ++tile) {
-        for (int split = 1; split <= 16; split *= 2) {
+        for (int split = 1; split <= (batch > 1 ? 1 : 16); split *= 2) {
             if (split > 1 && split_chunk(K, split, kTiles[tile].bk) * (split - 1) >= K)
                 break;  // the last split would be empty
-            const double c = model_cost(M, N, K, cu_count, tile, split);
+            const double c = model_cost(M * batch, N, K, cu_count, tile, split);
             if (best == 0.0 || c < best * 0.98) {
                 best = c;
                 best_tile = tile;
@@ -147,7 +157,7 @@ void select_config(int64_t M, int64_t N, int64_t K, int cu_count, xgemm_config *
     const TileShape &t = kTiles[best_tile];
     out->tile = best_tile;
     out->split_k = best_split;
-    out->group_m = choose_group_m(cdiv(M, t.bm), cdiv(N, t.bn), best_split);
+    out->group_m = choose_group_m(cdiv(M, t.bm), cdiv(N, t.bn), best_split * (int)(batch < 64 ? batch : 64));
     // The tail split is not chosen automatically: on MI355X a partial last
     // wave runs at a higher clock (fewer busy CUs, less power), and the
     // measured 4096 x 14336 x 4096 problem (3.5 waves) took 447 us with a
@@ -321,6 +331,8 @@ int make_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const
     base.vec_ab = ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 8 == 0) && (ldb % 8 == 0);
     base.tile_base = 0;
     base.tile_major = 0;
+    base.batch = 1;
+    base.stride_a = base.stride_b = base.stride_c = 0;
     out->tile = cfg.tile;
     out->ldw = cdiv(N, 4) * 4;
     out->ws = 0;
@@ -456,6 +468,65 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     return XGEMM_OK;
 }
 
+int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                int64_t sa, const void *B, int64_t ldb, int64_t sb, float *C, int64_t ldc, int64_t sc, int dtype,
+                void *stream)
+{
+    if (batch < 0 || sa < 0 || sb < 0 || sc < 0)
+        return XGEMM_ERR_INVALID_ARG;
+    int rc = check_args(h, M, N, K, A, lda, B, ldb, C, ldc, dtype);
+    if (rc != XGEMM_OK)
+        return rc;
+    if (batch == 0 || M == 0 || N == 0)
+        return XGEMM_OK;
+    if (batch == 1)
+        return run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream, nullptr);
+    // outputs of different problems must not overlap; every problem's
+    // matrices must stay addressable
+    if (sc < (M - 1) * ldc + N)
+        return XGEMM_ERR_INVALID_ARG;
+    const double last = (double)(batch - 1);
+    if (last * sa + (double)M * lda > 9.0e18 || last * sb + (double)K * ldb > 9.0e18 ||
+        last * sc + (double)M * ldc > 9.0e18 || batch > 0x7fffffff)
+        return XGEMM_ERR_INVALID_ARG;
+    h->last_error[0] = '\0';
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (K == 0) {
+        for (int64_t b = 0; b < batch; ++b) {
+            rc = run(h, M, N, 0, A, lda, B, ldb, C + b * sc, ldc, dtype, stream, nullptr);
+            if (rc != XGEMM_OK)
+                return rc;
+        }
+        return XGEMM_OK;
+    }
+    xgemm_config cfg;
+    select_config_batched(batch, M, N, K, h->cu_count, &cfg);
+    Plan plan;
+    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan);
+    if (rc != XGEMM_OK)
+        return rc;
+    Segment &g = plan.seg[0];
+    if (plan.nseg != 1 || g.reduce != 0 || g.p.split != 1)
+        return XGEMM_ERR_INVALID_ARG;  // batched plans are single unsplit launches
+    if (g.grid * batch > 0x7fffffff)
+        return XGEMM_ERR_INVALID_ARG;
+    g.p.batch = (int)batch;
+    g.p.stride_a = sa;
+    g.p.stride_b = sb;
+    g.p.stride_c = sc;
+    // 16-byte vector paths need every problem's matrices aligned
+    g.p.vec_ab = g.p.vec_ab && (sa % 8 == 0) && (sb % 8 == 0);
+    g.p.vec_c = g.p.vec_c && (sc % 4 == 0);
+    g.dma = dma_eligible(g.p, kTiles[plan.tile].bm);
+    e = launch_tile(plan.tile, g.dma, dtype, g.p, (int)(g.grid * batch), s);
+    if (e != hipSuccess) {
+        set_error(h, "gemm launch", e);
+        return XGEMM_ERR_HIP;
+    }
+    return XGEMM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -515,6 +586,13 @@ int xgemm_run_config(xgemm_handle_t h, int64_t M, int64_t N, int64_t K, const vo
     if (!cfg)
         return XGEMM_ERR_INVALID_ARG;
     return run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream, cfg);
+}
+
+int xgemm_run_strided_batched(xgemm_handle_t h, int64_t batch, int64_t M, int64_t N, int64_t K, const void *A,
+                              int64_t lda, int64_t stride_a, const void *B, int64_t ldb, int64_t stride_b, float *C,
+                              int64_t ldc, int64_t stride_c, int dtype, void *stream)
+{
+    return run_batched(h, batch, M, N, K, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c, dtype, stream);
 }
 
 int xgemm_select_config(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, xgemm_config *out)

@@ -75,6 +75,9 @@ lib.xgemm_run.restype = _i32
 lib.xgemm_run_config.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p,
                                  ctypes.POINTER(xgemm_config)]
 lib.xgemm_run_config.restype = _i32
+lib.xgemm_run_strided_batched.argtypes = [_handle_t, _i64, _i64, _i64, _i64, _p, _i64, _i64, _p, _i64, _i64,
+                                          _p, _i64, _i64, _i32, _p]
+lib.xgemm_run_strided_batched.restype = _i32
 lib.xgemm_select_config.argtypes = [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(xgemm_config)]
 lib.xgemm_select_config.restype = _i32
 lib.xgemm_tile_info.argtypes = [_i32] + [ctypes.POINTER(ctypes.c_int)] * 4
@@ -120,6 +123,12 @@ def xgemm_run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream) -> int:
 def xgemm_run_config(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream, cfg) -> int:
     return lib.xgemm_run_config(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream,
                                 ctypes.byref(cfg) if cfg is not None else None)
+
+
+def xgemm_run_strided_batched(h, batch, M, N, K, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c,
+                              dtype, stream) -> int:
+    return lib.xgemm_run_strided_batched(h, batch, M, N, K, A, lda, stride_a, B, ldb, stride_b, C, ldc, stride_c,
+                                         dtype, stream)
 
 
 def xgemm_select_config(M, N, K, dtype, cu_count) -> xgemm_config:
@@ -191,6 +200,41 @@ def _ld(t) -> int:
     if t.shape[0] <= 1:
         return max(t.shape[1], t.stride(0))
     return t.stride(0)
+
+
+def bmm(A, B, out=None, stream=None):
+    """out[b] = A[b] @ B[b] (fp32) for 3-D tensors through xgemm_run_strided_batched.
+
+    A: (L, M, K), B: (L, K, N) bf16/fp16 CUDA tensors with contiguous rows (any
+    batch stride, including 0 for a broadcast operand); out: optional (L, M, N)
+    float32 tensor with contiguous rows.
+    """
+    import torch
+    if A.dim() != 3 or B.dim() != 3 or A.shape[0] != B.shape[0] or A.shape[2] != B.shape[1]:
+        raise ValueError("expected A (L, M, K) and B (L, K, N)")
+    if A.dtype != B.dtype:
+        raise TypeError("A and B must have the same dtype")
+    dtype = _dtype_code(A)
+    L, M, K = A.shape
+    N = B.shape[2]
+    if out is None:
+        out = torch.empty((L, M, N), dtype=torch.float32, device=A.device)
+    if out.dtype != torch.float32 or tuple(out.shape) != (L, M, N):
+        raise ValueError("out must be a float32 (L, M, N) tensor")
+    for t in (A, B, out):
+        if t.shape[2] > 1 and t.stride(2) != 1:
+            raise ValueError("rows must be contiguous")
+    s = stream if stream is not None else torch.cuda.current_stream(A.device)
+    h = handle(A.device.index)
+    lda = A.stride(1) if M > 1 else max(K, 1)
+    ldb = B.stride(1) if K > 1 else max(N, 1)
+    ldc = out.stride(1) if M > 1 else max(N, 1)
+    rc = xgemm_run_strided_batched(h, L, M, N, K, A.data_ptr() or None, lda, A.stride(0) if L > 1 else 0,
+                                   B.data_ptr() or None, ldb, B.stride(0) if L > 1 else 0,
+                                   out.data_ptr() or None, ldc, out.stride(0) if L > 1 else 0, dtype, s.cuda_stream)
+    if rc != XGEMM_OK:
+        raise XgemmError(rc, xgemm_last_error(h))
+    return out
 
 
 def gemm(A, B, out=None, config: xgemm_config | None = None, stream=None):

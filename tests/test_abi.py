@@ -135,3 +135,8 @@ def test_kernel_family_rules():
     assert fam(0, 8, 32) == -1
     bad = xg.xgemm_config(tile=7, split_k=1, group_m=4, tail_split=0)
     assert fam(8, 8, 32, c=bad) == -1
+
+
+def test_batched_null_handle():
+    assert xg.xgemm_run_strided_batched(None, 1, 1, 1, 1, None, 1, 0, None, 1, 0, None, 1, 0, 0, None) \
+        == xg.XGEMM_ERR_INVALID_ARG

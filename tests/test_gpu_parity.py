@@ -343,3 +343,94 @@ def test_full_size_8192_integer_exact_sampled():
     ri, ci = rng.integers(0, M, 4096), rng.integers(0, N, 4096)
     c, _ = oracle.gemm_entries(A, B, "bf16", ri, ci)
     check_exact(C[ri, ci][None], c[None], "int entries")
+
+
+# ---------------------------------------------------------------------------
+# strided batched products
+# ---------------------------------------------------------------------------
+
+def _batched_case(L, M, N, K, dtype, seed, shared_a=False):
+    As, Bs = [], []
+    for b in range(L):
+        A, B = wl.make_inputs(M, N, K, dtype, "uniform", seed=seed * 100 + b)
+        As.append(A)
+        Bs.append(B)
+    if shared_a:
+        As = [As[0]] * L
+    return As, Bs
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+@pytest.mark.parametrize("shape", [(3, 512, 264, 1024), (4, 300, 200, 100), (5, 64, 520, 320)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_strided_batched(dtype, shape):
+    L, M, N, K = shape
+    As, Bs = _batched_case(L, M, N, K, dtype, seed=L + M)
+    A = torch.stack([to_device(a, dtype) for a in As])
+    B = torch.stack([to_device(b, dtype) for b in Bs])
+    C = xg.bmm(A, B)
+    torch.cuda.synchronize()
+    C = C.cpu().numpy()
+    for b in range(L):
+        C_ref, S = oracle.gemm(As[b], Bs[b], dtype)
+        check_close(C[b], C_ref, S, "batch %d of %s" % (b, shape))
+
+
+def test_strided_batched_shared_a_and_padding():
+    L, M, N, K = 3, 260, 136, 448
+    As, Bs = _batched_case(L, M, N, K, "bf16", seed=7, shared_a=True)
+    h = xg.handle()
+    dA = to_device(As[0], "bf16")                         # stride_a = 0: one A for all
+    sb = K * N + 64                                       # padded batch stride for B
+    Bbuf = torch.zeros(L * sb, dtype=torch.bfloat16, device="cuda")
+    for b in range(L):
+        Bbuf[b * sb:b * sb + K * N] = to_device(Bs[b], "bf16").reshape(-1)
+    ldc, sc = N + 8, (M + 2) * (N + 8)                    # padded rows and batch stride for C
+    Cbuf = torch.full((L * sc,), 777.0, dtype=torch.float32, device="cuda")
+    rc = xg.xgemm_run_strided_batched(h, L, M, N, K, dA.data_ptr(), K, 0, Bbuf.data_ptr(), N, sb,
+                                      Cbuf.data_ptr(), ldc, sc, xg.XGEMM_BF16,
+                                      torch.cuda.current_stream().cuda_stream)
+    assert rc == xg.XGEMM_OK, xg.xgemm_last_error(h)
+    torch.cuda.synchronize()
+    Ch = Cbuf.cpu().numpy()
+    for b in range(L):
+        C_ref, S = oracle.gemm(As[0], Bs[b], "bf16")
+        blk = Ch[b * sc:b * sc + M * ldc].reshape(M, ldc)
+        check_close(blk[:, :N], C_ref, S, "shared-A batch %d" % b)
+        assert np.all(blk[:, N:] == 777.0)                # row padding untouched
+        assert np.all(Ch[b * sc + M * ldc:(b + 1) * sc] == 777.0)
+
+
+def test_strided_batched_integer_exact_and_single():
+    L, M, N, K = 2, 256, 256, 512
+    As, Bs = [], []
+    for b in range(L):
+        A, B = wl.make_int_inputs(M, N, K, "fp16", seed=b)
+        As.append(A)
+        Bs.append(B)
+    A = torch.stack([to_device(a, "fp16") for a in As])
+    B = torch.stack([to_device(b, "fp16") for b in Bs])
+    C = xg.bmm(A, B).cpu().numpy()
+    for b in range(L):
+        check_exact(C[b], oracle.gemm(As[b], Bs[b], "fp16")[0], "int batch %d" % b)
+    # batch of one equals the plain call
+    C1 = xg.bmm(A[:1], B[:1]).cpu().numpy()
+    check_exact(C1[0], oracle.gemm(As[0], Bs[0], "fp16")[0], "batch 1")
+
+
+def test_strided_batched_arguments():
+    h = xg.handle()
+    s = torch.cuda.current_stream().cuda_stream
+    A = torch.zeros((2, 64, 64), dtype=torch.bfloat16, device="cuda")
+    C = torch.zeros((2, 64, 64), dtype=torch.float32, device="cuda")
+    a, c = A.data_ptr(), C.data_ptr()
+    ok = xg.xgemm_run_strided_batched(h, 0, 64, 64, 64, a, 64, 4096, a, 64, 4096, c, 64, 4096, 0, s)
+    assert ok == xg.XGEMM_OK                                   # batch 0: no-op
+    bad = xg.xgemm_run_strided_batched(h, 2, 64, 64, 64, a, 64, 4096, a, 64, 4096, c, 64, 100, 0, s)
+    assert bad == xg.XGEMM_ERR_INVALID_ARG                     # overlapping outputs
+    bad = xg.xgemm_run_strided_batched(h, 2, 64, 64, 64, a, 64, -1, a, 64, 4096, c, 64, 4096, 0, s)
+    assert bad == xg.XGEMM_ERR_INVALID_ARG                     # negative stride
+    bad = xg.xgemm_run_strided_batched(h, -1, 64, 64, 64, a, 64, 4096, a, 64, 4096, c, 64, 4096, 0, s)
+    assert bad == xg.XGEMM_ERR_INVALID_ARG
+    torch.cuda.synchronize()
+    assert torch.all(C == 0)
