@@ -152,6 +152,9 @@ def main():
     ap.add_argument("--no-comparator", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="also run a plain device copy of this many bytes (counter calibration)")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="time xgemm_run_strided_batched on this many independent problems of the "
+                         "workload's shape instead of one xgemm_run (one JSON line, no baselines)")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
                     help="write profiles/counters_<workload>.json from rocprofv3 --pmc output and exit")
     args = ap.parse_args()
@@ -188,6 +191,35 @@ def main():
                           code, stream.cuda_stream)
         if rc != xg.XGEMM_OK:
             raise xg.XgemmError(rc, xg.xgemm_last_error(h))
+
+    if args.batch > 0:
+        # independent problems: the workload's A and B followed by re-seeded copies
+        L = args.batch
+        Ab = torch.empty((L, w.M, w.K), dtype=tdt, device=dev)
+        Bb = torch.empty((L, w.K, w.N), dtype=tdt, device=dev)
+        for b in range(L):
+            if b == 0:
+                Ab[0].copy_(A)
+                Bb[0].copy_(B)
+            else:
+                a_bits, b_bits = wl.make_inputs(w.M, w.N, w.K, w.dtype, w.dist, w.seed + 1000 * b, w.param)
+                Ab[b].copy_(torch.from_numpy(a_bits.view(np.int16)).to(dev).view(tdt))
+                Bb[b].copy_(torch.from_numpy(b_bits.view(np.int16)).to(dev).view(tdt))
+        Cb = torch.empty((L, w.M, w.N), dtype=torch.float32, device=dev)
+        for _ in range(args.warmup):
+            xg.bmm(Ab, Bb, out=Cb)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            xg.bmm(Ab, Bb, out=Cb)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) * 1e-3 / args.steps
+        print(json.dumps({"metric": "strided batched GEMM TFLOP/s", "value": round(L * w.flops / t / 1e12, 2),
+                          "unit": "TFLOP/s", "batch": L, "ms_per_step": round(t * 1e3, 4), "dtype": w.dtype,
+                          "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K}}), flush=True)
+        return
 
     for _ in range(args.warmup):
         step()
