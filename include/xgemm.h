@@ -45,7 +45,8 @@ enum xgemm_dtype {
 enum xgemm_status {
     XGEMM_OK = 0,
     XGEMM_ERR_INVALID_ARG = 1, /* bad size, leading dimension, pointer, dtype or config */
-    XGEMM_ERR_UNSUPPORTED = 2, /* the current device is not a gfx950 GPU */
+    XGEMM_ERR_UNSUPPORTED = 2, /* the current device is not a gfx950 GPU; for traces: a launch of the
+                                  general kernel family, which is not traced */
     XGEMM_ERR_ALLOC = 3,       /* the split-k workspace could not be allocated */
     XGEMM_ERR_HIP = 4          /* a HIP runtime call failed; see xgemm_last_error */
 };
@@ -181,6 +182,84 @@ int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t 
  * Host-only.  Returns 0 for invalid arguments.
  */
 size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, const xgemm_config *cfg);
+
+/*
+ * Synchronisation traces (host-only; touch no GPU).
+ *
+ * The paper checks its kernels' synchronisation by running an abstract
+ * machine over the program with concrete sizes: every shared-memory access
+ * leaves a read or mutate record, and fences, arrivals and waits raise the
+ * visibility of those records (Section 5, Abstract Machine).  These entry
+ * points provide the input for such a check of this library: they run the
+ * pipelined kernel's own body on the host, for one workgroup of a planned
+ * launch, with every hardware operation recorded as an event instead of
+ * executed.  A, B, C and W are only used as addresses (never dereferenced),
+ * so any values that satisfy the alignment of a real call may be passed.
+ */
+
+/* Event kinds of a workgroup trace. */
+enum xgemm_trace_op {
+    XGEMM_TRACE_LDS_LOAD = 0,  /* direct global-to-LDS load (vector-memory counter): the lane's
+                                  `arg` bytes at global address `addr` land at LDS offset
+                                  lds + arg * lane (lane = thread id % 64) */
+    XGEMM_TRACE_LDS_READ = 1,  /* LDS read (LDS counter) of `arg` bytes at LDS offset `lds` */
+    XGEMM_TRACE_WAIT_VM = 2,   /* s_waitcnt vmcnt(arg): all but the arg most recent vector-memory
+                                  operations of the wave have completed */
+    XGEMM_TRACE_WAIT_LGKM = 3, /* s_waitcnt lgkmcnt(arg), likewise for LDS operations */
+    XGEMM_TRACE_BARRIER = 4,   /* s_barrier across the workgroup */
+    XGEMM_TRACE_STORE = 5      /* global store (vector-memory counter) of `arg` bytes at `addr` */
+};
+
+/* One event of one thread.  LDS offsets count bytes from the start of the
+   workgroup's LDS allocation; global addresses are byte addresses. */
+typedef struct xgemm_trace_event {
+    int32_t op;   /* an xgemm_trace_op */
+    int32_t arg;  /* bytes per lane (accesses) or the wait count (waits) */
+    int64_t lds;  /* LDS offset (LDS_LOAD: the wave's base; LDS_READ: this lane's) */
+    int64_t addr; /* global byte address (LDS_LOAD source, STORE destination) */
+} xgemm_trace_event;
+
+/* One kernel launch of a planned call. */
+typedef struct xgemm_trace_info {
+    int32_t segments;        /* GEMM launches in the plan: 1, or 2 with a tail split */
+    int32_t family;          /* xgemm_kernel_family_id of this launch */
+    int32_t reduce;          /* 0: writes C; 1: full-matrix split partials in W, summed by a later
+                                launch; 2: tile-major split partials in W, likewise */
+    int32_t threads;         /* threads per workgroup */
+    int32_t lds_bytes;       /* LDS bytes per workgroup of the pipelined kernel (else 0) */
+    int32_t split;           /* split-k factor of this launch */
+    int64_t grid;            /* workgroups in this launch */
+    int64_t workspace_bytes; /* bytes of W the whole plan writes */
+    int32_t tile_base;       /* the launch covers logical tiles [tile_base, tile_base + tile_count) */
+    int32_t tile_count;
+} xgemm_trace_info;
+
+/*
+ * Launch `segment` (0 .. segments-1) of the plan xgemm_run_config would
+ * make for these arguments on a device with cu_count CUs.
+ * XGEMM_ERR_INVALID_ARG for invalid arguments (including M, N or K == 0,
+ * which launch no GEMM kernel), a segment out of range or info == NULL.
+ */
+int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+                     const float *C, int64_t ldc, const xgemm_config *cfg, int cu_count, int segment,
+                     xgemm_trace_info *info);
+
+/*
+ * Trace of workgroup `block` (0 .. grid-1) of launch `segment`: for each
+ * thread t (0 .. threads-1), its events in program order are written to
+ * out[t * capacity ...], at most `capacity` of them, and their number to
+ * counts[t] (counts has `threads` entries, the caller owns both arrays).  A
+ * count above capacity means the trace was cut; call again with a larger
+ * capacity (capacity 0 with out == NULL only counts).  W is the workspace
+ * address for launches that write partials (reduce != 0), else unused.
+ * XGEMM_ERR_UNSUPPORTED if the launch uses the general kernel family (only
+ * the pipelined kernel is traced); XGEMM_ERR_INVALID_ARG as
+ * xgemm_trace_plan, or for a block out of range, counts == NULL, or W ==
+ * NULL where it is needed.
+ */
+int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+                          float *C, int64_t ldc, float *W, const xgemm_config *cfg, int cu_count, int segment,
+                          int64_t block, xgemm_trace_event *out, int64_t capacity, int64_t *counts);
 
 /* Static description of a status code; never NULL. */
 const char *xgemm_strerror(int status);

@@ -105,12 +105,12 @@ __host__ __device__ __forceinline__ void logical_tile(int t, int tiles_m, int ti
 // in lexicographic order and leave other orders to future work, Section
 // 4.2.)
 // The batch index is outermost of all: the problems of a batch run one
-// after another across the grid.  Returns the workgroup's parameters with
-// A, B and C moved to its problem.
-__device__ __forceinline__ GemmParams map_tile(const GemmParams &p_in, int &tm, int &tn, int &ks, int &local)
+// after another across the grid.  w is the workgroup id and total the grid
+// size.  Returns the workgroup's parameters with A, B and C moved to its
+// problem.
+__host__ __device__ __forceinline__ GemmParams map_tile(const GemmParams &p_in, int w, int total, int &tm, int &tn,
+                                                       int &ks, int &local)
 {
-    const int total = gridDim.x;
-    const int w = blockIdx.x;
     const int per = total / kNumXcd;
     int lid = (w < per * kNumXcd) ? (w % kNumXcd) * per + w / kNumXcd : w;
     const int per_batch = p_in.tile_count * p_in.split;
@@ -137,7 +137,7 @@ struct OutView {
 };
 
 template <int BM, int BN>
-__device__ __forceinline__ OutView out_view(const GemmParams &p, int ks, int local, int m0, int n0)
+__host__ __device__ __forceinline__ OutView out_view(const GemmParams &p, int ks, int local, int m0, int n0)
 {
     OutView o;
     if (p.tile_major) {
@@ -213,7 +213,7 @@ gemm_kernel(GemmParams p_in)
     __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
 
     int tm, tn, ks, local;
-    const GemmParams p = map_tile(p_in, tm, tn, ks, local);
+    const GemmParams p = map_tile(p_in, blockIdx.x, gridDim.x, tm, tn, ks, local);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = ks * p.k_chunk;
     const int kend = min(p.K, kbeg + p.k_chunk);
@@ -477,15 +477,60 @@ __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0
 // r+8, r+12 get distinct slots; with 128-byte rows, two rows share a window
 // and rows of one parity within 16 get distinct slots.
 template <int ROWB>
-__device__ __forceinline__ int aswz(int r)
+__host__ __device__ __forceinline__ int aswz(int r)
 {
     static_assert(ROWB == 64 || ROWB == 128, "A row size");
     return ROWB == 64 ? ((r >> 2) & 3) : ((r >> 1) & 7);
 }
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT>
-__global__ void __launch_bounds__(WGM * WGN * 64, 1)
-gemm_kernel_dma(GemmParams p_in)
+// Operations of the pipelined kernel as the device executes them.  The
+// kernel body (dma_tile) issues every direct load, LDS read, MFMA, wait,
+// barrier and global store through such an object, so that the same body
+// can be run on the host with an object that records these operations
+// instead (the synchronisation checker replays the record).
+struct DeviceOps {
+    char *smem;
+    __device__ __forceinline__ char *lds() const { return smem; }
+    // LDS address of a pointer into the workgroup's LDS
+    __device__ __forceinline__ uint32_t lds_addr(const char *q) const { return lds_address(q); }
+    __device__ __forceinline__ int uniform(int x) const { return __builtin_amdgcn_readfirstlane(x); }
+    // 16 bytes per lane from gbase + goff to LDS address lds + 16 * lane
+    __device__ __forceinline__ void load16(const void *gbase, uint32_t goff, uint32_t lds) const
+    {
+        lds_load16(gbase, goff, lds);
+    }
+    __device__ __forceinline__ u32x4 read16(const char *q) const { return *(const u32x4 *)q; }
+    __device__ __forceinline__ v4i16 read_tr8(const char *q) const { return ds_read_tr16(q); }
+    template <int DT>
+    __device__ __forceinline__ f32x16 mfma(u32x4 a, u32x4 b, f32x16 c) const
+    {
+        return mfma32<DT>(a, b, c);
+    }
+    template <int N>
+    __device__ __forceinline__ void wait_vm() const
+    {
+        wait_vmcnt<N>();
+    }
+    __device__ __forceinline__ void wait_lgkm0() const { wait_lgkmcnt0(); }
+    __device__ __forceinline__ void barrier() const { barrier_only(); }
+    __device__ __forceinline__ void fence() const { sched_fence(); }
+    __device__ __forceinline__ void store4(float *q, f32x4 v) const { *(f32x4 *)q = v; }
+    __device__ __forceinline__ void store1(float *q, float v) const { *q = v; }
+};
+
+// LDS bytes the pipelined kernel allocates.
+template <int BM, int BN, int BK, int STAGES>
+constexpr int dma_lds_bytes()
+{
+    return STAGES * (BM * BK * 2 + BK * BN * 2);
+}
+
+// One workgroup (id `block` of `nblocks`) of the pipelined kernel, as seen
+// by thread `tid`.  The host launches it only when every split has at least
+// STAGES K steps.
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, class Ops>
+__host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmParams &p_in, int block, int nblocks,
+                                                  int tid)
 {
     constexpr int NW = WGM * WGN;
     constexpr int TM = BM / WGM, TN = BN / WGN;
@@ -507,20 +552,18 @@ gemm_kernel_dma(GemmParams p_in)
     static_assert(KS >= 2 && STAGES >= 2 && STAGES * STAGE <= 160 * 1024, "pipeline shape");
     static_assert((STAGES - 1) * LD < 64, "vmcnt range");
 
-    __shared__ __attribute__((aligned(1024))) char smem[STAGES * STAGE];
-
     int tm, tn, ks, local;
-    const GemmParams p = map_tile(p_in, tm, tn, ks, local);
+    const GemmParams p = map_tile(p_in, block, nblocks, tm, tn, ks, local);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = ks * p.k_chunk;
     const int kend = min(p.K, kbeg + p.k_chunk);
     const int nk = kend > kbeg ? (kend - kbeg) / BK : 0;
 
-    const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wave = ops.uniform(tid >> 6);
     const int wm = wave % WGM, wn = wave / WGM;
     const int64_t lda = p.lda, ldb = p.ldb;
+    char *const smem = ops.lds();
 
     // --- per-lane byte offsets of the direct loads (relative to the tile) ---
     uint32_t a_goff[A_LD], b_goff[B_LD];
@@ -545,14 +588,14 @@ gemm_kernel_dma(GemmParams p_in)
         const int k0 = kbeg + kstep * BK;
         const uint16_t *Ab = p.A + (int64_t)m0 * lda + k0;
         const uint16_t *Bb = p.B + (int64_t)k0 * ldb + n0;
-        const uint32_t sA = lds_address(smem) + stage * STAGE;
+        const uint32_t sA = ops.lds_addr(smem) + stage * STAGE;
         const uint32_t sB = sA + A_BYTES;
 #pragma unroll
         for (int j = 0; j < A_LD; ++j)
-            lds_load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
+            ops.load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
 #pragma unroll
         for (int j = 0; j < B_LD; ++j)
-            lds_load16(Bb, b_goff[j], sB + (wave * B_LD + j) * 1024);
+            ops.load16(Bb, b_goff[j], sB + (wave * B_LD + j) * 1024);
     };
 
     // --- fragment addressing ---
@@ -581,13 +624,13 @@ gemm_kernel_dma(GemmParams p_in)
 
     auto read_A = [&](int stage, int kk, int buf, int i) {
         const char *sA = smem + stage * STAGE + a_lane + (((2 * kk) ^ a_x) << 4);
-        fa[buf][i] = *(const u32x4 *)(sA + i * 32 * A_ROWB);
+        fa[buf][i] = ops.read16(sA + i * 32 * A_ROWB);
     };
     auto read_B = [&](int stage, int kk, int buf, int j) {
         const char *pb = smem + stage * STAGE + A_BYTES + kk * 16 * B_ROWB + b_lane +
                          (((b_blk0 + j) ^ t4) << 6);
-        const v4i16 lo = ds_read_tr16(pb);
-        const v4i16 hi = ds_read_tr16(pb + 4 * B_ROWB);
+        const v4i16 lo = ops.read_tr8(pb);
+        const v4i16 hi = ops.read_tr8(pb + 4 * B_ROWB);
         u32x4 v;
         v.x = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1));
         v.y = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3));
@@ -618,19 +661,19 @@ gemm_kernel_dma(GemmParams p_in)
     // MFMA n of a sub-step, row-major over the (i, j) blocks.
     auto mfma_n = [&](int buf, int n) {
         const int i = n / FN, j = n % FN;
-        acc[i][j] = mfma32<DT>(fb[buf][j], fa[buf][i], acc[i][j]);
+        acc[i][j] = ops.template mfma<DT>(fb[buf][j], fa[buf][i], acc[i][j]);
     };
 
     // Direct load j (0 .. LD-1) of K step u into LDS stage `stage`.
     auto load_j = [&](int u, int stage, int j) {
         const int k0 = kbeg + u * BK;
-        const uint32_t sA = lds_address(smem) + stage * STAGE;
+        const uint32_t sA = ops.lds_addr(smem) + stage * STAGE;
         if (j < A_LD) {
             const uint16_t *Ab = p.A + (int64_t)m0 * lda + k0;
-            lds_load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
+            ops.load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
         } else {
             const uint16_t *Bb = p.B + (int64_t)k0 * ldb + n0;
-            lds_load16(Bb, b_goff[j - A_LD], sA + A_BYTES + (wave * B_LD + (j - A_LD)) * 1024);
+            ops.load16(Bb, b_goff[j - A_LD], sA + A_BYTES + (wave * B_LD + (j - A_LD)) * 1024);
         }
     };
     // With three or more stages the loads of one K step are issued in two
@@ -644,7 +687,8 @@ gemm_kernel_dma(GemmParams p_in)
     constexpr int H1 = SPLIT ? (LD + 1) / 2 : LD;   // loads issued after the barrier
     constexpr int H2 = LD - H1;                      // loads issued before the next barrier
     constexpr int STEP1 = H1 > 0 ? (FM * FN) / H1 > 0 ? (FM * FN) / H1 : 1 : 1;
-    constexpr int STEP2 = H2 > 0 ? ((KS - 1) * FM * FN) / H2 > 0 ? ((KS - 1) * FM * FN) / H2 : 1 : 1;
+    constexpr int H2D = H2 > 0 ? H2 : 1;
+    constexpr int STEP2 = ((KS - 1) * FM * FN) / H2D > 0 ? ((KS - 1) * FM * FN) / H2D : 1;
 
     // One K step t.  LOAD1: issue the first half of step t+STAGES's loads
     // (into stage t, freed by this step's barrier).  LOAD2: issue the second
@@ -670,15 +714,15 @@ gemm_kernel_dma(GemmParams p_in)
                     if (gi % STEP2 == 0 && gi / STEP2 < H2)
                         load_j(t - 1 + STAGES, prev, H1 + gi / STEP2);
                 }
-                sched_fence();
+                ops.fence();
             }
         }
         // stage t fully read by this wave; stage t+1 landed for this wave
-        wait_lgkmcnt0();
+        ops.wait_lgkm0();
         if constexpr (WAIT >= 0)
-            wait_vmcnt<WAIT * LD>();
-        barrier_only();
-        sched_fence();
+            ops.template wait_vm<WAIT * LD>();
+        ops.barrier();
+        ops.fence();
         // last sub-step: its MFMAs, with the first-half loads of step
         // t+STAGES into the freed stage and the reads of step t+1's first
         // sub-step
@@ -700,19 +744,17 @@ gemm_kernel_dma(GemmParams p_in)
                         load_j(t + STAGES, stage, j);
                 }
             }
-            sched_fence();
+            ops.fence();
         }
     };
 
-    // The host launches this kernel only when every split has at least
-    // STAGES K steps.
     if (nk >= STAGES) {
         // prologue: fill every stage, wait for stage 0
 #pragma unroll
         for (int t = 0; t < STAGES; ++t)
             issue_loads(t, t);
-        wait_vmcnt<(STAGES - 1) * LD>();
-        barrier_only();
+        ops.template wait_vm<(STAGES - 1) * LD>();
+        ops.barrier();
         read_frags(0, 0, 0);
         if (nk > STAGES) {
             // step 0: the prologue issued all of step STAGES-1's loads
@@ -752,16 +794,25 @@ gemm_kernel_dma(GemmParams p_in)
                 v.z = acc[i][j][4 * q + 2];
                 v.w = acc[i][j][4 * q + 3];
                 if (vec_store) {
-                    *(f32x4 *)(Cb + (int64_t)(row - ov.r0) * ldc + (col - ov.c0)) = v;
+                    ops.store4(Cb + (int64_t)(row - ov.r0) * ldc + (col - ov.c0), v);
                 } else if (row < p.M) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         if (col + e < p.N)
-                            Cb[(int64_t)(row - ov.r0) * ldc + (col - ov.c0) + e] = v[e];
+                            ops.store1(Cb + (int64_t)(row - ov.r0) * ldc + (col - ov.c0) + e, v[e]);
                 }
             }
         }
     }
+}
+
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT>
+__global__ void __launch_bounds__(WGM * WGN * 64, 1)
+gemm_kernel_dma(GemmParams p_in)
+{
+    __shared__ __attribute__((aligned(1024))) char smem[dma_lds_bytes<BM, BN, BK, STAGES>()];
+    const DeviceOps ops{smem};
+    dma_tile<BM, BN, BK, STAGES, WGM, WGN, DT>(ops, p_in, blockIdx.x, gridDim.x, threadIdx.x);
 }
 
 // C[i][j] = sum over p of W[p][i][j], p ascending (a fixed order, so the

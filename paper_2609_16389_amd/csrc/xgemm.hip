@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <new>
+#include <vector>
 
 #include "xgemm.h"
 #include "gemm_kernel.hpp"
@@ -217,19 +218,37 @@ bool dma_eligible(const GemmParams &p, int bm)
            (int64_t)bm * p.lda * 2 < ((int64_t)1 << 32) && (int64_t)kDmaBK * p.ldb * 2 < ((int64_t)1 << 32);
 }
 
-hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int grid, hipStream_t s)
+// Template arguments of the pipelined kernel per tile (tile rows and
+// columns, K step, LDS stages, waves along M and N).  Launches and host
+// traces both take them from here, so a trace follows the kernel that runs.
+template <int BM_, int BN_, int STAGES_>
+struct DmaTile {
+    static constexpr int BM = BM_, BN = BN_, BK = kDmaBK, STAGES = STAGES_, WGM = 2, WGN = 2;
+};
+
+template <class F>
+auto with_dma_tile(int tile, F &&f)
 {
     switch (tile) {
-    case XGEMM_TILE_256x256:
-        return dma ? launch_dma<256, 256, kDmaBK, kDmaStages256x256, 2, 2>(dtype, p, grid, s)
-                   : launch_gemm<256, 256, 64, 2, 2>(dtype, p, grid, s);
-    case XGEMM_TILE_256x128:
-        return dma ? launch_dma<256, 128, kDmaBK, kDmaStages256x128, 2, 2>(dtype, p, grid, s)
-                   : launch_gemm<256, 128, 64, 2, 2>(dtype, p, grid, s);
-    case XGEMM_TILE_128x128:
-        return dma ? launch_dma<128, 128, kDmaBK, kDmaStages128x128, 2, 2>(dtype, p, grid, s)
-                   : launch_gemm<128, 128, 64, 2, 2>(dtype, p, grid, s);
-    default: return hipErrorInvalidValue;
+    case XGEMM_TILE_256x256: return f(DmaTile<256, 256, kDmaStages256x256>{});
+    case XGEMM_TILE_256x128: return f(DmaTile<256, 128, kDmaStages256x128>{});
+    default: return f(DmaTile<128, 128, kDmaStages128x128>{});
+    }
+}
+
+hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int grid, hipStream_t s)
+{
+    if (tile < 0 || tile >= XGEMM_TILE_COUNT)
+        return hipErrorInvalidValue;
+    if (dma)
+        return with_dma_tile(tile, [&](auto t) {
+            using T = decltype(t);
+            return launch_dma<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN>(dtype, p, grid, s);
+        });
+    switch (tile) {
+    case XGEMM_TILE_256x256: return launch_gemm<256, 256, 64, 2, 2>(dtype, p, grid, s);
+    case XGEMM_TILE_256x128: return launch_gemm<256, 128, 64, 2, 2>(dtype, p, grid, s);
+    default: return launch_gemm<128, 128, 64, 2, 2>(dtype, p, grid, s);
     }
 }
 
@@ -527,6 +546,71 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
     return XGEMM_OK;
 }
 
+// Host stand-in for the device operations of the pipelined kernel: each
+// call appends one event to the calling thread's trace instead of touching
+// memory.  LDS pointers point into a host buffer of the kernel's LDS size,
+// so LDS addresses are byte offsets from its start.
+struct TraceOps {
+    char *base;
+    std::vector<xgemm_trace_event> *ev;
+    char *lds() const { return base; }
+    uint32_t lds_addr(const char *q) const { return (uint32_t)(q - base); }
+    int uniform(int x) const { return x; }
+    void push(int op, int arg, int64_t lds, int64_t addr) const
+    {
+        xgemm_trace_event e;
+        e.op = op;
+        e.arg = arg;
+        e.lds = lds;
+        e.addr = addr;
+        ev->push_back(e);
+    }
+    void load16(const void *g, uint32_t goff, uint32_t lds) const
+    {
+        push(XGEMM_TRACE_LDS_LOAD, 16, lds, (int64_t)((uintptr_t)g + goff));
+    }
+    xgemm_dev::u32x4 read16(const char *q) const
+    {
+        push(XGEMM_TRACE_LDS_READ, 16, q - base, 0);
+        return xgemm_dev::u32x4{0, 0, 0, 0};
+    }
+    xgemm_dev::v4i16 read_tr8(const char *q) const
+    {
+        push(XGEMM_TRACE_LDS_READ, 8, q - base, 0);
+        return xgemm_dev::v4i16{0, 0, 0, 0};
+    }
+    template <int DT>
+    xgemm_dev::f32x16 mfma(xgemm_dev::u32x4, xgemm_dev::u32x4, xgemm_dev::f32x16 c) const
+    {
+        return c;
+    }
+    template <int N>
+    void wait_vm() const
+    {
+        push(XGEMM_TRACE_WAIT_VM, N, 0, 0);
+    }
+    void wait_lgkm0() const { push(XGEMM_TRACE_WAIT_LGKM, 0, 0, 0); }
+    void barrier() const { push(XGEMM_TRACE_BARRIER, 0, 0, 0); }
+    void fence() const {}
+    void store4(float *q, xgemm_dev::f32x4) const { push(XGEMM_TRACE_STORE, 16, 0, (int64_t)(uintptr_t)q); }
+    void store1(float *q, float) const { push(XGEMM_TRACE_STORE, 4, 0, (int64_t)(uintptr_t)q); }
+};
+
+// Plan of a traced call: the same checks and plan as xgemm_run_config.
+int trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+               const float *C, int64_t ldc, const xgemm_config *cfg, int cu_count, int segment, Plan *plan)
+{
+    if (!valid_config(cfg) || cu_count < 1 || M <= 0 || N <= 0 || K <= 0 || M >= kMaxDim || N >= kMaxDim ||
+        K >= kMaxDim || lda < K || ldb < N || ldc < N || !A || !B || !C)
+        return XGEMM_ERR_INVALID_ARG;
+    const int rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, *cfg, cu_count, plan);
+    if (rc != XGEMM_OK)
+        return rc;
+    if (segment < 0 || segment >= plan->nseg)
+        return XGEMM_ERR_INVALID_ARG;
+    return XGEMM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -640,12 +724,78 @@ size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, cons
     return plan.ws;
 }
 
+int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+                     const float *C, int64_t ldc, const xgemm_config *cfg, int cu_count, int segment,
+                     xgemm_trace_info *info)
+{
+    if (!info)
+        return XGEMM_ERR_INVALID_ARG;
+    Plan plan;
+    const int rc = trace_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, cu_count, segment, &plan);
+    if (rc != XGEMM_OK)
+        return rc;
+    const Segment &g = plan.seg[segment];
+    info->segments = plan.nseg;
+    info->family = g.dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
+    info->reduce = g.reduce;
+    info->threads = kTiles[plan.tile].threads;
+    info->lds_bytes = g.dma ? with_dma_tile(plan.tile, [](auto t) {
+        using T = decltype(t);
+        return xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>();
+    }) : 0;
+    info->split = g.p.split;
+    info->grid = g.grid;
+    info->workspace_bytes = (int64_t)plan.ws;
+    info->tile_base = g.p.tile_base;
+    info->tile_count = g.p.tile_count;
+    return XGEMM_OK;
+}
+
+int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+                          float *C, int64_t ldc, float *W, const xgemm_config *cfg, int cu_count, int segment,
+                          int64_t block, xgemm_trace_event *out, int64_t capacity, int64_t *counts)
+{
+    if (!counts || capacity < 0 || (capacity > 0 && !out))
+        return XGEMM_ERR_INVALID_ARG;
+    Plan plan;
+    int rc = trace_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, cu_count, segment, &plan);
+    if (rc != XGEMM_OK)
+        return rc;
+    Segment &g = plan.seg[segment];
+    if (block < 0 || block >= g.grid)
+        return XGEMM_ERR_INVALID_ARG;
+    if (!g.dma)
+        return XGEMM_ERR_UNSUPPORTED;
+    if (g.reduce) {
+        if (!W)
+            return XGEMM_ERR_INVALID_ARG;
+        g.p.C = W;
+    }
+    const int threads = kTiles[plan.tile].threads;
+    return with_dma_tile(plan.tile, [&](auto t) {
+        using T = decltype(t);
+        std::vector<char> lds(xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>());
+        std::vector<xgemm_trace_event> ev;
+        for (int tid = 0; tid < threads; ++tid) {
+            ev.clear();
+            const TraceOps ops{lds.data(), &ev};
+            xgemm_dev::dma_tile<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, 0>(ops, g.p, (int)block,
+                                                                                    (int)g.grid, tid);
+            counts[tid] = (int64_t)ev.size();
+            const int64_t n = counts[tid] < capacity ? counts[tid] : capacity;
+            if (n > 0)
+                memcpy(out + (int64_t)tid * capacity, ev.data(), (size_t)n * sizeof(xgemm_trace_event));
+        }
+        return (int)XGEMM_OK;
+    });
+}
+
 const char *xgemm_strerror(int status)
 {
     switch (status) {
     case XGEMM_OK: return "success";
     case XGEMM_ERR_INVALID_ARG: return "invalid argument";
-    case XGEMM_ERR_UNSUPPORTED: return "unsupported device (gfx950 required)";
+    case XGEMM_ERR_UNSUPPORTED: return "unsupported (device is not gfx950, or a launch the trace does not cover)";
     case XGEMM_ERR_ALLOC: return "workspace allocation failed";
     case XGEMM_ERR_HIP: return "HIP runtime error";
     default: return "unknown status";

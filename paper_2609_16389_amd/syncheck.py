@@ -1,0 +1,530 @@
+"""Synchronisation checker for the pipelined GEMM kernel: an abstract machine
+run over the kernel's own operation trace at concrete sizes.
+
+The paper makes every kernel's synchronisation checkable by interpreting an
+abstract machine over the program for concrete problem sizes (Section 5,
+Abstract Machine): each access to shared memory leaves a read or mutate
+record with a visibility level per thread, fences, barrier arrivals and
+waits raise those levels, and an access fails its check when an earlier
+conflicting record is not yet visible to the accessing thread.  Its
+evaluation times that interpreter over square GEMM sizes (Section 6).
+
+Here the same idea is applied to what gfx950 actually synchronises:
+
+* Records live on 8-byte granules of the workgroup's LDS allocation.  A
+  direct global-to-LDS load leaves a mutate record, an LDS read a read
+  record; each record remembers the wave that issued it and its position
+  in that wave's counter (vector memory for direct loads and stores, LDS
+  for LDS reads), because on this hardware an access completes
+  asynchronously and only ``s_waitcnt`` makes its completion known.
+* Visibility levels, lowest first: *in flight* (issued, not known to have
+  completed); *issuer-ordered* (the issuing wave's ``s_waitcnt`` retired
+  it, so it is ordered before that wave's later operations: the paper's
+  temporally ordered level for a single thread); *workgroup-ordered* (it
+  was issuer-ordered when its wave arrived at an ``s_barrier``, so it is
+  ordered before every wave's operations after that barrier: the paper's
+  fully ordered level).  ``s_waitcnt`` plays the role of the paper's Fence
+  and ``s_barrier`` of Arrive plus Await.
+* Checks (the paper's CheckReads / CheckMutates / CheckBarrier): a read
+  needs the location's mutate record visible to the reader (no
+  read-after-write race) and the location written at all; a direct load
+  needs every earlier read and mutate record of its locations visible to
+  its wave (no write-after-read or write-after-write race); every wave
+  must execute the same number of barriers; no direct load may still be in
+  flight when the wave exits (its LDS would be handed to the next
+  workgroup); every LDS access stays inside the allocation.
+
+Counters retire in issue order: ``s_waitcnt vmcnt(n)`` means all but the n
+most recent vector-memory operations of the wave have completed, and
+likewise for ``lgkmcnt``.  A record that the model cannot prove ordered is
+reported; the model never assumes an ordering the hardware does not
+guarantee (for example it ignores waits the compiler adds for register
+dependences, which can only make real executions safer).
+
+Barrier epochs are interpreted in lock step: all waves' operations between
+barrier e-1 and barrier e are checked before any after barrier e.  Two
+conflicting accesses in the same epoch from different waves are never
+ordered, and whichever is checked second fails, so the order in which
+waves are visited inside an epoch does not change the verdict.
+
+Beyond the LDS, ``check_launch`` checks each launch's global accesses: every
+direct load reads inside A or B, and the stores of all workgroups together
+write each element of the launch's output (C, or the split-k partials)
+exactly once and nothing else -- two workgroups of one launch are never
+ordered, so any overlap is a race.  Partials are summed by a later launch
+on the same stream, which the kernel boundary orders after all of them.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+import time
+
+import numpy as np
+
+from . import xgemm as xg
+
+GRANULE = 8          # bytes per LDS record location
+LANES = 64           # wavefront width
+
+LDS_LOAD = xg.XGEMM_TRACE_LDS_LOAD
+LDS_READ = xg.XGEMM_TRACE_LDS_READ
+WAIT_VM = xg.XGEMM_TRACE_WAIT_VM
+WAIT_LGKM = xg.XGEMM_TRACE_WAIT_LGKM
+BARRIER = xg.XGEMM_TRACE_BARRIER
+STORE = xg.XGEMM_TRACE_STORE
+
+
+@dataclasses.dataclass
+class Violation:
+    kind: str        # raw, war, waw, uninit, lds_bounds, barrier_count, inflight_exit, divergent,
+                     # unsupported, global_bounds, coverage
+    wave: int        # -1 when not tied to one wave
+    event: int       # index in the wave's event stream (-1 if none)
+    detail: str
+
+    def __str__(self):
+        return "%s (wave %d, event %d): %s" % (self.kind, self.wave, self.event, self.detail)
+
+
+@dataclasses.dataclass
+class WaveStream:
+    """One wave's operations in program order; per-lane fields are [n, 64]."""
+    op: np.ndarray     # [n] int32
+    arg: np.ndarray    # [n] int32
+    lds: np.ndarray    # [n, 64] int64
+    addr: np.ndarray   # [n, 64] int64
+
+
+def _drop_stores(events, counts):
+    """Per-thread traces without their global stores.  Stores under a lane
+    mask (edge tiles) make lanes of a wave issue different numbers of them;
+    they take part only in the global checks.  A vector-memory wait after a
+    store would make the store count matter for the wait, which these
+    traces never contain; it is reported rather than modelled."""
+    threads = events.shape[0]
+    valid = np.arange(events.shape[1])[None, :] < counts[:, None]
+    keep = valid & (events["op"] != STORE)
+    if (keep == valid).all():
+        return events, counts, False
+    first_store = np.where((valid & ~keep).any(axis=1), np.argmax(valid & ~keep, axis=1), events.shape[1])
+    after = np.arange(events.shape[1])[None, :] > first_store[:, None]
+    wait_after = bool((valid & after & (events["op"] == WAIT_VM)).any())
+    new_counts = keep.sum(axis=1)
+    out = np.zeros((threads, max(int(new_counts.max()), 1)), dtype=events.dtype)
+    for t in range(threads):
+        row = events[t][keep[t]]
+        out[t, :len(row)] = row
+    return out, new_counts, wait_after
+
+
+def wave_streams(events: np.ndarray, counts: np.ndarray, violations: list | None = None):
+    """Group a workgroup trace (threads x capacity records, per-thread
+    counts) into per-wave streams of its LDS loads, LDS reads, waits and
+    barriers.  Lanes of one wave must issue the same operations with the
+    same wave-uniform operands; a lane that does not is reported as a
+    divergence and the wave's stream is cut there."""
+    threads = events.shape[0]
+    assert threads % LANES == 0
+    events, counts, wait_after_store = _drop_stores(events, counts)
+    if wait_after_store and violations is not None:
+        violations.append(Violation("unsupported", -1, -1, "vector-memory wait after a global store"))
+    out = []
+    for w in range(threads // LANES):
+        lanes = slice(w * LANES, (w + 1) * LANES)
+        cnt = counts[lanes]
+        n = int(cnt.min())
+        if int(cnt.max()) != n and violations is not None:
+            violations.append(Violation("divergent", w, n, "lanes issue %d to %d operations" %
+                                        (n, int(cnt.max()))))
+        ev = events[lanes, :n]
+        op = ev["op"][0].copy()
+        arg = ev["arg"][0].copy()
+        same = (ev["op"] == op).all(axis=0) & (ev["arg"] == arg).all(axis=0)
+        uniform_lds = (op == LDS_LOAD)
+        same &= ~uniform_lds | (ev["lds"] == ev["lds"][0]).all(axis=0)
+        if not same.all():
+            cut = int(np.argmin(same))
+            if violations is not None:
+                violations.append(Violation("divergent", w, cut, "lanes disagree on the operation"))
+            n = cut
+            op, arg, ev = op[:n], arg[:n], ev[:, :n]
+        out.append(WaveStream(op=op, arg=arg, lds=np.ascontiguousarray(ev["lds"].T),
+                              addr=np.ascontiguousarray(ev["addr"].T)))
+    return out
+
+
+class LdsMachine:
+    """Abstract machine over one workgroup's LDS (see the module docstring)."""
+
+    def __init__(self, lds_bytes: int, nwaves: int, max_reports: int = 20):
+        self.lds_bytes = lds_bytes
+        self.nw = nwaves
+        g = (lds_bytes + GRANULE - 1) // GRANULE
+        self.mut_w = np.full(g, -1, dtype=np.int64)     # wave of the live mutate record
+        self.mut_s = np.full(g, -1, dtype=np.int64)     # its vector-memory counter position
+        self.rd_s = np.full((g, nwaves), -1, dtype=np.int64)  # latest read per wave since then
+        self.issued = {"vm": np.zeros(nwaves, np.int64), "lgkm": np.zeros(nwaves, np.int64)}
+        self.done = {"vm": np.zeros(nwaves, np.int64), "lgkm": np.zeros(nwaves, np.int64)}
+        self.seen = {"vm": np.zeros(nwaves, np.int64), "lgkm": np.zeros(nwaves, np.int64)}
+        self.last_load = np.full(nwaves, -1, dtype=np.int64)  # counter position of the last direct load
+        self.violations: list[Violation] = []
+        self.max_reports = max_reports
+        self.n_reported = {}
+
+    # -- helpers -------------------------------------------------------------
+    def _report(self, kind, wave, event, detail):
+        k = self.n_reported.get(kind, 0)
+        self.n_reported[kind] = k + 1
+        if k < self.max_reports:
+            self.violations.append(Violation(kind, wave, event, detail))
+
+    def _visible(self, counter, owner, pos, x):
+        """Records (owner wave, counter position) visible to wave x."""
+        return (pos < self.seen[counter][owner]) | ((owner == x) & (pos < self.done[counter][x]))
+
+    def _granules(self, wave, i, start, nbytes):
+        """Granules covered by per-lane accesses [start, start + nbytes)."""
+        if (start < 0).any() or (start + nbytes > self.lds_bytes).any():
+            bad = start[(start < 0) | (start + nbytes > self.lds_bytes)]
+            self._report("lds_bounds", wave, i, "LDS bytes [%d, %d) outside the %d-byte allocation" %
+                         (int(bad[0]), int(bad[0]) + nbytes, self.lds_bytes))
+            start = start[(start >= 0) & (start + nbytes <= self.lds_bytes)]
+        first = start // GRANULE
+        last = (start + nbytes - 1) // GRANULE
+        span = int((last - first).max()) + 1 if len(first) else 0
+        g = (first[:, None] + np.arange(span)[None, :])
+        g = g[g <= last[:, None]]
+        return np.unique(g)
+
+    # -- operations ----------------------------------------------------------
+    def lds_load(self, w, i, base, nbytes):
+        """Direct load: lane l writes nbytes at base + nbytes * l."""
+        g = self._granules(w, i, base + nbytes * np.arange(LANES, dtype=np.int64), nbytes)
+        mw = self.mut_w[g]
+        has = mw >= 0
+        if has.any():
+            ok = self._visible("vm", mw[has], self.mut_s[g][has], w)
+            if not ok.all():
+                bad = g[has][~ok][0]
+                self._report("waw", w, i, "LDS byte %d: earlier direct load by wave %d not ordered before "
+                             "this one" % (bad * GRANULE, int(self.mut_w[bad])))
+        rs = self.rd_s[g]                                     # [len(g), nw]
+        has = rs >= 0
+        if has.any():
+            owners = np.broadcast_to(np.arange(self.nw), rs.shape)[has]
+            ok = self._visible("lgkm", owners, rs[has], w)
+            if not ok.all():
+                rows, cols = np.nonzero(has)
+                k = int(np.argmin(ok))
+                self._report("war", w, i, "LDS byte %d: read by wave %d not complete and ordered before "
+                             "this direct load overwrites it" % (g[rows[k]] * GRANULE, int(cols[k])))
+        pos = self.issued["vm"][w]
+        self.mut_w[g] = w
+        self.mut_s[g] = pos
+        self.rd_s[g] = -1
+        self.last_load[w] = pos
+        self.issued["vm"][w] += 1
+
+    def lds_read(self, w, i, addrs, nbytes):
+        g = self._granules(w, i, addrs, nbytes)
+        mw = self.mut_w[g]
+        if (mw < 0).any():
+            bad = g[mw < 0][0]
+            self._report("uninit", w, i, "LDS byte %d read but never written" % (bad * GRANULE))
+        has = mw >= 0
+        if has.any():
+            ok = self._visible("vm", mw[has], self.mut_s[g][has], w)
+            if not ok.all():
+                bad = g[has][~ok][0]
+                self._report("raw", w, i, "LDS byte %d: direct load by wave %d not complete and ordered "
+                             "before this read" % (bad * GRANULE, int(self.mut_w[bad])))
+        self.rd_s[g, w] = self.issued["lgkm"][w]
+        self.issued["lgkm"][w] += 1
+
+    def wait(self, w, counter, n):
+        self.done[counter][w] = max(self.done[counter][w], self.issued[counter][w] - n)
+
+    def barrier(self):
+        for c in ("vm", "lgkm"):
+            self.seen[c] = self.done[c].copy()
+
+    # -- driver --------------------------------------------------------------
+    def run(self, waves: list[WaveStream]):
+        """Interpret every wave's stream; returns the violations found."""
+        assert len(waves) == self.nw
+        cuts = []
+        for ws in waves:
+            b = np.nonzero(ws.op == BARRIER)[0]
+            cuts.append(np.concatenate([[-1], b, [len(ws.op)]]))
+        nb = [len(c) - 2 for c in cuts]
+        if len(set(nb)) != 1:
+            self._report("barrier_count", -1, -1, "waves execute %s barriers (a workgroup barrier "
+                         "needs every wave)" % nb)
+        epochs = min(nb) + 1
+        for e in range(epochs):
+            for w, ws in enumerate(waves):
+                lo, hi = cuts[w][e] + 1, cuts[w][e + 1]
+                for i in range(lo, hi):
+                    op = ws.op[i]
+                    if op == LDS_LOAD:
+                        self.lds_load(w, i, int(ws.lds[i, 0]), int(ws.arg[i]))
+                    elif op == LDS_READ:
+                        self.lds_read(w, i, ws.lds[i], int(ws.arg[i]))
+                    elif op == WAIT_VM:
+                        self.wait(w, "vm", int(ws.arg[i]))
+                    elif op == WAIT_LGKM:
+                        self.wait(w, "lgkm", int(ws.arg[i]))
+            if e + 1 < epochs:
+                self.barrier()
+        for w in range(self.nw):
+            if self.last_load[w] >= self.done["vm"][w]:
+                self._report("inflight_exit", w, len(waves[w].op),
+                             "direct loads into LDS still in flight when the wave exits")
+        return self.violations
+
+
+def check_workgroup_lds(waves: list[WaveStream], lds_bytes: int) -> list[Violation]:
+    return LdsMachine(lds_bytes, len(waves)).run(waves)
+
+
+# ---------------------------------------------------------------------------
+# whole launches
+# ---------------------------------------------------------------------------
+
+# Stand-in addresses for traced calls: 16-byte aligned, far apart, never
+# dereferenced.
+BASE_A = 1 << 40
+BASE_B = 2 << 40
+BASE_C = 3 << 40
+BASE_W = 4 << 40
+
+
+@dataclasses.dataclass
+class LaunchReport:
+    shape: tuple
+    config: str
+    segments: int
+    workgroups: int
+    lds_classes: int         # distinct LDS operation streams interpreted
+    events: int              # operations traced (all threads)
+    seconds: float
+    violations: list
+
+    @property
+    def ok(self):
+        return not self.violations
+
+
+def trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, threads, capacity=None):
+    """(events [threads, capacity], counts [threads]) of one workgroup."""
+    import ctypes
+    counts = np.zeros(threads, dtype=np.int64)
+    cptr = counts.ctypes.data_as(ctypes.c_void_p)
+    args = (M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, BASE_W, ctypes.byref(cfg), cu_count, seg, block)
+    if capacity is None:
+        rc = xg.lib.xgemm_trace_workgroup(*args, None, 0, cptr)
+        if rc != xg.XGEMM_OK:
+            raise xg.XgemmError(rc)
+        capacity = max(int(counts.max()), 1)
+    ev = np.zeros((threads, capacity), dtype=xg.TRACE_EVENT_DTYPE)
+    rc = xg.lib.xgemm_trace_workgroup(*args, ev.ctypes.data_as(ctypes.c_void_p), capacity, cptr)
+    if rc != xg.XGEMM_OK:
+        raise xg.XgemmError(rc)
+    if int(counts.max()) > capacity:
+        return trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, threads, int(counts.max()))
+    return ev, counts
+
+
+class _Coverage:
+    """Counts how often each element of a launch's output is stored."""
+
+    def __init__(self, info, M, N, ldc, bm, bn):
+        self.reduce = info.reduce
+        self.M, self.N, self.ldc, self.bm, self.bn = M, N, ldc, bm, bn
+        self.split = info.split
+        if info.reduce == 0:
+            self.base, self.shape = BASE_C, (M, N)
+        elif info.reduce == 1:
+            self.ldw = (N + 3) // 4 * 4
+            self.base, self.shape = BASE_W, (info.split, M, N)
+        else:
+            self.base, self.shape = BASE_W, (info.split, info.tile_count, bm * bn)
+        self.count = np.zeros(self.shape, dtype=np.uint8)
+
+    def add(self, addr, nbytes):
+        """Record stores of nbytes at each address; returns a list of problems."""
+        bad = []
+        off = addr - self.base
+        if (off % 4).any():
+            bad.append("store not aligned to a float")
+        elem = off // 4
+        for k in range(nbytes // 4):
+            e = elem + k
+            if self.reduce == 0:
+                i, j = e // self.ldc, e % self.ldc
+                ok = (e >= 0) & (i < self.M) & (j < self.N)
+                idx = (i[ok], j[ok])
+            elif self.reduce == 1:
+                per = self.M * self.ldw
+                p, r = e // per, e % per
+                i, j = r // self.ldw, r % self.ldw
+                ok = (e >= 0) & (p < self.split) & (j < self.N)
+                idx = (p[ok], i[ok], j[ok])
+            else:
+                per = self.bm * self.bn
+                blk, r = e // per, e % per
+                p, t = blk // self.shape[1], blk % self.shape[1]
+                ok = (e >= 0) & (p < self.split)
+                idx = (p[ok], t[ok], r[ok])
+            if not ok.all():
+                bad.append("store outside the output at byte offset %d" % int(off[~ok][0] + 4 * k))
+            np.add.at(self.count, idx, 1)
+        return bad
+
+    def result(self):
+        zero = int((self.count == 0).sum())
+        many = int((self.count > 1).sum())
+        return zero, many
+
+
+def check_launch(M, N, K, cfg, cu_count=256, lda=None, ldb=None, ldc=None, max_blocks=None):
+    """Trace every workgroup of every launch of the plan for this call and
+    run the checks; returns a LaunchReport.  max_blocks limits the
+    workgroups traced per launch (for quick checks of large shapes; the
+    coverage check is then skipped)."""
+    lda = K if lda is None else lda
+    ldb = N if ldb is None else ldb
+    ldc = N if ldc is None else ldc
+    t0 = time.perf_counter()
+    violations: list[Violation] = []
+    lds_seen = set()
+    n_events = 0
+    n_blocks = 0
+    bm, bn, _, _ = xg.xgemm_tile_info(cfg.tile)
+    a_lo, a_hi = BASE_A, BASE_A + 2 * ((M - 1) * lda + K)
+    b_lo, b_hi = BASE_B, BASE_B + 2 * ((K - 1) * ldb + N)
+    info0 = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, 0)
+    c_cov = None
+    for seg in range(info0.segments):
+        info = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, seg)
+        if info.family != xg.XGEMM_KERNEL_PIPELINED:
+            raise xg.XgemmError(xg.XGEMM_ERR_UNSUPPORTED, "launch %d uses the general kernel, which is "
+                                "not traced" % seg)
+        cov = _Coverage(info, M, N, ldc, bm, bn)
+        if info.reduce == 0:
+            c_cov = cov
+        nblk = info.grid if max_blocks is None else min(info.grid, max_blocks)
+        for block in range(nblk):
+            ev, counts = trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, info.threads)
+            n_blocks += 1
+            n_events += int(counts.sum())
+            valid = np.arange(ev.shape[1])[None, :] < counts[:, None]
+            # global reads of the direct loads
+            ld = valid & (ev["op"] == LDS_LOAD)
+            ga = ev["addr"][ld]
+            nb = ev["arg"][ld]
+            inside = ((ga >= a_lo) & (ga + nb <= a_hi)) | ((ga >= b_lo) & (ga + nb <= b_hi))
+            if not inside.all():
+                violations.append(Violation("global_bounds", -1, -1, "launch %d workgroup %d: direct load "
+                                            "reads outside A and B at address %#x" %
+                                            (seg, block, int(ga[~inside][0]))))
+            # global stores
+            st = valid & (ev["op"] == STORE)
+            for nbytes in np.unique(ev["arg"][st]):
+                sel = st & (ev["arg"] == nbytes)
+                for msg in cov.add(ev["addr"][sel], int(nbytes)):
+                    violations.append(Violation("global_bounds", -1, -1, "launch %d workgroup %d: %s" %
+                                                (seg, block, msg)))
+            # LDS: one interpretation per distinct operation stream
+            key = hashlib.sha1()
+            for f in ("op", "arg", "lds"):
+                key.update(np.where(valid, ev[f], 0).tobytes())
+            key.update(counts.tobytes())
+            key = key.digest()
+            if key not in lds_seen:
+                lds_seen.add(key)
+                pre = []
+                waves = wave_streams(ev, counts, pre)
+                violations.extend(pre)
+                for v in check_workgroup_lds(waves, info.lds_bytes):
+                    v.detail = "launch %d workgroup %d: %s" % (seg, block, v.detail)
+                    violations.append(v)
+        if max_blocks is None:
+            zero, many = cov.result()
+            if info.reduce == 2 or info.reduce == 1 or info.reduce == 0:
+                if many:
+                    violations.append(Violation("coverage", -1, -1, "launch %d: %d output elements stored by "
+                                                "more than one store (unordered workgroups race)" % (seg, many)))
+                if zero and info.reduce != 0:
+                    violations.append(Violation("coverage", -1, -1, "launch %d: %d partial elements never "
+                                                "written" % (seg, zero)))
+    if max_blocks is None and c_cov is not None:
+        # C must be covered once by the direct launch plus the tiles whose
+        # partials a later launch sums (tail split): those are reported by
+        # the tile-partial coverage above, so only the direct launch's tiles
+        # are counted here.
+        zero, _ = c_cov.result()
+        expect_missing = 0
+        if info0.segments > 1:
+            info1 = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, 1)
+            expect_missing = _tile_elements(M, N, bm, bn, cfg.group_m, info1.tile_base, info1.tile_count)
+        if zero != expect_missing:
+            violations.append(Violation("coverage", -1, -1, "%d elements of C never written (expected %d left "
+                                        "to the partial sums)" % (zero, expect_missing)))
+    return LaunchReport(shape=(M, N, K), config=repr(cfg), segments=info0.segments, workgroups=n_blocks,
+                        lds_classes=len(lds_seen), events=n_events, seconds=time.perf_counter() - t0,
+                        violations=violations)
+
+
+def _tile_elements(M, N, bm, bn, group_m, first, count):
+    """Elements of C inside logical tiles [first, first + count)."""
+    tiles_m, tiles_n = -(-M // bm), -(-N // bn)
+    total = 0
+    for t in range(first, first + count):
+        group = group_m * tiles_n
+        g = t // group
+        first_m = g * group_m
+        gm = min(tiles_m - first_m, group_m)
+        r = t - g * group
+        tm, tn = first_m + r % gm, r // gm
+        total += (min(M, (tm + 1) * bm) - tm * bm) * (min(N, (tn + 1) * bn) - tn * bn)
+    return total
+
+
+def main(argv=None):
+    import argparse
+    ap = argparse.ArgumentParser(description="synchronisation check of the pipelined GEMM kernel")
+    ap.add_argument("M", type=int)
+    ap.add_argument("N", type=int)
+    ap.add_argument("K", type=int)
+    ap.add_argument("--tile", type=int, default=None)
+    ap.add_argument("--split", type=int, default=None)
+    ap.add_argument("--tail-split", type=int, default=0)
+    ap.add_argument("--group-m", type=int, default=None)
+    ap.add_argument("--cu-count", type=int, default=256)
+    ap.add_argument("--max-blocks", type=int, default=None)
+    args = ap.parse_args(argv)
+    cfg = xg.xgemm_select_config(args.M, args.N, args.K, xg.XGEMM_BF16, args.cu_count)
+    if args.tile is not None:
+        cfg.tile = args.tile
+    if args.split is not None:
+        cfg.split_k = args.split
+    if args.group_m is not None:
+        cfg.group_m = args.group_m
+    cfg.tail_split = args.tail_split
+    try:
+        rep = check_launch(args.M, args.N, args.K, cfg, args.cu_count, max_blocks=args.max_blocks)
+    except xg.XgemmError as e:
+        print("%s %r: not checked: %s" % ((args.M, args.N, args.K), cfg, e))
+        return 2
+    print("%s %s: %d launch(es), %d workgroups, %d LDS streams, %d events, %.2f s: %s" % (
+        rep.shape, rep.config, rep.segments, rep.workgroups, rep.lds_classes, rep.events, rep.seconds,
+        "OK" if rep.ok else "%d violation(s)" % len(rep.violations)))
+    for v in rep.violations[:20]:
+        print("  ", v)
+    return 0 if rep.ok else 1
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())

@@ -43,6 +43,26 @@ class xgemm_config(ctypes.Structure):
             self.tile, self.split_k, self.group_m, self.tail_split)
 
 
+XGEMM_TRACE_LDS_LOAD = 0
+XGEMM_TRACE_LDS_READ = 1
+XGEMM_TRACE_WAIT_VM = 2
+XGEMM_TRACE_WAIT_LGKM = 3
+XGEMM_TRACE_BARRIER = 4
+XGEMM_TRACE_STORE = 5
+
+
+class xgemm_trace_event(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("arg", ctypes.c_int32), ("lds", ctypes.c_int64),
+                ("addr", ctypes.c_int64)]
+
+
+class xgemm_trace_info(ctypes.Structure):
+    _fields_ = [("segments", ctypes.c_int32), ("family", ctypes.c_int32), ("reduce", ctypes.c_int32),
+                ("threads", ctypes.c_int32), ("lds_bytes", ctypes.c_int32), ("split", ctypes.c_int32),
+                ("grid", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
+                ("tile_base", ctypes.c_int32), ("tile_count", ctypes.c_int32)]
+
+
 class XgemmError(RuntimeError):
     def __init__(self, status: int, detail: str = ""):
         self.status = status
@@ -86,6 +106,12 @@ lib.xgemm_kernel_family.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, ctypes
 lib.xgemm_kernel_family.restype = _i32
 lib.xgemm_workspace_bytes.argtypes = [_i64, _i64, _i64, _i32, ctypes.POINTER(xgemm_config)]
 lib.xgemm_workspace_bytes.restype = ctypes.c_size_t
+lib.xgemm_trace_plan.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, ctypes.POINTER(xgemm_config),
+                                 _i32, _i32, ctypes.POINTER(xgemm_trace_info)]
+lib.xgemm_trace_plan.restype = _i32
+lib.xgemm_trace_workgroup.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _p,
+                                      ctypes.POINTER(xgemm_config), _i32, _i32, _i64, _p, _i64, _p]
+lib.xgemm_trace_workgroup.restype = _i32
 lib.xgemm_strerror.argtypes = [_i32]
 lib.xgemm_strerror.restype = ctypes.c_char_p
 lib.xgemm_last_error.argtypes = [_handle_t]
@@ -153,6 +179,44 @@ def xgemm_kernel_family(M, N, K, A, lda, B, ldb, cfg) -> int:
 
 def xgemm_workspace_bytes(M, N, K, cu_count, cfg) -> int:
     return int(lib.xgemm_workspace_bytes(M, N, K, cu_count, ctypes.byref(cfg)))
+
+
+def xgemm_trace_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, cu_count, segment) -> xgemm_trace_info:
+    """Launch `segment` of the plan for these arguments; raises XgemmError."""
+    info = xgemm_trace_info()
+    rc = lib.xgemm_trace_plan(M, N, K, A, lda, B, ldb, C, ldc, ctypes.byref(cfg), cu_count, segment,
+                              ctypes.byref(info))
+    if rc != XGEMM_OK:
+        raise XgemmError(rc)
+    return info
+
+
+# numpy layout of xgemm_trace_event
+TRACE_EVENT_DTYPE = [("op", "<i4"), ("arg", "<i4"), ("lds", "<i8"), ("addr", "<i8")]
+
+
+def xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, cfg, cu_count, segment, block, threads,
+                          capacity=None):
+    """Events of every thread of one workgroup: a list of `threads` numpy
+    record arrays (fields op, arg, lds, addr).  Raises XgemmError."""
+    import numpy as np
+    counts = np.zeros(threads, dtype=np.int64)
+    cptr = counts.ctypes.data_as(ctypes.c_void_p)
+    if capacity is None:
+        rc = lib.xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, ctypes.byref(cfg), cu_count,
+                                       segment, block, None, 0, cptr)
+        if rc != XGEMM_OK:
+            raise XgemmError(rc)
+        capacity = int(counts.max())
+    out = np.zeros((threads, max(capacity, 1)), dtype=TRACE_EVENT_DTYPE)
+    rc = lib.xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, ctypes.byref(cfg), cu_count, segment,
+                                   block, out.ctypes.data_as(ctypes.c_void_p), out.shape[1], cptr)
+    if rc != XGEMM_OK:
+        raise XgemmError(rc)
+    if int(counts.max()) > out.shape[1]:
+        return xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, cfg, cu_count, segment, block,
+                                     threads, int(counts.max()))
+    return [out[t, :counts[t]] for t in range(threads)]
 
 
 def xgemm_strerror(status: int) -> str:

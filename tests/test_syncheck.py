@@ -1,0 +1,310 @@
+"""Synchronisation checker (the abstract machine over the pipelined kernel's
+own trace, Section 5 of the paper).
+
+1. The machine is pinned on hand-built wave programs whose verdicts follow
+   from the hardware's ordering rules (a wait retires the issuing wave's
+   operations; a barrier orders what each wave had retired before arriving).
+2. The kernel's traces pass at concrete sizes: every tile, pipeline depths
+   from the minimum up, ragged edges, padded leading dimensions, split-k and
+   the tail split.
+3. Planted mistakes in a real trace (a wait too weak, a missing LDS wait, a
+   missing or unmatched barrier, a read hoisted above its barrier, output
+   written twice, a load outside A and B) are all caught.
+CPU only: the traces come from the library's host-side replay of the kernel
+body, no GPU is touched."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import paper_2609_16389_amd.xgemm as xg
+from paper_2609_16389_amd import syncheck as sc
+
+LANE = np.arange(64, dtype=np.int64)
+LDS = 4096
+
+
+def prog(*ops):
+    """A wave program: ('load', base) a 16-byte direct load per lane to
+    base + 16*lane; ('read', base) a 16-byte read per lane at base +
+    16*lane; ('read8', addrs) an 8-byte read at per-lane addrs; ('wvm', n),
+    ('wlgkm', n); ('bar',)."""
+    op, arg, lds = [], [], []
+    for o in ops:
+        k = o[0]
+        if k == "load":
+            op.append(sc.LDS_LOAD); arg.append(16); lds.append(np.full(64, o[1]))
+        elif k == "read":
+            op.append(sc.LDS_READ); arg.append(16); lds.append(o[1] + 16 * LANE)
+        elif k == "read8":
+            op.append(sc.LDS_READ); arg.append(8); lds.append(np.asarray(o[1], dtype=np.int64))
+        elif k == "wvm":
+            op.append(sc.WAIT_VM); arg.append(o[1]); lds.append(np.zeros(64))
+        elif k == "wlgkm":
+            op.append(sc.WAIT_LGKM); arg.append(o[1]); lds.append(np.zeros(64))
+        elif k == "bar":
+            op.append(sc.BARRIER); arg.append(0); lds.append(np.zeros(64))
+        else:
+            raise ValueError(k)
+    n = len(op)
+    return sc.WaveStream(op=np.array(op, dtype=np.int32), arg=np.array(arg, dtype=np.int32),
+                         lds=np.array(lds, dtype=np.int64).reshape(n, 64), addr=np.zeros((n, 64), np.int64))
+
+
+def verdict(*waves, lds=LDS):
+    return {v.kind for v in sc.check_workgroup_lds(list(waves), lds)}
+
+
+# ---------------------------------------------------------------------------
+# 1. the machine on programs with known verdicts
+# ---------------------------------------------------------------------------
+
+def test_load_wait_barrier_read_is_ordered():
+    assert verdict(prog(("load", 0), ("wvm", 0), ("bar",)),
+                   prog(("bar",), ("read", 0))) == set()
+
+
+def test_missing_wait_is_a_read_after_write_race():
+    assert verdict(prog(("load", 0), ("bar",)),
+                   prog(("bar",), ("read", 0))) == {"raw", "inflight_exit"}
+
+
+def test_wait_after_the_barrier_does_not_order_other_waves():
+    assert verdict(prog(("load", 0), ("bar",), ("wvm", 0)),
+                   prog(("bar",), ("read", 0))) == {"raw"}
+
+
+def test_missing_barrier_is_a_race_even_with_the_wait():
+    assert verdict(prog(("load", 0), ("wvm", 0)),
+                   prog(("read", 0))) == {"raw"}
+
+
+def test_race_found_whichever_wave_is_visited_first():
+    w_load = prog(("load", 0), ("wvm", 0))
+    w_read = prog(("read", 0))
+    assert "raw" in verdict(w_load, w_read)
+    # reader visited first: it sees no write (uninit), then the write finds
+    # an unordered read of its location
+    assert {"uninit", "war"} <= verdict(w_read, w_load)
+
+
+def test_own_load_needs_only_the_wait():
+    assert verdict(prog(("load", 0), ("wvm", 0), ("read", 0))) == set()
+    assert verdict(prog(("load", 0), ("read", 0), ("wvm", 0))) == {"raw"}
+
+
+def test_vmcnt_retires_all_but_the_most_recent():
+    # two loads, vmcnt(1): the first has landed, the second may not have
+    assert verdict(prog(("load", 0), ("load", 1024), ("wvm", 1), ("read", 0), ("wvm", 0))) == set()
+    assert verdict(prog(("load", 0), ("load", 1024), ("wvm", 1), ("read", 1024), ("wvm", 0))) == {"raw"}
+
+
+def test_overwrite_after_reads_needs_their_completion_and_a_barrier():
+    setup = (("load", 0), ("wvm", 0), ("bar",))
+    ok = verdict(prog(*setup, ("bar",), ("load", 0), ("wvm", 0)),
+                 prog(("bar",), ("read", 0), ("wlgkm", 0), ("bar",)))
+    assert ok == set()
+    no_lgkm = verdict(prog(*setup, ("bar",), ("load", 0), ("wvm", 0)),
+                      prog(("bar",), ("read", 0), ("bar",)))
+    assert no_lgkm == {"war"}
+    no_barrier = verdict(prog(*setup, ("load", 0), ("wvm", 0), ("bar",)),
+                         prog(("bar",), ("read", 0), ("wlgkm", 0), ("bar",)))
+    assert "war" in no_barrier or "raw" in no_barrier
+
+
+def test_two_unordered_loads_to_one_location():
+    assert verdict(prog(("load", 0), ("wvm", 0)), prog(("load", 0), ("wvm", 0))) == {"waw"}
+    assert verdict(prog(("load", 0), ("wvm", 0), ("bar",)),
+                   prog(("bar",), ("load", 0), ("wvm", 0))) == set()
+
+
+def test_read_of_unwritten_lds():
+    assert verdict(prog(("read", 0))) == {"uninit"}
+    # partial coverage: the load covers bytes 0..1023, the read 1024..2047
+    assert verdict(prog(("load", 0), ("wvm", 0), ("read", 1024))) == {"uninit"}
+
+
+def test_unmatched_barriers():
+    assert "barrier_count" in verdict(prog(("bar",)), prog())
+
+
+def test_load_in_flight_at_exit():
+    assert verdict(prog(("load", 0))) == {"inflight_exit"}
+
+
+def test_lds_bounds():
+    assert "lds_bounds" in verdict(prog(("load", LDS - 16), ("wvm", 0)))
+    assert "lds_bounds" in verdict(prog(("load", 0), ("wvm", 0), ("read8", np.full(64, -8))))
+
+
+def test_per_lane_read_granules():
+    # 8-byte reads touch one granule each: reading only the first half of
+    # what was loaded is fine, one byte past it is not
+    assert verdict(prog(("load", 0), ("wvm", 0), ("read8", 8 * LANE))) == set()
+    assert verdict(prog(("load", 0), ("wvm", 0), ("read8", 1024 + 0 * LANE))) == {"uninit"}
+
+
+# ---------------------------------------------------------------------------
+# 2. the kernel's own traces
+# ---------------------------------------------------------------------------
+
+def cfg(tile, split=1, group_m=4, tail_split=0):
+    return xg.xgemm_config(tile, split, group_m, tail_split)
+
+
+def stages(tile):
+    info = xg.xgemm_trace_plan(512, 512, 64 * 8, sc.BASE_A, 512, sc.BASE_B, 512, sc.BASE_C, 512, cfg(tile),
+                               256, 0)
+    bm, bn, bk, _ = xg.xgemm_tile_info(tile)
+    return info.lds_bytes // (2 * bk * (bm + bn))
+
+
+@pytest.mark.parametrize("tile", [0, 1, 2])
+def test_kernel_trace_structure(tile):
+    """Per wave: one barrier after the prologue and one per K step, and the
+    direct loads of every K step exactly once."""
+    bm, bn, bk, threads = xg.xgemm_tile_info(tile)
+    nk = stages(tile) + 3
+    K = nk * bk
+    ev, counts = sc.trace_workgroup(bm, bn, K, K, bn, bn, cfg(tile), 256, 0, 0, threads)
+    waves = sc.wave_streams(ev, counts)
+    loads_per_step = (bm + bn) * bk * 2 // 1024 // len(waves)
+    for ws in waves:
+        assert (ws.op == sc.BARRIER).sum() == nk + 1
+        assert (ws.op == sc.LDS_LOAD).sum() == nk * loads_per_step
+    # every byte of every stage is loaded once per step that uses it
+    base = np.concatenate([ws.lds[ws.op == sc.LDS_LOAD, 0] for ws in waves])
+    per_stage = np.bincount(base // 1024, minlength=stages(tile) * (bm + bn) * bk * 2 // 1024)
+    assert per_stage.sum() == nk * loads_per_step * len(waves)
+
+
+@pytest.mark.parametrize("tile", [0, 1, 2])
+@pytest.mark.parametrize("extra", [0, 1, 2, 5])
+def test_kernel_pipeline_depths_are_race_free(tile, extra):
+    bm, bn, bk, _ = xg.xgemm_tile_info(tile)
+    nk = max(stages(tile), 3) + extra
+    rep = sc.check_launch(bm, bn, nk * bk, cfg(tile))
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+@pytest.mark.parametrize("shape,tile", [((255, 264, 512), 2), ((1000, 1000, 1024), 1), ((264, 520, 320), 0),
+                                        ((130, 136, 192), 0)])
+def test_kernel_ragged_edges(shape, tile):
+    rep = sc.check_launch(*shape, cfg(tile))
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+def test_kernel_padded_leading_dimensions():
+    rep = sc.check_launch(300, 264, 448, cfg(2), lda=448 + 72, ldb=264 + 8, ldc=264 + 12)
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+@pytest.mark.parametrize("tile,split", [(2, 4), (1, 2), (0, 3)])
+def test_kernel_split_k_partials(tile, split):
+    bm, bn, bk, _ = xg.xgemm_tile_info(tile)
+    rep = sc.check_launch(bm + 40, bn * 2, split * 3 * bk, cfg(tile, split))
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+def test_kernel_tail_split():
+    # 3 x 3 tiles of 128 x 128 on a 2-CU device (4 slots): one tail tile
+    # runs as a second launch with 4-way split partials
+    rep = sc.check_launch(384, 384, 64 * 16, cfg(2, 1, 4, 4), cu_count=2)
+    assert rep.segments == 2
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+def test_general_family_is_not_traced():
+    with pytest.raises(xg.XgemmError):
+        sc.check_launch(100, 100, 100, cfg(2))  # K not a multiple of 64: general kernel
+
+
+# ---------------------------------------------------------------------------
+# 3. planted mistakes in a real trace
+# ---------------------------------------------------------------------------
+
+def real_waves(tile, extra=3):
+    bm, bn, bk, threads = xg.xgemm_tile_info(tile)
+    nk = max(stages(tile), 3) + extra
+    ev, counts = sc.trace_workgroup(bm, bn, nk * bk, nk * bk, bn, bn, cfg(tile), 256, 0, 0, threads)
+    info = xg.xgemm_trace_plan(bm, bn, nk * bk, sc.BASE_A, nk * bk, sc.BASE_B, bn, sc.BASE_C, bn, cfg(tile), 256, 0)
+    return sc.wave_streams(ev, counts), info.lds_bytes
+
+
+def edit(ws, keep=None, arg=None):
+    op, a, lds, addr = ws.op.copy(), ws.arg.copy(), ws.lds.copy(), ws.addr.copy()
+    if arg is not None:
+        a = arg(op, a)
+    if keep is not None:
+        k = keep(op)
+        op, a, lds, addr = op[k], a[k], lds[k], addr[k]
+    return sc.WaveStream(op=op, arg=a, lds=lds, addr=addr)
+
+
+def nth(op, kind, n):
+    return np.nonzero(op == kind)[0][n]
+
+
+MUTANTS = {
+    "vmcnt one too weak": lambda w, ws: edit(ws, arg=lambda op, a: np.where(op == sc.WAIT_VM, a + 1, a)),
+    "no LDS waits": lambda w, ws: edit(ws, keep=lambda op: op != sc.WAIT_LGKM),
+    "no vector-memory waits": lambda w, ws: edit(ws, keep=lambda op: op != sc.WAIT_VM),
+    "third barrier dropped": lambda w, ws: edit(ws, keep=lambda op: np.arange(len(op)) != nth(op, sc.BARRIER, 2)),
+    "one wave skips a barrier": lambda w, ws: ws if w else edit(
+        ws, keep=lambda op: np.arange(len(op)) != nth(op, sc.BARRIER, 3)),
+}
+
+
+@pytest.mark.parametrize("tile", [0, 1])
+def test_unmutated_trace_passes(tile):
+    waves, lds = real_waves(tile)
+    assert sc.check_workgroup_lds(waves, lds) == []
+
+
+@pytest.mark.parametrize("tile", [0, 1])
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_schedule_mistakes_are_caught(tile, name):
+    waves, lds = real_waves(tile)
+    mutated = [MUTANTS[name](w, ws) for w, ws in enumerate(waves)]
+    found = {v.kind for v in sc.check_workgroup_lds(mutated, lds)}
+    assert found, name
+
+
+@pytest.mark.parametrize("tile", [0, 1])
+def test_read_hoisted_above_its_barrier_is_caught(tile):
+    waves, lds = real_waves(tile)
+    out = []
+    for ws in waves:
+        b = nth(ws.op, sc.BARRIER, 3)
+        r = b + 1 + int(np.argmax(ws.op[b + 1:] == sc.LDS_READ))
+        order = np.arange(len(ws.op))
+        order[b], order[r] = r, b          # the first read after the barrier moves before it
+        out.append(sc.WaveStream(op=ws.op[order], arg=ws.arg[order], lds=ws.lds[order], addr=ws.addr[order]))
+    assert {v.kind for v in sc.check_workgroup_lds(out, lds)} & {"raw", "war"}
+
+
+def test_duplicate_workgroup_output_is_caught(monkeypatch):
+    real = sc.trace_workgroup
+    monkeypatch.setattr(sc, "trace_workgroup",
+                        lambda M, N, K, lda, ldb, ldc, c, cu, seg, block, threads, capacity=None:
+                        real(M, N, K, lda, ldb, ldc, c, cu, seg, 0, threads, capacity))
+    rep = sc.check_launch(512, 512, 256, cfg(0))
+    assert "coverage" in {v.kind for v in rep.violations}
+
+
+def test_load_outside_a_and_b_is_caught(monkeypatch):
+    real = sc.trace_workgroup
+
+    def shifted(*args, **kw):
+        ev, counts = real(*args, **kw)
+        ev = ev.copy()
+        ev["addr"] = np.where(ev["op"] == sc.LDS_LOAD, ev["addr"] + 2 * 256 * 256, ev["addr"])
+        return ev, counts
+    monkeypatch.setattr(sc, "trace_workgroup", shifted)
+    rep = sc.check_launch(256, 256, 256, cfg(0))
+    assert "global_bounds" in {v.kind for v in rep.violations}
+
+
+def test_cli_reports_ok(capsys):
+    assert sc.main(["256", "512", "448", "--tile", "0", "--split", "1"]) == 0
+    assert "OK" in capsys.readouterr().out
