@@ -1,15 +1,19 @@
-"""Oracle for the dense 16-bit GEMM hot path (C = A*B, fp64 evaluation).
+"""Oracles for the dense 16-bit GEMM hot path (C = A*B) and the fp32 GEMV
+(y = A*x), both evaluated in fp64.
 
 TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the CPU-baseline
 leg of the benchmark may import this package; the product library never does.
 It shares no code with the GPU path.  Inputs are the stored 16-bit bit patterns
 (numpy ``uint16`` arrays, row-major); outputs are fp64.
 
-The arithmetic lives in ``gemm_oracle.c`` (plain C, OpenMP over rows), which
-``build()`` compiles with gcc into ``liboracle.so`` next to this file.  The
-definition it follows is the plain one the paper's sequential GEMM program
-states (Introduction; Section 2.3): C[i][j] = sum_k A[i][k] * B[k][j], summed in
-ascending k, together with the tolerance scale S[i][j] = sum_k |A[i][k]*B[k][j]|.
+The arithmetic lives in ``gemm_oracle.c`` and ``gemv_oracle.c`` (plain C,
+OpenMP over rows), which ``build()`` compiles with gcc into ``liboracle.so``
+next to this file.  The GEMM definition is the plain one the paper's
+sequential GEMM program states (Introduction; Section 2.3): C[i][j] = sum_k
+A[i][k] * B[k][j], summed in ascending k, together with the tolerance scale
+S[i][j] = sum_k |A[i][k]*B[k][j]|.  The GEMV is the paper's fp32
+matrix-vector benchmark (Section 6): y[i] = sum_k A[i][k] * x[k] with
+s[i] = sum_k |A[i][k]*x[k]|, A and x given as float32 arrays.
 """
 from __future__ import annotations
 
@@ -20,7 +24,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "gemm_oracle.c")
+_SRC = [os.path.join(_HERE, "gemm_oracle.c"), os.path.join(_HERE, "gemv_oracle.c")]
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 
 BF16 = 0
@@ -31,12 +35,12 @@ _lib = None
 
 
 def build(force: bool = True) -> str:
-    """Compile ``gemm_oracle.c`` into ``liboracle.so`` (gcc, OpenMP, no fast-math)."""
+    """Compile the oracle sources into ``liboracle.so`` (gcc, OpenMP, no fast-math)."""
     if not force and os.path.exists(_LIB_PATH):
         return _LIB_PATH
     tmp = _LIB_PATH + ".tmp%d" % os.getpid()
     cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
-           "-ffp-contract=off", "-fno-fast-math", _SRC, "-o", tmp, "-lm"]
+           "-ffp-contract=off", "-fno-fast-math"] + _SRC + ["-o", tmp, "-lm"]
     subprocess.run(cmd, check=True)
     os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
@@ -62,6 +66,10 @@ def _load():
     lib.oracle_gemm_rows.restype = i32
     lib.oracle_gemm_entries.argtypes = [i64, i64, i64, p, i64, p, i64, i32, p, p, i64, p, p, i32]
     lib.oracle_gemm_entries.restype = i32
+    lib.oracle_gemv_rows.argtypes = [i64, i64, p, i64, p, p, i64, p, p, i32]
+    lib.oracle_gemv_rows.restype = i32
+    lib.oracle_gemv.argtypes = [i64, i64, p, i64, p, p, p, i32]
+    lib.oracle_gemv.restype = i32
     lib.oracle_thread_count.argtypes = [i32]
     lib.oracle_thread_count.restype = i32
     _lib = lib
@@ -171,3 +179,48 @@ def gemm_entries(A: np.ndarray, B: np.ndarray, dtype, rows, cols, nthreads: int 
 def thread_count(nthreads: int = 0) -> int:
     """Threads an oracle call with this ``nthreads`` argument runs on."""
     return int(_load().oracle_thread_count(nthreads))
+
+
+def _as_f32_matrix(A: np.ndarray):
+    if A.dtype != np.float32 or A.ndim != 2:
+        raise TypeError("A must be a 2-D float32 array")
+    if A.size and A.shape[1] > 1 and A.strides[1] != 4:
+        raise ValueError("A must have unit stride along its rows")
+    if A.size == 0 or A.shape[0] == 1:
+        lda = max(A.shape[1], A.strides[0] // 4 if A.size else 0)
+    else:
+        lda = A.strides[0] // 4
+    return A, lda
+
+
+def _as_f32_vector(x: np.ndarray, K: int) -> np.ndarray:
+    if x.dtype != np.float32 or x.ndim != 1 or x.shape[0] != K:
+        raise TypeError("x must be a float32 vector of %d values" % K)
+    return np.ascontiguousarray(x)
+
+
+def gemv(A: np.ndarray, x: np.ndarray, nthreads: int = 0):
+    """y = A x for float32 A (M x K, may be a row-padded view) and x (K).
+    Returns (y, s), fp64 of shape (M,)."""
+    A, lda = _as_f32_matrix(A)
+    M, K = A.shape
+    x = _as_f32_vector(x, K)
+    y = np.empty(M, dtype=np.float64)
+    s = np.empty(M, dtype=np.float64)
+    rc = _load().oracle_gemv(M, K, _ptr(A), lda, _ptr(x), _ptr(y), _ptr(s), nthreads)
+    _check(rc, "oracle_gemv")
+    return y, s
+
+
+def gemv_rows(A: np.ndarray, x: np.ndarray, rows, nthreads: int = 0):
+    """Selected entries of y and s: returns (y_rows, s_rows), shape (len(rows),)."""
+    A, lda = _as_f32_matrix(A)
+    M, K = A.shape
+    x = _as_f32_vector(x, K)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    y = np.empty(rows.size, dtype=np.float64)
+    s = np.empty(rows.size, dtype=np.float64)
+    rc = _load().oracle_gemv_rows(M, K, _ptr(A), lda, _ptr(x), _ptr(rows), rows.size, _ptr(y), _ptr(s),
+                                  nthreads)
+    _check(rc, "oracle_gemv_rows")
+    return y, s
