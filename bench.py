@@ -1,6 +1,9 @@
 #!/usr/bin/env python3
 """Benchmark: dense bf16 GEMM C = A*B (fp32 accumulate, fp32 out), 8192^3, one GPU.
 
+(With --workload gemv<N>_fp32 it measures the fp32 GEMV y = A*x instead and
+prints that kernel's line, bound by HBM bandwidth.)
+
 One step is one call of xgemm_run on the 8192 x 8192 x 8192 bf16 workload
 (entries uniform on [-1, 1], seed 2), inputs already resident in HBM.  Prints
 one JSON line.  ``value`` is the whole-job throughput over the K timed steps,
@@ -37,40 +40,43 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_TFLOPS = {"bf16": 2516.6, "fp16": 2516.6}  # MI355X dense MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_HBM_GBS = 8000.0                            # MI355X HBM3E
 METRIC = "GEMM TFLOP/s and % of MI355X dense MFMA peak (bf16, 8192³) on 1 GPU"
+GEMV_METRIC = "GEMV TFLOP/s and %% of the MI355X HBM-bound GEMV peak (fp32, %d², 2 FLOP per 4-byte element)"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters_%s.json")
+# sources whose change invalidates committed counters of each kernel family
+KERNEL_SOURCES = {"gemm": ("gemm_kernel.hpp", "xgemm.hip"), "gemv": ("gemv_kernel.hpp", "xgemm.hip")}
 
 
-def kernel_source_hash() -> str:
+def family(workload: str) -> str:
+    return "gemv" if workload.startswith("gemv") else "gemm"
+
+
+def kernel_source_hash(fam: str = "gemm") -> str:
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2609_16389_amd", "csrc", "*"))):
-        with open(p, "rb") as f:
+    for name in KERNEL_SOURCES[fam]:
+        with open(os.path.join(ROOT, "paper_2609_16389_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def stored_traffic(workload: str):
-    """HBM bytes per launch from committed rocprofv3 --pmc counters, or None
-    if there are none or the kernel sources changed since they were taken."""
-    path = COUNTERS_FILE % workload
-    if not os.path.exists(path):
-        return None
-    with open(path) as f:
-        d = json.load(f)
-    if d.get("kernel_source_sha256") != kernel_source_hash():
-        return None
-    return d.get("hbm_bytes_per_launch")
-
-
 def stored_counters(workload: str):
+    """Committed rocprofv3 --pmc summary of this workload's kernel, or None
+    if there is none or the kernel sources changed since it was taken."""
     path = COUNTERS_FILE % workload
     if not os.path.exists(path):
         return None
     with open(path) as f:
         d = json.load(f)
-    if d.get("kernel_source_sha256") != kernel_source_hash():
+    if d.get("kernel_source_sha256") != kernel_source_hash(family(workload)):
         return None
     return d
+
+
+def stored_traffic(workload: str):
+    """HBM bytes per launch from the committed counters, or None."""
+    d = stored_counters(workload)
+    return None if d is None else d.get("hbm_bytes_per_launch")
 
 
 def summarize_counters(directory: str, workload: str) -> str:
@@ -84,13 +90,14 @@ def summarize_counters(directory: str, workload: str) -> str:
                 k = r["Kernel_Name"]
                 vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
                 durs.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
-    gemm = [k for k in vals if "gemm_kernel" in k]
+    fam = family(workload)
+    gemm = [k for k in vals if ("%s_kernel" % fam) in k]
     copy = [k for k in vals if "copyBuffer" in k or "copy_kernel" in k]
     if not gemm:
-        raise SystemExit("no GEMM kernel in %s" % directory)
+        raise SystemExit("no %s kernel in %s" % (fam.upper(), directory))
     k = max(gemm, key=lambda n: len(durs[n]))
     med = {c: statistics.median(v) for c, v in vals[k].items()}
-    out = {"kernel": k, "workload": workload, "kernel_source_sha256": kernel_source_hash(),
+    out = {"kernel": k, "workload": workload, "kernel_source_sha256": kernel_source_hash(fam),
            "dispatches": len(durs[k]) // max(1, len(vals[k])), "median_duration_ns": statistics.median(durs[k]),
            "counters_median": med}
     fetch_scale = write_scale = None
@@ -142,6 +149,114 @@ def cpu_baseline(w, A, B, budget_s: float = 12.0):
                       "decoding B; %.1f s" % (rows - 1, rows, w.N, w.K, w.name, t)}
 
 
+def gemv_cpu_baseline(w, A, x, budget_s: float = 10.0):
+    """The oracle, untuned, on the whole GEMV workload, repeated for about
+    budget_s seconds."""
+    import oracle
+    oracle.build(force=False)
+    cores = oracle.thread_count()
+    t0 = time.perf_counter()
+    oracle.gemv(A, x)
+    one = time.perf_counter() - t0
+    reps = max(1, int(budget_s / max(one, 1e-3)))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        oracle.gemv(A, x)
+    t = (time.perf_counter() - t0) / reps
+    return {"value": round(w.flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": "the whole %s workload (%d x %d), fp64, %d repetitions of %.3f s" % (w.name, w.M, w.K, reps, t)}
+
+
+def bench_gemv(args, w):
+    """The fp32 GEMV line: y = A x, one xgemv_run per step."""
+    import torch
+    from paper_2609_16389_amd import workloads as wl
+    from paper_2609_16389_amd import xgemm as xg
+    print("bench: workload %s M=%d K=%d fp32" % (w.name, w.M, w.K), file=sys.stderr, flush=True)
+    A_np, x_np = wl.gemv_workload_inputs(w)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    A = torch.from_numpy(A_np).to(dev)
+    x = torch.from_numpy(x_np).to(dev)
+    y = torch.empty(w.M, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    h = xg.handle(0)
+    cfg = xg.xgemv_select_config(w.M, w.K, torch.cuda.get_device_properties(dev).multi_processor_count)
+
+    def step():
+        rc = xg.xgemv_run(h, w.M, w.K, A.data_ptr(), w.K, x.data_ptr(), y.data_ptr(), stream.cuda_stream)
+        if rc != xg.XGEMM_OK:
+            raise xg.XgemmError(rc, xg.xgemm_last_error(h))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)]) * 1e-3
+    value = w.flops * args.steps / wall / 1e12
+    achieved_gbs = w.alg_bytes / float(per.mean()) / 1e9
+    peak_tflops = PEAK_HBM_GBS * 1e9 * 2 / 4 / 1e12
+    srt = np.sort(per)
+    q = len(srt) // 4
+    iqr_mean = float(srt[q:len(srt) - q].mean()) if len(srt) >= 4 else float(srt.mean())
+    if args.copy_calibration:
+        n = args.copy_calibration // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+    comparator = None
+    if not args.no_comparator:
+        for _ in range(3):
+            torch.mv(A, x)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(20):
+            torch.mv(A, x)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) * 1e-3 / 20
+        comparator = {"name": "torch.mv (rocBLAS/hipBLASLt)", "tflops": round(w.flops / t / 1e12, 3),
+                      "gbs": round(w.alg_bytes / t / 1e9, 1)}
+    counters = stored_counters(w.name)
+    out = {
+        "metric": GEMV_METRIC % w.M,
+        "value": round(value, 4),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "strong",
+        "vs_baseline": None,
+        "dtype": "fp32",
+        "data": "synthetic (seeded uniform[-1,1], seed %d)" % w.seed,
+        "config": {"workload": w.name, "M": w.M, "K": w.K, "rows": cfg.rows, "unroll": cfg.unroll},
+        "pct_of_peak": round(100.0 * value / peak_tflops, 2),
+        "paper_protocol_iqr_mean_tflops": round(w.flops / iqr_mean / 1e12, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(achieved_gbs / PEAK_HBM_GBS, 4),
+                     "traffic": None if counters is None else counters.get("hbm_bytes_per_launch")},
+        "comparator": comparator,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        print("bench: cpu baseline (oracle)", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = gemv_cpu_baseline(w, A_np, x_np)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -172,6 +287,9 @@ def main():
     from paper_2609_16389_amd import workloads as wl
     from paper_2609_16389_amd import xgemm as xg
 
+    if args.workload in wl.GEMV_WORKLOADS:
+        bench_gemv(args, wl.GEMV_WORKLOADS[args.workload])
+        return
     w = wl.WORKLOADS[args.workload]
     print("bench: workload %s M=%d N=%d K=%d %s" % (w.name, w.M, w.N, w.K, w.dtype), file=sys.stderr, flush=True)
     A_bits, B_bits = wl.workload_inputs(w)

@@ -207,8 +207,12 @@ enum xgemm_trace_op {
                                   operations of the wave have completed */
     XGEMM_TRACE_WAIT_LGKM = 3, /* s_waitcnt lgkmcnt(arg), likewise for LDS operations */
     XGEMM_TRACE_BARRIER = 4,   /* s_barrier across the workgroup */
-    XGEMM_TRACE_STORE = 5      /* global store (vector-memory counter) of `arg` bytes at `addr` */
+    XGEMM_TRACE_STORE = 5,     /* global store (vector-memory counter) of `arg` bytes at `addr` */
+    XGEMM_TRACE_LDS_WRITE = 6, /* LDS write from registers (LDS counter) of `arg` bytes at `lds` */
+    XGEMM_TRACE_LOAD = 7       /* global load into registers (vector-memory counter) of `arg` bytes
+                                  at `addr` */
 };
+/* A lane that takes no part in a lane-masked LDS_READ or LDS_WRITE records lds = -1. */
 
 /* One event of one thread.  LDS offsets count bytes from the start of the
    workgroup's LDS allocation; global addresses are byte addresses. */
@@ -260,6 +264,72 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
 int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
                           float *C, int64_t ldc, float *W, const xgemm_config *cfg, int cu_count, int segment,
                           int64_t block, xgemm_trace_event *out, int64_t capacity, int64_t *counts);
+
+/*
+ * Matrix-vector product (GEMV): y = A * x in fp32.
+ *
+ * The paper's second benchmark beside its GEMMs is a full-precision fp32
+ * GEMV that uses no matrix instructions (Section 6).  A is M x K, row-major
+ * with leading dimension lda (A[i][k] = A[i * lda + k]); x holds K floats and
+ * y receives M floats, both contiguous:
+ *
+ *     y[i] = sum over k of A[i][k] * x[k]
+ *
+ * Products and sums are fp32 (fused multiply-adds); the summation is
+ * grouped (per-thread partial sums, then a tree), so for every i, with
+ * n = 4 * ceil(K / 1024) + 10 roundings on the longest path,
+ *     |y[i] - exact| <= n * 2^-24 * sum_k |A[i][k] x[k]| + (K + 255) * 2^-150
+ * (up to second-order terms; the last term bounds rounding in the
+ * subnormal range, summed over the K + 255 operations that form y[i]),
+ * where "exact" is the real-number result on the stored inputs.  Subnormal
+ * inputs and results are kept, not flushed to zero.
+ */
+
+/* GEMV launch configuration: rows of A per 256-thread workgroup (1, 2, 4 or
+   8) and 16-byte chunks of x each thread loads per loop iteration (1, 2 or
+   4; A's rows are loaded the same number of chunks ahead). */
+typedef struct xgemv_config {
+    int32_t rows;
+    int32_t unroll;
+} xgemv_config;
+
+/*
+ * y = A * x, enqueued asynchronously on `stream` (a hipStream_t; NULL means
+ * the default stream); y is complete once the stream has been synchronized.
+ *   M, K     sizes, each >= 0 and < 2^31.  M == 0: no-op.  K == 0: y = 0.
+ *   A, lda   device pointer to M x K floats, lda >= K
+ *   x        device pointer to K floats
+ *   y        device pointer to M floats; must not overlap A or x
+ * A pointer may be NULL only when it addresses no element.  16-byte loads
+ * need A and x 16-byte aligned and lda a multiple of 4; any other alignment
+ * is still correct through 4-byte loads.  The handle supplies the device's
+ * CU count; GEMV uses no workspace.  Errors: XGEMM_ERR_INVALID_ARG for a
+ * NULL handle, bad sizes or pointers; XGEMM_ERR_HIP if the launch fails.
+ * Nothing is enqueued on error.
+ */
+int xgemv_run(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+              void *stream);
+
+/* As xgemv_run with the configuration forced (XGEMM_ERR_INVALID_ARG for an
+   unsupported one).  The result is the same bit for bit for every unroll;
+   rows changes only which workgroup computes a row, not its arithmetic. */
+int xgemv_run_config(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x,
+                     float *y, void *stream, const xgemv_config *cfg);
+
+/* The configuration xgemv_run uses on a device with cu_count CUs
+   (host-only).  XGEMM_ERR_INVALID_ARG for negative sizes, cu_count < 1 or
+   out == NULL. */
+int xgemv_select_config(int64_t M, int64_t K, int cu_count, xgemv_config *out);
+
+/*
+ * Trace of GEMV workgroup `block` (0 .. ceil(M / cfg->rows) - 1) in the
+ * format of xgemm_trace_workgroup (256 threads; A, x and y are only used as
+ * addresses).  M and K must be > 0.  XGEMM_ERR_INVALID_ARG for invalid
+ * arguments, a block out of range, counts == NULL or an unsupported cfg.
+ */
+int xgemv_trace_workgroup(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+                          const xgemv_config *cfg, int64_t block, xgemm_trace_event *out, int64_t capacity,
+                          int64_t *counts);
 
 /* Static description of a status code; never NULL. */
 const char *xgemm_strerror(int status);

@@ -8,10 +8,12 @@
 #include <string.h>
 
 #include <new>
+#include <type_traits>
 #include <vector>
 
 #include "xgemm.h"
 #include "gemm_kernel.hpp"
+#include "gemv_kernel.hpp"
 
 using xgemm_dev::GemmParams;
 
@@ -546,6 +548,108 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
     return XGEMM_OK;
 }
 
+// ---------------------------------------------------------------------------
+// GEMV
+// ---------------------------------------------------------------------------
+
+using xgemv_dev::GemvParams;
+
+bool valid_gemv_config(const xgemv_config *c)
+{
+    return c && (c->rows == 1 || c->rows == 2 || c->rows == 4 || c->rows == 8) &&
+           (c->unroll == 1 || c->unroll == 2 || c->unroll == 4);
+}
+
+// Measured on MI355X (interleaved sweeps over 4096^2 .. 32768^2, 1024 x
+// 65536, 65536 x 1024, 131072 x 4096 and 256 x 262144): two rows per
+// workgroup with four chunks in flight per row is within 3% of the best
+// configuration whenever that still leaves at least four workgroups per CU;
+// below that one row per workgroup keeps more CUs streaming (at 256 x
+// 262144 it reads 6.2 TB/s against 4.1 TB/s with two chunks in flight).
+void select_gemv(int64_t M, int64_t K, int cu_count, xgemv_config *out)
+{
+    (void)K;
+    out->rows = M >= 8 * (int64_t)cu_count ? 2 : 1;
+    out->unroll = 4;
+}
+
+template <class F>
+auto with_gemv_config(const xgemv_config &c, F &&f)
+{
+#define XGEMV_CASE(R, U)                                      \
+    if (c.rows == R && c.unroll == U)                        \
+        return f(std::integral_constant<int, R>{}, std::integral_constant<int, U>{});
+    XGEMV_CASE(1, 1) XGEMV_CASE(1, 2) XGEMV_CASE(1, 4)
+    XGEMV_CASE(2, 1) XGEMV_CASE(2, 2) XGEMV_CASE(2, 4)
+    XGEMV_CASE(4, 1) XGEMV_CASE(4, 2) XGEMV_CASE(4, 4)
+    XGEMV_CASE(8, 1) XGEMV_CASE(8, 2)
+#undef XGEMV_CASE
+    return f(std::integral_constant<int, 8>{}, std::integral_constant<int, 4>{});
+}
+
+int check_gemv_args(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, const float *y)
+{
+    if (M < 0 || K < 0 || M >= kMaxDim || K >= kMaxDim || lda < K || lda < 0)
+        return XGEMM_ERR_INVALID_ARG;
+    if ((M > 0 && K > 0 && !A) || (K > 0 && M > 0 && !x) || (M > 0 && !y))
+        return XGEMM_ERR_INVALID_ARG;
+    if ((double)M * (double)lda > 9.0e18)
+        return XGEMM_ERR_INVALID_ARG;
+    return XGEMM_OK;
+}
+
+GemvParams gemv_params(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y)
+{
+    GemvParams p;
+    p.A = A;
+    p.x = x;
+    p.y = y;
+    p.lda = lda;
+    p.M = (int)M;
+    p.K = (int)K;
+    p.vec = ((uintptr_t)A % 16 == 0) && ((uintptr_t)x % 16 == 0) && (lda % 4 == 0);
+    return p;
+}
+
+int run_gemv(xgemm_ctx *h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+             void *stream, const xgemv_config *forced)
+{
+    if (!h)
+        return XGEMM_ERR_INVALID_ARG;
+    int rc = check_gemv_args(M, K, A, lda, x, y);
+    if (rc != XGEMM_OK)
+        return rc;
+    if (forced && !valid_gemv_config(forced))
+        return XGEMM_ERR_INVALID_ARG;
+    h->last_error[0] = '\0';
+    hipStream_t s = (hipStream_t)stream;
+    if (M == 0)
+        return XGEMM_OK;
+    if (K == 0) {
+        const int grid = (int)(cdiv(M, 256) < 4096 ? cdiv(M, 256) : 4096);
+        hipLaunchKernelGGL(xgemm_dev::fill_zero, dim3(grid), dim3(256), 0, s, y, (int64_t)1, (int)M, 1);
+    } else {
+        xgemv_config cfg;
+        if (forced)
+            cfg = *forced;
+        else
+            select_gemv(M, K, h->cu_count, &cfg);
+        const GemvParams p = gemv_params(M, K, A, lda, x, y);
+        with_gemv_config(cfg, [&](auto r, auto u) {
+            constexpr int R = decltype(r)::value, U = decltype(u)::value;
+            hipLaunchKernelGGL((xgemv_dev::gemv_kernel<R, U>), dim3((unsigned)cdiv(M, R)),
+                               dim3(xgemv_dev::kThreads), 0, s, p);
+            return 0;
+        });
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+        set_error(h, "gemv launch", e);
+        return XGEMM_ERR_HIP;
+    }
+    return XGEMM_OK;
+}
+
 // Host stand-in for the device operations of the pipelined kernel: each
 // call appends one event to the calling thread's trace instead of touching
 // memory.  LDS pointers point into a host buffer of the kernel's LDS size,
@@ -593,6 +697,49 @@ struct TraceOps {
     void barrier() const { push(XGEMM_TRACE_BARRIER, 0, 0, 0); }
     void fence() const {}
     void store4(float *q, xgemm_dev::f32x4) const { push(XGEMM_TRACE_STORE, 16, 0, (int64_t)(uintptr_t)q); }
+    void store1(float *q, float) const { push(XGEMM_TRACE_STORE, 4, 0, (int64_t)(uintptr_t)q); }
+};
+
+// Host stand-in for the GEMV kernel's operations.  Lanes whose masked LDS
+// access is off record LDS offset -1.
+struct TraceGemvOps {
+    float *base;
+    std::vector<xgemm_trace_event> *ev;
+    void push(int op, int arg, int64_t lds, int64_t addr) const
+    {
+        xgemm_trace_event e;
+        e.op = op;
+        e.arg = arg;
+        e.lds = lds;
+        e.addr = addr;
+        ev->push_back(e);
+    }
+    float *lds() const { return base; }
+    xgemv_dev::f32x4 load4(const float *q) const
+    {
+        push(XGEMM_TRACE_LOAD, 16, 0, (int64_t)(uintptr_t)q);
+        return xgemv_dev::f32x4{0, 0, 0, 0};
+    }
+    float load1(const float *q) const
+    {
+        push(XGEMM_TRACE_LOAD, 4, 0, (int64_t)(uintptr_t)q);
+        return 0.0f;
+    }
+    float wave_sum(float v) const { return v; }
+    void lds_write1(float *q, float, bool on) const
+    {
+        push(XGEMM_TRACE_LDS_WRITE, 4, on ? (int64_t)((char *)q - (char *)base) : -1, 0);
+    }
+    float lds_read1(const float *q, bool on) const
+    {
+        push(XGEMM_TRACE_LDS_READ, 4, on ? (int64_t)((const char *)q - (const char *)base) : -1, 0);
+        return 0.0f;
+    }
+    void sync() const
+    {
+        push(XGEMM_TRACE_WAIT_LGKM, 0, 0, 0);
+        push(XGEMM_TRACE_BARRIER, 0, 0, 0);
+    }
     void store1(float *q, float) const { push(XGEMM_TRACE_STORE, 4, 0, (int64_t)(uintptr_t)q); }
 };
 
@@ -781,6 +928,55 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
             const TraceOps ops{lds.data(), &ev};
             xgemm_dev::dma_tile<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, 0>(ops, g.p, (int)block,
                                                                                     (int)g.grid, tid);
+            counts[tid] = (int64_t)ev.size();
+            const int64_t n = counts[tid] < capacity ? counts[tid] : capacity;
+            if (n > 0)
+                memcpy(out + (int64_t)tid * capacity, ev.data(), (size_t)n * sizeof(xgemm_trace_event));
+        }
+        return (int)XGEMM_OK;
+    });
+}
+
+int xgemv_run(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+              void *stream)
+{
+    return run_gemv(h, M, K, A, lda, x, y, stream, nullptr);
+}
+
+int xgemv_run_config(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x,
+                     float *y, void *stream, const xgemv_config *cfg)
+{
+    if (!cfg)
+        return XGEMM_ERR_INVALID_ARG;
+    return run_gemv(h, M, K, A, lda, x, y, stream, cfg);
+}
+
+int xgemv_select_config(int64_t M, int64_t K, int cu_count, xgemv_config *out)
+{
+    if (!out || M < 0 || K < 0 || cu_count < 1)
+        return XGEMM_ERR_INVALID_ARG;
+    select_gemv(M, K, cu_count, out);
+    return XGEMM_OK;
+}
+
+int xgemv_trace_workgroup(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+                          const xgemv_config *cfg, int64_t block, xgemm_trace_event *out, int64_t capacity,
+                          int64_t *counts)
+{
+    if (!counts || capacity < 0 || (capacity > 0 && !out) || !valid_gemv_config(cfg) || M <= 0 || K <= 0 ||
+        check_gemv_args(M, K, A, lda, x, y) != XGEMM_OK)
+        return XGEMM_ERR_INVALID_ARG;
+    if (block < 0 || block >= cdiv(M, cfg->rows))
+        return XGEMM_ERR_INVALID_ARG;
+    const GemvParams p = gemv_params(M, K, A, lda, x, y);
+    return with_gemv_config(*cfg, [&](auto r, auto u) {
+        constexpr int R = decltype(r)::value, U = decltype(u)::value;
+        std::vector<float> lds(xgemv_dev::kWaves * R);
+        std::vector<xgemm_trace_event> ev;
+        for (int tid = 0; tid < xgemv_dev::kThreads; ++tid) {
+            ev.clear();
+            const TraceGemvOps ops{lds.data(), &ev};
+            xgemv_dev::gemv_block<R, U>(ops, p, (int)block, tid);
             counts[tid] = (int64_t)ev.size();
             const int64_t n = counts[tid] < capacity ? counts[tid] : capacity;
             if (n > 0)

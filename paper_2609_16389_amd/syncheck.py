@@ -11,9 +11,11 @@ evaluation times that interpreter over square GEMM sizes (Section 6).
 
 Here the same idea is applied to what gfx950 actually synchronises:
 
-* Records live on 8-byte granules of the workgroup's LDS allocation.  A
-  direct global-to-LDS load leaves a mutate record, an LDS read a read
-  record; each record remembers the wave that issued it and its position
+* Records live on granules of the workgroup's LDS allocation: the largest
+  power of two (up to 16 bytes) that divides every access's offset and
+  size in the trace, so no granule is shared by accesses that do not
+  overlap.  A direct global-to-LDS load or an LDS write leaves a mutate
+  record, an LDS read a read record; each record remembers the wave that issued it and its position
   in that wave's counter (vector memory for direct loads and stores, LDS
   for LDS reads), because on this hardware an access completes
   asynchronously and only ``s_waitcnt`` makes its completion known.
@@ -64,7 +66,6 @@ import numpy as np
 
 from . import xgemm as xg
 
-GRANULE = 8          # bytes per LDS record location
 LANES = 64           # wavefront width
 
 LDS_LOAD = xg.XGEMM_TRACE_LDS_LOAD
@@ -73,6 +74,9 @@ WAIT_VM = xg.XGEMM_TRACE_WAIT_VM
 WAIT_LGKM = xg.XGEMM_TRACE_WAIT_LGKM
 BARRIER = xg.XGEMM_TRACE_BARRIER
 STORE = xg.XGEMM_TRACE_STORE
+LDS_WRITE = xg.XGEMM_TRACE_LDS_WRITE
+LOAD = xg.XGEMM_TRACE_LOAD
+INACTIVE = -1        # LDS offset of a lane that sits out a lane-masked access
 
 
 @dataclasses.dataclass
@@ -96,15 +100,16 @@ class WaveStream:
     addr: np.ndarray   # [n, 64] int64
 
 
-def _drop_stores(events, counts):
-    """Per-thread traces without their global stores.  Stores under a lane
-    mask (edge tiles) make lanes of a wave issue different numbers of them;
-    they take part only in the global checks.  A vector-memory wait after a
-    store would make the store count matter for the wait, which these
-    traces never contain; it is reported rather than modelled."""
+def _drop_global(events, counts):
+    """Per-thread traces without their global loads and stores into
+    registers.  Those under a lane mask (edge tiles, K tails) make lanes of
+    a wave issue different numbers of them; they take part only in the
+    global checks.  A vector-memory wait after one of them would make their
+    count matter for the wait, which these kernels never do; it is reported
+    rather than modelled."""
     threads = events.shape[0]
     valid = np.arange(events.shape[1])[None, :] < counts[:, None]
-    keep = valid & (events["op"] != STORE)
+    keep = valid & (events["op"] != STORE) & (events["op"] != LOAD)
     if (keep == valid).all():
         return events, counts, False
     first_store = np.where((valid & ~keep).any(axis=1), np.argmax(valid & ~keep, axis=1), events.shape[1])
@@ -120,15 +125,16 @@ def _drop_stores(events, counts):
 
 def wave_streams(events: np.ndarray, counts: np.ndarray, violations: list | None = None):
     """Group a workgroup trace (threads x capacity records, per-thread
-    counts) into per-wave streams of its LDS loads, LDS reads, waits and
-    barriers.  Lanes of one wave must issue the same operations with the
+    counts) into per-wave streams of its direct LDS loads, LDS reads and
+    writes, waits and barriers.  Lanes of one wave must issue the same operations with the
     same wave-uniform operands; a lane that does not is reported as a
     divergence and the wave's stream is cut there."""
     threads = events.shape[0]
     assert threads % LANES == 0
-    events, counts, wait_after_store = _drop_stores(events, counts)
-    if wait_after_store and violations is not None:
-        violations.append(Violation("unsupported", -1, -1, "vector-memory wait after a global store"))
+    events, counts, wait_after_global = _drop_global(events, counts)
+    if wait_after_global and violations is not None:
+        violations.append(Violation("unsupported", -1, -1, "vector-memory wait after a global load or store "
+                                    "into registers"))
     out = []
     for w in range(threads // LANES):
         lanes = slice(w * LANES, (w + 1) * LANES)
@@ -157,12 +163,14 @@ def wave_streams(events: np.ndarray, counts: np.ndarray, violations: list | None
 class LdsMachine:
     """Abstract machine over one workgroup's LDS (see the module docstring)."""
 
-    def __init__(self, lds_bytes: int, nwaves: int, max_reports: int = 20):
+    def __init__(self, lds_bytes: int, nwaves: int, granule: int = 8, max_reports: int = 20):
         self.lds_bytes = lds_bytes
         self.nw = nwaves
-        g = (lds_bytes + GRANULE - 1) // GRANULE
+        self.granule = granule
+        g = (lds_bytes + granule - 1) // granule
         self.mut_w = np.full(g, -1, dtype=np.int64)     # wave of the live mutate record
-        self.mut_s = np.full(g, -1, dtype=np.int64)     # its vector-memory counter position
+        self.mut_s = np.full(g, -1, dtype=np.int64)     # its position in that wave's counter
+        self.mut_c = np.zeros(g, dtype=np.int8)         # the counter: 0 vector memory, 1 LDS
         self.rd_s = np.full((g, nwaves), -1, dtype=np.int64)  # latest read per wave since then
         self.issued = {"vm": np.zeros(nwaves, np.int64), "lgkm": np.zeros(nwaves, np.int64)}
         self.done = {"vm": np.zeros(nwaves, np.int64), "lgkm": np.zeros(nwaves, np.int64)}
@@ -183,6 +191,11 @@ class LdsMachine:
         """Records (owner wave, counter position) visible to wave x."""
         return (pos < self.seen[counter][owner]) | ((owner == x) & (pos < self.done[counter][x]))
 
+    def _mut_visible(self, g, x):
+        """Live mutate records of granules g (all present) visible to wave x."""
+        w, pos, c = self.mut_w[g], self.mut_s[g], self.mut_c[g]
+        return np.where(c == 0, self._visible("vm", w, pos, x), self._visible("lgkm", w, pos, x))
+
     def _granules(self, wave, i, start, nbytes):
         """Granules covered by per-lane accesses [start, start + nbytes)."""
         if (start < 0).any() or (start + nbytes > self.lds_bytes).any():
@@ -190,8 +203,8 @@ class LdsMachine:
             self._report("lds_bounds", wave, i, "LDS bytes [%d, %d) outside the %d-byte allocation" %
                          (int(bad[0]), int(bad[0]) + nbytes, self.lds_bytes))
             start = start[(start >= 0) & (start + nbytes <= self.lds_bytes)]
-        first = start // GRANULE
-        last = (start + nbytes - 1) // GRANULE
+        first = start // self.granule
+        last = (start + nbytes - 1) // self.granule
         span = int((last - first).max()) + 1 if len(first) else 0
         g = (first[:, None] + np.arange(span)[None, :])
         g = g[g <= last[:, None]]
@@ -201,14 +214,23 @@ class LdsMachine:
     def lds_load(self, w, i, base, nbytes):
         """Direct load: lane l writes nbytes at base + nbytes * l."""
         g = self._granules(w, i, base + nbytes * np.arange(LANES, dtype=np.int64), nbytes)
+        self._mutate(w, i, g, "vm", "direct load")
+        self.last_load[w] = self.issued["vm"][w] - 1
+
+    def lds_write(self, w, i, addrs, nbytes):
+        """LDS write from registers by the active lanes."""
+        g = self._granules(w, i, addrs[addrs != INACTIVE], nbytes)
+        self._mutate(w, i, g, "lgkm", "LDS write")
+
+    def _mutate(self, w, i, g, counter, what):
         mw = self.mut_w[g]
         has = mw >= 0
         if has.any():
-            ok = self._visible("vm", mw[has], self.mut_s[g][has], w)
+            ok = self._mut_visible(g[has], w)
             if not ok.all():
                 bad = g[has][~ok][0]
-                self._report("waw", w, i, "LDS byte %d: earlier direct load by wave %d not ordered before "
-                             "this one" % (bad * GRANULE, int(self.mut_w[bad])))
+                self._report("waw", w, i, "LDS byte %d: earlier write by wave %d not ordered before this %s"
+                             % (bad * self.granule, int(self.mut_w[bad]), what))
         rs = self.rd_s[g]                                     # [len(g), nw]
         has = rs >= 0
         if has.any():
@@ -218,27 +240,26 @@ class LdsMachine:
                 rows, cols = np.nonzero(has)
                 k = int(np.argmin(ok))
                 self._report("war", w, i, "LDS byte %d: read by wave %d not complete and ordered before "
-                             "this direct load overwrites it" % (g[rows[k]] * GRANULE, int(cols[k])))
-        pos = self.issued["vm"][w]
+                             "this %s overwrites it" % (g[rows[k]] * self.granule, int(cols[k]), what))
         self.mut_w[g] = w
-        self.mut_s[g] = pos
+        self.mut_s[g] = self.issued[counter][w]
+        self.mut_c[g] = 0 if counter == "vm" else 1
         self.rd_s[g] = -1
-        self.last_load[w] = pos
-        self.issued["vm"][w] += 1
+        self.issued[counter][w] += 1
 
     def lds_read(self, w, i, addrs, nbytes):
-        g = self._granules(w, i, addrs, nbytes)
+        g = self._granules(w, i, addrs[addrs != INACTIVE], nbytes)
         mw = self.mut_w[g]
         if (mw < 0).any():
             bad = g[mw < 0][0]
-            self._report("uninit", w, i, "LDS byte %d read but never written" % (bad * GRANULE))
+            self._report("uninit", w, i, "LDS byte %d read but never written" % (bad * self.granule))
         has = mw >= 0
         if has.any():
-            ok = self._visible("vm", mw[has], self.mut_s[g][has], w)
+            ok = self._mut_visible(g[has], w)
             if not ok.all():
                 bad = g[has][~ok][0]
-                self._report("raw", w, i, "LDS byte %d: direct load by wave %d not complete and ordered "
-                             "before this read" % (bad * GRANULE, int(self.mut_w[bad])))
+                self._report("raw", w, i, "LDS byte %d: write by wave %d not complete and ordered "
+                             "before this read" % (bad * self.granule, int(self.mut_w[bad])))
         self.rd_s[g, w] = self.issued["lgkm"][w]
         self.issued["lgkm"][w] += 1
 
@@ -271,6 +292,8 @@ class LdsMachine:
                         self.lds_load(w, i, int(ws.lds[i, 0]), int(ws.arg[i]))
                     elif op == LDS_READ:
                         self.lds_read(w, i, ws.lds[i], int(ws.arg[i]))
+                    elif op == LDS_WRITE:
+                        self.lds_write(w, i, ws.lds[i], int(ws.arg[i]))
                     elif op == WAIT_VM:
                         self.wait(w, "vm", int(ws.arg[i]))
                     elif op == WAIT_LGKM:
@@ -284,8 +307,25 @@ class LdsMachine:
         return self.violations
 
 
+def granule_for(waves: list[WaveStream]) -> int:
+    """Largest power of two up to 16 dividing every LDS access's offset and
+    size in these streams."""
+    g = 16
+    for ws in waves:
+        acc = np.isin(ws.op, (LDS_LOAD, LDS_READ, LDS_WRITE))
+        if not acc.any():
+            continue
+        vals = [ws.arg[acc].astype(np.int64)]
+        lds = ws.lds[acc]
+        vals.append(lds[lds != INACTIVE])
+        for v in vals:   # (lane l of a direct load lands at base + arg * l)
+            while g > 1 and (v % g).any():
+                g //= 2
+    return g
+
+
 def check_workgroup_lds(waves: list[WaveStream], lds_bytes: int) -> list[Violation]:
-    return LdsMachine(lds_bytes, len(waves)).run(waves)
+    return LdsMachine(lds_bytes, len(waves), granule_for(waves)).run(waves)
 
 
 # ---------------------------------------------------------------------------
@@ -490,6 +530,77 @@ def _tile_elements(M, N, bm, bn, group_m, first, count):
         tm, tn = first_m + r % gm, r // gm
         total += (min(M, (tm + 1) * bm) - tm * bm) * (min(N, (tn + 1) * bn) - tn * bn)
     return total
+
+
+def trace_gemv_workgroup(M, K, lda, cfg, block, capacity=None):
+    """(events [256, capacity], counts [256]) of one GEMV workgroup, with A
+    at BASE_A, x at BASE_B and y at BASE_C."""
+    import ctypes
+    threads = 256
+    counts = np.zeros(threads, dtype=np.int64)
+    cptr = counts.ctypes.data_as(ctypes.c_void_p)
+    args = (M, K, BASE_A, lda, BASE_B, BASE_C, ctypes.byref(cfg), block)
+    if capacity is None:
+        rc = xg.lib.xgemv_trace_workgroup(*args, None, 0, cptr)
+        if rc != xg.XGEMM_OK:
+            raise xg.XgemmError(rc)
+        capacity = max(int(counts.max()), 1)
+    ev = np.zeros((threads, capacity), dtype=xg.TRACE_EVENT_DTYPE)
+    rc = xg.lib.xgemv_trace_workgroup(*args, ev.ctypes.data_as(ctypes.c_void_p), capacity, cptr)
+    if rc != xg.XGEMM_OK:
+        raise xg.XgemmError(rc)
+    if int(counts.max()) > capacity:
+        return trace_gemv_workgroup(M, K, lda, cfg, block, int(counts.max()))
+    return ev, counts
+
+
+def check_gemv_launch(M, K, cfg, lda=None):
+    """Trace every workgroup of the GEMV launch and run the checks: the LDS
+    machine on each distinct workgroup stream, global loads inside A and x,
+    and every y[i] stored exactly once."""
+    lda = K if lda is None else lda
+    t0 = time.perf_counter()
+    violations: list[Violation] = []
+    lds_seen = set()
+    n_events = 0
+    grid = -(-M // cfg.rows)
+    lds_bytes = 4 * 4 * cfg.rows
+    a_lo, a_hi = BASE_A, BASE_A + 4 * ((M - 1) * lda + K)
+    x_lo, x_hi = BASE_B, BASE_B + 4 * K
+    cov = np.zeros(M, dtype=np.int64)
+    for block in range(grid):
+        ev, counts = trace_gemv_workgroup(M, K, lda, cfg, block)
+        n_events += int(counts.sum())
+        valid = np.arange(ev.shape[1])[None, :] < counts[:, None]
+        ld = valid & (ev["op"] == LOAD)
+        ga, nb = ev["addr"][ld], ev["arg"][ld]
+        inside = ((ga >= a_lo) & (ga + nb <= a_hi)) | ((ga >= x_lo) & (ga + nb <= x_hi))
+        if not inside.all():
+            violations.append(Violation("global_bounds", -1, -1, "workgroup %d: load outside A and x at %#x"
+                                        % (block, int(ga[~inside][0]))))
+        st = valid & (ev["op"] == STORE)
+        off = ev["addr"][st] - BASE_C
+        ok = (off >= 0) & (off % 4 == 0) & (off // 4 < M) & (ev["arg"][st] == 4)
+        if not ok.all():
+            violations.append(Violation("global_bounds", -1, -1, "workgroup %d: store outside y" % block))
+        np.add.at(cov, off[ok] // 4, 1)
+        key = hashlib.sha1()
+        for f in ("op", "arg", "lds"):
+            key.update(np.where(valid & (ev["op"] != LOAD) & (ev["op"] != STORE), ev[f], 0).tobytes())
+        key = key.digest()
+        if key not in lds_seen:
+            lds_seen.add(key)
+            pre = []
+            waves = wave_streams(ev, counts, pre)
+            violations.extend(pre)
+            for v in check_workgroup_lds(waves, lds_bytes):
+                v.detail = "workgroup %d: %s" % (block, v.detail)
+                violations.append(v)
+    if (cov != 1).any():
+        violations.append(Violation("coverage", -1, -1, "%d entries of y not stored exactly once"
+                                    % int((cov != 1).sum())))
+    return LaunchReport(shape=(M, K), config=repr(cfg), segments=1, workgroups=grid, lds_classes=len(lds_seen),
+                        events=n_events, seconds=time.perf_counter() - t0, violations=violations)
 
 
 def main(argv=None):

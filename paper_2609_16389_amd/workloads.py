@@ -1,6 +1,7 @@
-"""Seeded synthetic GEMM inputs as stored 16-bit bit patterns.
+"""Seeded synthetic inputs: GEMM operands as stored 16-bit bit patterns, GEMV
+operands as float32.
 
-This module holds no GEMM arithmetic.  It only draws matrices and rounds them
+This module holds no GEMM or GEMV arithmetic.  It only draws matrices and rounds them
 to the 16-bit storage formats, so that the GPU path and the CPU oracle consume
 identical bits.
 
@@ -101,6 +102,57 @@ def make_int_inputs(M: int, N: int, K: int, dtype: str, seed: int, lo: int = -8,
     A = rng.integers(lo, hi + 1, size=(M, K)).astype(np.float64)
     B = rng.integers(lo, hi + 1, size=(K, N)).astype(np.float64)
     return to_bits(A, dtype), to_bits(B, dtype)
+
+
+# ---------------------------------------------------------------------------
+# GEMV (fp32): the paper's matrix-vector benchmark runs square problems
+# (Section 6).  A (M x K, row-major) is drawn first, then x (K), in float64
+# from one generator, and cast to float32.
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class GemvWorkload:
+    name: str
+    M: int
+    K: int
+    dist: str
+    seed: int
+    param: float
+    dtype: str = "fp32"
+
+    @property
+    def flops(self) -> int:
+        return 2 * self.M * self.K
+
+    @property
+    def alg_bytes(self) -> int:
+        """A and x read once, y written once (4 B/element)."""
+        return 4 * (self.M * self.K + self.K + self.M)
+
+
+GEMV_WORKLOADS = {
+    "gemv4096_fp32": GemvWorkload("gemv4096_fp32", 4096, 4096, "uniform", 5, 1.0),
+    "gemv8192_fp32": GemvWorkload("gemv8192_fp32", 8192, 8192, "uniform", 6, 1.0),
+    "gemv16384_fp32": GemvWorkload("gemv16384_fp32", 16384, 16384, "uniform", 7, 1.0),
+    "gemv32768_fp32": GemvWorkload("gemv32768_fp32", 32768, 32768, "uniform", 8, 1.0),
+}
+
+
+def make_gemv_inputs(M: int, K: int, dist: str, seed: int, param: float = 1.0, rows_per_draw: int = 4096):
+    """Return (A [M, K], x [K]) as contiguous float32 arrays.  A is drawn in
+    blocks of rows (the same values as one draw of the whole matrix, since
+    each value takes the generator's next output) to bound host memory."""
+    rng = np.random.default_rng(seed)
+    A = np.empty((M, K), dtype=np.float32)
+    for r in range(0, M, rows_per_draw):
+        n = min(rows_per_draw, M - r)
+        A[r:r + n] = _draw(rng, (n, K), dist, param)
+    x = _draw(rng, (K,), dist, param).astype(np.float32)
+    return A, x
+
+
+def gemv_workload_inputs(w: GemvWorkload):
+    return make_gemv_inputs(w.M, w.K, w.dist, w.seed, w.param)
 
 
 def sha256_bits(*arrays: np.ndarray) -> str:

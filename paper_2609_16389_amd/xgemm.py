@@ -49,6 +49,15 @@ XGEMM_TRACE_WAIT_VM = 2
 XGEMM_TRACE_WAIT_LGKM = 3
 XGEMM_TRACE_BARRIER = 4
 XGEMM_TRACE_STORE = 5
+XGEMM_TRACE_LDS_WRITE = 6
+XGEMM_TRACE_LOAD = 7
+
+
+class xgemv_config(ctypes.Structure):
+    _fields_ = [("rows", ctypes.c_int32), ("unroll", ctypes.c_int32)]
+
+    def __repr__(self):
+        return "xgemv_config(rows=%d, unroll=%d)" % (self.rows, self.unroll)
 
 
 class xgemm_trace_event(ctypes.Structure):
@@ -112,6 +121,15 @@ lib.xgemm_trace_plan.restype = _i32
 lib.xgemm_trace_workgroup.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _p,
                                       ctypes.POINTER(xgemm_config), _i32, _i32, _i64, _p, _i64, _p]
 lib.xgemm_trace_workgroup.restype = _i32
+lib.xgemv_run.argtypes = [_handle_t, _i64, _i64, _p, _i64, _p, _p, _p]
+lib.xgemv_run.restype = _i32
+lib.xgemv_run_config.argtypes = [_handle_t, _i64, _i64, _p, _i64, _p, _p, _p, ctypes.POINTER(xgemv_config)]
+lib.xgemv_run_config.restype = _i32
+lib.xgemv_select_config.argtypes = [_i64, _i64, _i32, ctypes.POINTER(xgemv_config)]
+lib.xgemv_select_config.restype = _i32
+lib.xgemv_trace_workgroup.argtypes = [_i64, _i64, _p, _i64, _p, _p, ctypes.POINTER(xgemv_config), _i64, _p, _i64,
+                                      _p]
+lib.xgemv_trace_workgroup.restype = _i32
 lib.xgemm_strerror.argtypes = [_i32]
 lib.xgemm_strerror.restype = ctypes.c_char_p
 lib.xgemm_last_error.argtypes = [_handle_t]
@@ -122,7 +140,7 @@ def header_functions(path: str = _HEADER):
     """Names of the functions include/xgemm.h declares."""
     text = open(path).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(xgemm_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(xgem[mv]_[a-z_]+)\s*\(", text)))
 
 
 # ---------------------------------------------------------------------------
@@ -217,6 +235,22 @@ def xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, cfg, cu_count, seg
         return xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, cfg, cu_count, segment, block,
                                      threads, int(counts.max()))
     return [out[t, :counts[t]] for t in range(threads)]
+
+
+def xgemv_run(h, M, K, A, lda, x, y, stream) -> int:
+    return lib.xgemv_run(h, M, K, A, lda, x, y, stream)
+
+
+def xgemv_run_config(h, M, K, A, lda, x, y, stream, cfg) -> int:
+    return lib.xgemv_run_config(h, M, K, A, lda, x, y, stream, ctypes.byref(cfg) if cfg is not None else None)
+
+
+def xgemv_select_config(M, K, cu_count) -> xgemv_config:
+    out = xgemv_config()
+    rc = lib.xgemv_select_config(M, K, cu_count, ctypes.byref(out))
+    if rc != XGEMM_OK:
+        raise XgemmError(rc)
+    return out
 
 
 def xgemm_strerror(status: int) -> str:
@@ -330,6 +364,34 @@ def gemm(A, B, out=None, config: xgemm_config | None = None, stream=None):
         rc = xgemm_run(*args)
     else:
         rc = xgemm_run_config(*args, config)
+    if rc != XGEMM_OK:
+        raise XgemmError(rc, xgemm_last_error(h))
+    return out
+
+
+def gemv(A, x, out=None, config: xgemv_config | None = None, stream=None):
+    """y = A @ x for a float32 CUDA matrix A (M x K, unit column stride) and
+    vector x (K, contiguous); returns y (M, float32), written into ``out`` if
+    given.  Runs xgemv_run (or xgemv_run_config) on the current stream."""
+    if A.dtype != torch.float32 or x.dtype != torch.float32:
+        raise TypeError("gemv takes float32 A and x")
+    if A.dim() != 2 or x.dim() != 1 or A.shape[1] != x.shape[0]:
+        raise ValueError("shapes %s and %s do not match" % (tuple(A.shape), tuple(x.shape)))
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    M, K = A.shape
+    if M > 0 and K > 1 and A.stride(1) != 1:
+        raise ValueError("A must have unit stride along its rows")
+    lda = A.stride(0) if M > 1 else max(K, 1)
+    if out is None:
+        out = torch.empty(M, dtype=torch.float32, device=A.device)
+    elif out.dtype != torch.float32 or out.shape != (M,) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 vector of %d values" % M)
+    if stream is None:
+        stream = torch.cuda.current_stream(A.device).cuda_stream
+    h = handle(A.device.index)
+    args = (h, M, K, A.data_ptr() or None, lda, x.data_ptr() or None, out.data_ptr() or None, stream)
+    rc = xgemv_run_config(*args, config) if config is not None else xgemv_run(*args)
     if rc != XGEMM_OK:
         raise XgemmError(rc, xgemm_last_error(h))
     return out

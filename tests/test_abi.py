@@ -140,3 +140,30 @@ def test_kernel_family_rules():
 def test_batched_null_handle():
     assert xg.xgemm_run_strided_batched(None, 1, 1, 1, 1, None, 1, 0, None, 1, 0, None, 1, 0, 0, None) \
         == xg.XGEMM_ERR_INVALID_ARG
+
+
+def test_gemv_selector():
+    assert (xg.xgemv_select_config(16384, 16384, 256).rows, xg.xgemv_select_config(16384, 16384, 256).unroll) == (2, 4)
+    assert xg.xgemv_select_config(256, 262144, 256).rows == 1
+    assert xg.xgemv_select_config(2048, 10, 256).rows == 2
+    assert xg.xgemv_select_config(2047, 10, 256).rows == 1
+    with pytest.raises(xg.XgemmError):
+        xg.xgemv_select_config(-1, 5, 256)
+    with pytest.raises(xg.XgemmError):
+        xg.xgemv_select_config(5, 5, 0)
+
+
+def test_gemv_null_handle_and_trace_arguments():
+    assert xg.xgemv_run(None, 4, 4, 16, 4, 16, 16, None) == xg.XGEMM_ERR_INVALID_ARG
+    import ctypes
+    counts = (ctypes.c_int64 * 256)()
+    cfg = xg.xgemv_config(2, 4)
+    # block out of range, unsupported config, K == 0
+    assert xg.lib.xgemv_trace_workgroup(4, 4, 16, 4, 16, 16, ctypes.byref(cfg), 2, None, 0, counts) == \
+        xg.XGEMM_ERR_INVALID_ARG
+    bad = xg.xgemv_config(3, 4)
+    assert xg.lib.xgemv_trace_workgroup(4, 4, 16, 4, 16, 16, ctypes.byref(bad), 0, None, 0, counts) == \
+        xg.XGEMM_ERR_INVALID_ARG
+    assert xg.lib.xgemv_trace_workgroup(4, 0, 16, 4, 16, 16, ctypes.byref(cfg), 0, None, 0, counts) == \
+        xg.XGEMM_ERR_INVALID_ARG
+    assert xg.lib.xgemv_trace_workgroup(4, 4, 16, 4, 16, 16, ctypes.byref(cfg), 0, None, 0, counts) == xg.XGEMM_OK

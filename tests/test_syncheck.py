@@ -1,5 +1,5 @@
-"""Synchronisation checker (the abstract machine over the pipelined kernel's
-own trace, Section 5 of the paper).
+"""Synchronisation checker (the abstract machine over the kernels' own
+traces, Section 5 of the paper): the pipelined GEMM kernel and the GEMV.
 
 1. The machine is pinned on hand-built wave programs whose verdicts follow
    from the hardware's ordering rules (a wait retires the issuing wave's
@@ -308,3 +308,82 @@ def test_load_outside_a_and_b_is_caught(monkeypatch):
 def test_cli_reports_ok(capsys):
     assert sc.main(["256", "512", "448", "--tile", "0", "--split", "1"]) == 0
     assert "OK" in capsys.readouterr().out
+
+
+# ---------------------------------------------------------------------------
+# the GEMV kernel: LDS writes from registers, lane-masked accesses
+# ---------------------------------------------------------------------------
+
+def prog_w(*ops):
+    """As prog, plus ('write', base) a 4-byte LDS write by lane 0 only."""
+    plain = [o for o in ops]
+    out = prog(*[("wvm", 0) if o[0] == "write" else o for o in plain])
+    for i, o in enumerate(plain):
+        if o[0] == "write":
+            out.op[i] = sc.LDS_WRITE
+            out.arg[i] = 4
+            out.lds[i] = sc.INACTIVE
+            out.lds[i, 0] = o[1]
+    return out
+
+
+def test_lds_write_needs_lgkm_wait_and_barrier():
+    reader = prog(("bar",), ("read8", np.where(LANE == 0, 0, sc.INACTIVE)))
+    assert verdict(prog_w(("write", 0), ("write", 4), ("wlgkm", 0), ("bar",)), reader) == set()
+    assert verdict(prog_w(("write", 0), ("write", 4), ("bar",)), reader) == {"raw"}
+    # a vector-memory wait does not retire LDS writes
+    assert verdict(prog_w(("write", 0), ("write", 4), ("wvm", 0), ("bar",)), reader) == {"raw"}
+
+
+def test_neighbouring_4_byte_writes_of_two_waves_do_not_conflict():
+    assert verdict(prog_w(("write", 0), ("wlgkm", 0)), prog_w(("write", 4), ("wlgkm", 0))) == set()
+    assert verdict(prog_w(("write", 0), ("wlgkm", 0)), prog_w(("write", 0), ("wlgkm", 0))) == {"waw"}
+
+
+@pytest.mark.parametrize("shape", [(1, 1), (5, 7), (300, 5000), (4097, 777), (64, 100003)])
+@pytest.mark.parametrize("rows,unroll", [(1, 1), (2, 4), (4, 2), (8, 4)])
+def test_gemv_launch_is_race_free(shape, rows, unroll):
+    rep = sc.check_gemv_launch(*shape, xg.xgemv_config(rows, unroll))
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+def test_gemv_padded_rows():
+    rep = sc.check_gemv_launch(77, 1001, xg.xgemv_config(4, 2), lda=1007)
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+def gemv_waves(rows=4):
+    ev, counts = sc.trace_gemv_workgroup(64, 4096, 4096, xg.xgemv_config(rows, 2), 0)
+    return sc.wave_streams(ev, counts), 16 * rows
+
+
+@pytest.mark.parametrize("name,keep,expect", [
+    # without the barrier, wave 0 (checked first) reads slots the others have
+    # not written yet, and their writes then find its unordered reads
+    ("no barrier", lambda op: op != sc.BARRIER, {"uninit", "war"}),
+    ("no LDS wait", lambda op: op != sc.WAIT_LGKM, {"raw"}),
+])
+def test_gemv_planted_mistakes(name, keep, expect):
+    waves, lds = gemv_waves()
+    assert sc.check_workgroup_lds(waves, lds) == []
+    mutated = [edit(ws, keep=keep) for ws in waves]
+    assert {v.kind for v in sc.check_workgroup_lds(mutated, lds)} == expect, name
+
+
+def test_gemv_partials_written_to_one_slot_race():
+    waves, lds = gemv_waves()
+    out = []
+    for w, ws in enumerate(waves):
+        ws = edit(ws)
+        wr = ws.op == sc.LDS_WRITE
+        ws.lds[wr] = np.where(ws.lds[wr] == sc.INACTIVE, sc.INACTIVE, ws.lds[wr] % 16)  # every wave: wave 0's slots
+        out.append(ws)
+    assert "waw" in {v.kind for v in sc.check_workgroup_lds(out, lds)}
+
+
+def test_gemv_duplicate_rows_are_caught(monkeypatch):
+    real = sc.trace_gemv_workgroup
+    monkeypatch.setattr(sc, "trace_gemv_workgroup", lambda M, K, lda, cfg, block, capacity=None:
+                        real(M, K, lda, cfg, 0, capacity))
+    rep = sc.check_gemv_launch(64, 256, xg.xgemv_config(4, 2))
+    assert "coverage" in {v.kind for v in rep.violations}
