@@ -45,8 +45,7 @@ enum xgemm_dtype {
 enum xgemm_status {
     XGEMM_OK = 0,
     XGEMM_ERR_INVALID_ARG = 1, /* bad size, leading dimension, pointer, dtype or config */
-    XGEMM_ERR_UNSUPPORTED = 2, /* the current device is not a gfx950 GPU; for traces: a launch of the
-                                  general kernel family, which is not traced */
+    XGEMM_ERR_UNSUPPORTED = 2, /* the current device is not a gfx950 GPU */
     XGEMM_ERR_ALLOC = 3,       /* the split-k workspace could not be allocated */
     XGEMM_ERR_HIP = 4          /* a HIP runtime call failed; see xgemm_last_error */
 };
@@ -191,10 +190,11 @@ size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, cons
  * leaves a read or mutate record, and fences, arrivals and waits raise the
  * visibility of those records (Section 5, Abstract Machine).  These entry
  * points provide the input for such a check of this library: they run the
- * pipelined kernel's own body on the host, for one workgroup of a planned
- * launch, with every hardware operation recorded as an event instead of
- * executed.  A, B, C and W are only used as addresses (never dereferenced),
- * so any values that satisfy the alignment of a real call may be passed.
+ * kernels' own bodies on the host, for one workgroup of a planned launch
+ * (either kernel family), with every hardware operation recorded as an
+ * event instead of executed.  A, B, C and W are only used as addresses
+ * (never dereferenced), so any values that satisfy the alignment of a real
+ * call may be passed.
  */
 
 /* Event kinds of a workgroup trace. */
@@ -256,8 +256,7 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
  * count above capacity means the trace was cut; call again with a larger
  * capacity (capacity 0 with out == NULL only counts).  W is the workspace
  * address for launches that write partials (reduce != 0), else unused.
- * XGEMM_ERR_UNSUPPORTED if the launch uses the general kernel family (only
- * the pipelined kernel is traced); XGEMM_ERR_INVALID_ARG as
+ * Both kernel families are traced.  XGEMM_ERR_INVALID_ARG as
  * xgemm_trace_plan, or for a block out of range, counts == NULL, or W ==
  * NULL where it is needed.
  */

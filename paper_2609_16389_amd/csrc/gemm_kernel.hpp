@@ -78,7 +78,7 @@ __device__ __forceinline__ f32x16 mfma32<1>(u32x4 a, u32x4 b, f32x16 c)
 // 16-byte chunk slot of logical chunk c in tile row r.  Rows r and r^j for
 // j < 16 never share a slot among 8 consecutive rows, nor a (row parity,
 // slot) pair among 16 consecutive rows.
-__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__host__ __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // Logical tile id -> (tile_m, tile_n): tiles are walked in groups of
 // group_m tile rows, column by column within a group, so that consecutive
@@ -155,13 +155,14 @@ __host__ __device__ __forceinline__ OutView out_view(const GemmParams &p, int ks
 }
 
 // Eight 16-bit values starting at base[off], the first `cnt` of them read
-// from memory and the rest zero.
-__device__ __forceinline__ u32x4 load8_masked(const uint16_t *base, int64_t off, int cnt)
+// from memory (through ops) and the rest zero.
+template <class Ops>
+__host__ __device__ __forceinline__ u32x4 load8_masked(const Ops &ops, const uint16_t *base, int64_t off, int cnt)
 {
     uint32_t h[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e)
-        h[e] = (e < cnt) ? (uint32_t)base[off + e] : 0u;
+        h[e] = (e < cnt) ? (uint32_t)ops.gload2(base + off + e) : 0u;
     u32x4 v;
     v.x = h[0] | (h[1] << 16);
     v.y = h[2] | (h[3] << 16);
@@ -173,7 +174,7 @@ __device__ __forceinline__ u32x4 load8_masked(const uint16_t *base, int64_t off,
 // Column c (0..7) of an 8 x 8 block of 16-bit values held as 8 rows of 4
 // dwords: returns the 8 values of that column, row 0 in the low half of
 // dword 0.
-__device__ __forceinline__ u32x4 column8(const u32x4 (&v)[8], int c)
+__host__ __device__ __forceinline__ u32x4 column8(const u32x4 (&v)[8], int c)
 {
     u32x4 w;
     const int d = c >> 1;
@@ -191,9 +192,19 @@ __device__ __forceinline__ u32x4 column8(const u32x4 (&v)[8], int c)
     return w;
 }
 
-template <int BM, int BN, int BK, int WGM, int WGN, int DT>
-__global__ void __launch_bounds__(WGM * WGN * 64)
-gemm_kernel(GemmParams p_in)
+// LDS bytes the general kernel allocates.
+template <int BM, int BN, int BK>
+constexpr int general_lds_bytes()
+{
+    return 2 * (BM + BN) * BK * 2;
+}
+
+// One workgroup (id `block` of `nblocks`) of the general kernel, as seen by
+// thread `tid`; every memory access, MFMA and barrier goes through `ops`
+// (see DeviceOps).
+template <int BM, int BN, int BK, int WGM, int WGN, int DT, class Ops>
+__host__ __device__ __forceinline__ void general_tile(const Ops &ops, const GemmParams &p_in, int block, int nblocks,
+                                                      int tid)
 {
     constexpr int NT = WGM * WGN * 64;
     constexpr int TM = BM / WGM, TN = BN / WGN;   // wave tile
@@ -208,18 +219,17 @@ gemm_kernel(GemmParams p_in)
     constexpr int A_BYTES = BM * ROWB, B_BYTES = BN * ROWB;
     constexpr int STAGE = A_BYTES + B_BYTES;
     static_assert(TM % 32 == 0 && TN % 32 == 0 && BK % 16 == 0 && KC <= 16, "tile shape");
-    static_assert(2 * STAGE <= 160 * 1024, "LDS budget");
+    static_assert(2 * STAGE <= 160 * 1024 && 2 * STAGE == general_lds_bytes<BM, BN, BK>(), "LDS budget");
 
-    __shared__ __attribute__((aligned(16))) char smem[2 * STAGE];
+    char *const smem = ops.lds();
 
     int tm, tn, ks, local;
-    const GemmParams p = map_tile(p_in, blockIdx.x, gridDim.x, tm, tn, ks, local);
+    const GemmParams p = map_tile(p_in, block, nblocks, tm, tn, ks, local);
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = ks * p.k_chunk;
     const int kend = min(p.K, kbeg + p.k_chunk);
     const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
-    const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
     const int wm = wave % WGM, wn = wave / WGM;
@@ -258,13 +268,13 @@ gemm_kernel(GemmParams p_in)
 #pragma unroll
             for (int it = 0; it < A_IT; ++it)
                 if (A_UNITS % NT == 0 || tid + it * NT < A_UNITS)
-                    ra[it] = *(const u32x4 *)(Ab + a_off[it]);
+                    ra[it] = ops.gload16(Ab + a_off[it]);
 #pragma unroll
             for (int it = 0; it < B_IT; ++it)
                 if (B_UNITS % NT == 0 || tid + it * NT < B_UNITS)
 #pragma unroll
                     for (int r = 0; r < 8; ++r)
-                        rb[it][r] = *(const u32x4 *)(Bb + b_off[it] + r * ldb);
+                        rb[it][r] = ops.gload16(Bb + b_off[it] + r * ldb);
         } else {
 #pragma unroll
             for (int it = 0; it < A_IT; ++it)
@@ -272,7 +282,7 @@ gemm_kernel(GemmParams p_in)
                     const int gm = m0 + a_row[it];
                     const int gk = k0 + a_c[it] * 8;
                     const int cnt = (gm < p.M) ? max(0, min(8, kend - gk)) : 0;
-                    ra[it] = load8_masked(Ab, a_off[it], cnt);
+                    ra[it] = load8_masked(ops, Ab, a_off[it], cnt);
                 }
 #pragma unroll
             for (int it = 0; it < B_IT; ++it)
@@ -282,7 +292,7 @@ gemm_kernel(GemmParams p_in)
 #pragma unroll
                     for (int r = 0; r < 8; ++r) {
                         const int gk = k0 + b_kg[it] * 8 + r;
-                        rb[it][r] = load8_masked(Bb, b_off[it] + r * ldb, gk < kend ? ncnt : 0);
+                        rb[it][r] = load8_masked(ops, Bb, b_off[it] + r * ldb, gk < kend ? ncnt : 0);
                     }
                 }
         }
@@ -295,7 +305,7 @@ gemm_kernel(GemmParams p_in)
         for (int it = 0; it < A_IT; ++it)
             if (A_UNITS % NT == 0 || tid + it * NT < A_UNITS) {
                 const int r = a_row[it];
-                *(u32x4 *)(sA + r * ROWB + ((a_c[it] ^ swz(r)) << 4)) = ra[it];
+                ops.lds_write16(sA + r * ROWB + ((a_c[it] ^ swz(r)) << 4), ra[it]);
             }
 #pragma unroll
         for (int it = 0; it < B_IT; ++it)
@@ -303,7 +313,7 @@ gemm_kernel(GemmParams p_in)
 #pragma unroll
                 for (int c = 0; c < 8; ++c) {
                     const int n = b_ng[it] * 8 + c;
-                    *(u32x4 *)(sB + n * ROWB + ((b_kg[it] ^ swz(n)) << 4)) = column8(rb[it], c);
+                    ops.lds_write16(sB + n * ROWB + ((b_kg[it] ^ swz(n)) << 4), column8(rb[it], c));
                 }
             }
     };
@@ -333,24 +343,24 @@ gemm_kernel(GemmParams p_in)
             u32x4 fa[FM], fb[FN];
 #pragma unroll
             for (int i = 0; i < FM; ++i)
-                fa[i] = *(const u32x4 *)(sA + i * 32 * ROWB + co);
+                fa[i] = ops.read16(sA + i * 32 * ROWB + co);
 #pragma unroll
             for (int j = 0; j < FN; ++j)
-                fb[j] = *(const u32x4 *)(sB + j * 32 * ROWB + co);
+                fb[j] = ops.read16(sB + j * 32 * ROWB + co);
             // B fragment as the first operand: the result lands with lanes
             // along rows of C and 4 consecutive columns per register quad.
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
-                    acc[i][j] = mfma32<DT>(fb[j], fa[i], acc[i][j]);
+                    acc[i][j] = ops.template mfma<DT>(fb[j], fa[i], acc[i][j]);
         }
     };
 
     if (nk > 0) {
         load_tiles(kbeg);
         store_tiles(0);
-        __syncthreads();
+        ops.sync();
         for (int kt = 0; kt < nk; ++kt) {
             const int cur = kt & 1;
             if (kt + 1 < nk)
@@ -358,7 +368,7 @@ gemm_kernel(GemmParams p_in)
             compute(cur);
             if (kt + 1 < nk)
                 store_tiles(cur ^ 1);
-            __syncthreads();
+            ops.sync();
         }
     }
 
@@ -382,12 +392,12 @@ gemm_kernel(GemmParams p_in)
                 v.z = acc[i][j][4 * q + 2];
                 v.w = acc[i][j][4 * q + 3];
                 if (vec_store) {
-                    *(f32x4 *)(Cb + (int64_t)(row - ov.r0) * ldc + (col - ov.c0)) = v;
+                    ops.store4(Cb + (int64_t)(row - ov.r0) * ldc + (col - ov.c0), v);
                 } else if (row < p.M) {
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         if (col + e < p.N)
-                            Cb[(int64_t)(row - ov.r0) * ldc + (col - ov.c0) + e] = v[e];
+                            ops.store1(Cb + (int64_t)(row - ov.r0) * ldc + (col - ov.c0) + e, v[e]);
                 }
             }
         }
@@ -516,7 +526,21 @@ struct DeviceOps {
     __device__ __forceinline__ void fence() const { sched_fence(); }
     __device__ __forceinline__ void store4(float *q, f32x4 v) const { *(f32x4 *)q = v; }
     __device__ __forceinline__ void store1(float *q, float v) const { *q = v; }
+    // general kernel: loads into registers, LDS writes, a full barrier
+    __device__ __forceinline__ u32x4 gload16(const uint16_t *q) const { return *(const u32x4 *)q; }
+    __device__ __forceinline__ uint16_t gload2(const uint16_t *q) const { return *q; }
+    __device__ __forceinline__ void lds_write16(char *q, u32x4 v) const { *(u32x4 *)q = v; }
+    __device__ __forceinline__ void sync() const { __syncthreads(); }
 };
+
+template <int BM, int BN, int BK, int WGM, int WGN, int DT>
+__global__ void __launch_bounds__(WGM * WGN * 64)
+gemm_kernel(GemmParams p_in)
+{
+    __shared__ __attribute__((aligned(16))) char smem[general_lds_bytes<BM, BN, BK>()];
+    const DeviceOps ops{smem};
+    general_tile<BM, BN, BK, WGM, WGN, DT>(ops, p_in, blockIdx.x, gridDim.x, threadIdx.x);
+}
 
 // LDS bytes the pipelined kernel allocates.
 template <int BM, int BN, int BK, int STAGES>

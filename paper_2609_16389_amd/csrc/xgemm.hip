@@ -238,6 +238,23 @@ auto with_dma_tile(int tile, F &&f)
     }
 }
 
+// Template arguments of the general kernel per tile, shared by launches and
+// traces like DmaTile.
+template <int BM_, int BN_>
+struct GeneralTile {
+    static constexpr int BM = BM_, BN = BN_, BK = 64, WGM = 2, WGN = 2;
+};
+
+template <class F>
+auto with_general_tile(int tile, F &&f)
+{
+    switch (tile) {
+    case XGEMM_TILE_256x256: return f(GeneralTile<256, 256>{});
+    case XGEMM_TILE_256x128: return f(GeneralTile<256, 128>{});
+    default: return f(GeneralTile<128, 128>{});
+    }
+}
+
 hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int grid, hipStream_t s)
 {
     if (tile < 0 || tile >= XGEMM_TILE_COUNT)
@@ -247,11 +264,10 @@ hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int g
             using T = decltype(t);
             return launch_dma<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN>(dtype, p, grid, s);
         });
-    switch (tile) {
-    case XGEMM_TILE_256x256: return launch_gemm<256, 256, 64, 2, 2>(dtype, p, grid, s);
-    case XGEMM_TILE_256x128: return launch_gemm<256, 128, 64, 2, 2>(dtype, p, grid, s);
-    default: return launch_gemm<128, 128, 64, 2, 2>(dtype, p, grid, s);
-    }
+    return with_general_tile(tile, [&](auto t) {
+        using T = decltype(t);
+        return launch_gemm<T::BM, T::BN, T::BK, T::WGM, T::WGN>(dtype, p, grid, s);
+    });
 }
 
 template <int BM, int BN>
@@ -698,6 +714,23 @@ struct TraceOps {
     void fence() const {}
     void store4(float *q, xgemm_dev::f32x4) const { push(XGEMM_TRACE_STORE, 16, 0, (int64_t)(uintptr_t)q); }
     void store1(float *q, float) const { push(XGEMM_TRACE_STORE, 4, 0, (int64_t)(uintptr_t)q); }
+    xgemm_dev::u32x4 gload16(const uint16_t *q) const
+    {
+        push(XGEMM_TRACE_LOAD, 16, 0, (int64_t)(uintptr_t)q);
+        return xgemm_dev::u32x4{0, 0, 0, 0};
+    }
+    uint16_t gload2(const uint16_t *q) const
+    {
+        push(XGEMM_TRACE_LOAD, 2, 0, (int64_t)(uintptr_t)q);
+        return 0;
+    }
+    void lds_write16(char *q, xgemm_dev::u32x4) const { push(XGEMM_TRACE_LDS_WRITE, 16, q - base, 0); }
+    // __syncthreads: the compiler emits s_waitcnt lgkmcnt(0) and s_barrier
+    void sync() const
+    {
+        push(XGEMM_TRACE_WAIT_LGKM, 0, 0, 0);
+        push(XGEMM_TRACE_BARRIER, 0, 0, 0);
+    }
 };
 
 // Host stand-in for the GEMV kernel's operations.  Lanes whose masked LDS
@@ -889,7 +922,10 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
     info->lds_bytes = g.dma ? with_dma_tile(plan.tile, [](auto t) {
         using T = decltype(t);
         return xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>();
-    }) : 0;
+    }) : with_general_tile(plan.tile, [](auto t) {
+        using T = decltype(t);
+        return xgemm_dev::general_lds_bytes<T::BM, T::BN, T::BK>();
+    });
     info->split = g.p.split;
     info->grid = g.grid;
     info->workspace_bytes = (int64_t)plan.ws;
@@ -911,29 +947,41 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
     Segment &g = plan.seg[segment];
     if (block < 0 || block >= g.grid)
         return XGEMM_ERR_INVALID_ARG;
-    if (!g.dma)
-        return XGEMM_ERR_UNSUPPORTED;
     if (g.reduce) {
         if (!W)
             return XGEMM_ERR_INVALID_ARG;
         g.p.C = W;
     }
     const int threads = kTiles[plan.tile].threads;
-    return with_dma_tile(plan.tile, [&](auto t) {
-        using T = decltype(t);
-        std::vector<char> lds(xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>());
+    // run `body(ops, tid)` for every thread, collecting each one's events
+    auto trace_threads = [&](size_t lds_bytes, auto &&body) {
+        std::vector<char> lds(lds_bytes);
         std::vector<xgemm_trace_event> ev;
         for (int tid = 0; tid < threads; ++tid) {
             ev.clear();
             const TraceOps ops{lds.data(), &ev};
-            xgemm_dev::dma_tile<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, 0>(ops, g.p, (int)block,
-                                                                                    (int)g.grid, tid);
+            body(ops, tid);
             counts[tid] = (int64_t)ev.size();
             const int64_t n = counts[tid] < capacity ? counts[tid] : capacity;
             if (n > 0)
                 memcpy(out + (int64_t)tid * capacity, ev.data(), (size_t)n * sizeof(xgemm_trace_event));
         }
         return (int)XGEMM_OK;
+    };
+    if (g.dma)
+        return with_dma_tile(plan.tile, [&](auto t) {
+            using T = decltype(t);
+            return trace_threads(xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>(),
+                                 [&](const TraceOps &ops, int tid) {
+                                     xgemm_dev::dma_tile<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, 0>(
+                                         ops, g.p, (int)block, (int)g.grid, tid);
+                                 });
+        });
+    return with_general_tile(plan.tile, [&](auto t) {
+        using T = decltype(t);
+        return trace_threads(xgemm_dev::general_lds_bytes<T::BM, T::BN, T::BK>(), [&](const TraceOps &ops, int tid) {
+            xgemm_dev::general_tile<T::BM, T::BN, T::BK, T::WGM, T::WGN, 0>(ops, g.p, (int)block, (int)g.grid, tid);
+        });
     });
 }
 
@@ -991,7 +1039,7 @@ const char *xgemm_strerror(int status)
     switch (status) {
     case XGEMM_OK: return "success";
     case XGEMM_ERR_INVALID_ARG: return "invalid argument";
-    case XGEMM_ERR_UNSUPPORTED: return "unsupported (device is not gfx950, or a launch the trace does not cover)";
+    case XGEMM_ERR_UNSUPPORTED: return "unsupported device (gfx950 required)";
     case XGEMM_ERR_ALLOC: return "workspace allocation failed";
     case XGEMM_ERR_HIP: return "HIP runtime error";
     default: return "unknown status";

@@ -214,9 +214,46 @@ def test_kernel_tail_split():
     assert rep.ok, [str(v) for v in rep.violations]
 
 
-def test_general_family_is_not_traced():
-    with pytest.raises(xg.XgemmError):
-        sc.check_launch(100, 100, 100, cfg(2))  # K not a multiple of 64: general kernel
+@pytest.mark.parametrize("shape,c,lds", [
+    ((100, 100, 100), cfg(2), {}),                    # K not a multiple of 64
+    ((300, 260, 448), cfg(0), {}),                    # N not a multiple of 8
+    ((256, 256, 128), cfg(1), {}),                    # 2 K steps: too few for the pipeline
+    ((129, 136, 320), cfg(2, 2), {"lda": 323}),       # lda not a multiple of 8
+    ((200, 130, 1000), cfg(1, 4), {"ldb": 131}),      # split-k over the general kernel
+])
+def test_general_kernel_traces_are_race_free(shape, c, lds):
+    info = xg.xgemm_trace_plan(*shape[:3], sc.BASE_A, lds.get("lda", shape[2]), sc.BASE_B, lds.get("ldb", shape[1]),
+                               sc.BASE_C, shape[1], c, 256, 0)
+    assert info.family == xg.XGEMM_KERNEL_GENERAL
+    rep = sc.check_launch(*shape, c, **lds)
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+def test_general_kernel_trace_structure():
+    """General kernel, n K steps: one barrier after the first tile store and
+    one per K step; each K step's tiles written to LDS once."""
+    ev, counts = sc.trace_workgroup(256, 256, 5 * 64 + 1, 5 * 64 + 1, 256, 256, cfg(0), 256, 0, 0, 256)
+    waves = sc.wave_streams(ev, counts)
+    nk = 6
+    for ws in waves:
+        assert (ws.op == sc.BARRIER).sum() == nk + 1
+        # per thread and K step: 8 of the 2048 16-byte A chunks, and one of
+        # the 256 8 x 8 B blocks written as 8 transposed columns
+        assert (ws.op == sc.LDS_WRITE).sum() == nk * (8 + 8)
+
+
+@pytest.mark.parametrize("name,keep", [
+    ("no barrier", lambda op: op != sc.BARRIER),
+    ("no LDS wait", lambda op: op != sc.WAIT_LGKM),
+])
+def test_general_kernel_planted_mistakes(name, keep):
+    ev, counts = sc.trace_workgroup(256, 256, 320, 320, 256, 256, cfg(0), 256, 0, 0, 256)
+    waves = sc.wave_streams(ev, counts)
+    lds = xg.xgemm_trace_plan(256, 256, 320, sc.BASE_A, 320, sc.BASE_B, 256, sc.BASE_C, 256, cfg(0), 256,
+                              0).lds_bytes
+    assert sc.check_workgroup_lds(waves, lds) == []
+    mutated = [edit(ws, keep=keep) for ws in waves]
+    assert sc.check_workgroup_lds(mutated, lds), name
 
 
 # ---------------------------------------------------------------------------
