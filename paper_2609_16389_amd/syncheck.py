@@ -80,12 +80,13 @@ STORE = xg.XGEMM_TRACE_STORE
 LDS_WRITE = xg.XGEMM_TRACE_LDS_WRITE
 LOAD = xg.XGEMM_TRACE_LOAD
 INACTIVE = -1        # LDS offset of a lane that sits out a lane-masked access
+VMEM = 100           # wave-stream entry: `arg` global loads or stores (vector-memory counter)
 
 
 @dataclasses.dataclass
 class Violation:
     kind: str        # raw, war, waw, uninit, lds_bounds, barrier_count, inflight_exit, divergent,
-                     # unsupported, global_bounds, coverage
+                     # global_bounds, coverage
     wave: int        # -1 when not tied to one wave
     event: int       # index in the wave's event stream (-1 if none)
     detail: str
@@ -103,41 +104,51 @@ class WaveStream:
     addr: np.ndarray   # [n, 64] int64
 
 
-def _drop_global(events, counts):
-    """Per-thread traces without their global loads and stores into
-    registers.  Those under a lane mask (edge tiles, K tails) make lanes of
-    a wave issue different numbers of them; they take part only in the
-    global checks.  A vector-memory wait after one of them would make their
-    count matter for the wait, which these kernels never do; it is reported
-    rather than modelled."""
-    threads = events.shape[0]
-    valid = np.arange(events.shape[1])[None, :] < counts[:, None]
-    keep = valid & (events["op"] != STORE) & (events["op"] != LOAD)
-    if (keep == valid).all():
-        return events, counts, False
-    first_store = np.where((valid & ~keep).any(axis=1), np.argmax(valid & ~keep, axis=1), events.shape[1])
-    after = np.arange(events.shape[1])[None, :] > first_store[:, None]
-    wait_after = bool((valid & after & (events["op"] == WAIT_VM)).any())
+def _collapse_global(events, counts):
+    """Per-thread traces with their global loads and stores into registers
+    taken out, and for every remaining event the number of such
+    vector-memory operations the thread issued since the previous remaining
+    event (``before``, one more column for those after the last).
+
+    Lane-masked global accesses (edge tiles, K tails) make lanes of a wave
+    issue different numbers of them, so they cannot stand in the wave's
+    stream one by one.  They matter to the synchronisation only through the
+    vector-memory counter, which they advance; the wave stream gets, before
+    each event, the smallest such count over the wave's lanes.  Counting
+    fewer operations than were issued makes every ``s_waitcnt vmcnt``
+    retire fewer direct loads in the model than on the hardware, so the
+    approximation can only report more, never fewer, hazards."""
+    threads, cap = events.shape
+    valid = np.arange(cap)[None, :] < counts[:, None]
+    glob = valid & ((events["op"] == STORE) | (events["op"] == LOAD))
+    if not glob.any():
+        return events, counts, np.zeros((threads, cap + 1), dtype=np.int64)
+    keep = valid & ~glob
     new_counts = keep.sum(axis=1)
-    out = np.zeros((threads, max(int(new_counts.max()), 1)), dtype=events.dtype)
+    n = max(int(new_counts.max()), 1)
+    out = np.zeros((threads, n), dtype=events.dtype)
+    before = np.zeros((threads, n + 1), dtype=np.int64)
     for t in range(threads):
-        row = events[t][keep[t]]
-        out[t, :len(row)] = row
-    return out, new_counts, wait_after
+        k = np.nonzero(keep[t])[0]
+        out[t, :len(k)] = events[t][k]
+        g = np.concatenate([[0], np.cumsum(glob[t])])      # g[i]: global ops at positions < i
+        at = g[k]
+        before[t, :len(k)] = np.diff(np.concatenate([[0], at]))
+        before[t, len(k)] = g[counts[t]] - (at[-1] if len(k) else 0)
+    return out, new_counts, before
 
 
 def wave_streams(events: np.ndarray, counts: np.ndarray, violations: list | None = None):
     """Group a workgroup trace (threads x capacity records, per-thread
     counts) into per-wave streams of its direct LDS loads, LDS reads and
-    writes, waits and barriers.  Lanes of one wave must issue the same operations with the
-    same wave-uniform operands; a lane that does not is reported as a
-    divergence and the wave's stream is cut there."""
+    writes, waits and barriers, with VMEM entries standing for the global
+    loads and stores between them (see _collapse_global).  Lanes of one
+    wave must issue the same operations with the same wave-uniform
+    operands; a lane that does not is reported as a divergence and the
+    wave's stream is cut there."""
     threads = events.shape[0]
     assert threads % LANES == 0
-    events, counts, wait_after_global = _drop_global(events, counts)
-    if wait_after_global and violations is not None:
-        violations.append(Violation("unsupported", -1, -1, "vector-memory wait after a global load or store "
-                                    "into registers"))
+    events, counts, before = _collapse_global(events, counts)
     out = []
     for w in range(threads // LANES):
         lanes = slice(w * LANES, (w + 1) * LANES)
@@ -158,8 +169,24 @@ def wave_streams(events: np.ndarray, counts: np.ndarray, violations: list | None
                 violations.append(Violation("divergent", w, cut, "lanes disagree on the operation"))
             n = cut
             op, arg, ev = op[:n], arg[:n], ev[:, :n]
-        out.append(WaveStream(op=op, arg=arg, lds=np.ascontiguousarray(ev["lds"].T),
-                              addr=np.ascontiguousarray(ev["addr"].T)))
+        vm = before[lanes, :n + 1].min(axis=0)
+        lds = ev["lds"].T
+        addr = ev["addr"].T
+        if vm.any():
+            # insert a VMEM entry before every event (and after the last) that
+            # follows global operations in every lane
+            pos = np.nonzero(vm[:n])[0]
+            op = np.insert(op, pos, VMEM)
+            arg = np.insert(arg, pos, vm[pos].astype(arg.dtype))
+            lds = np.insert(lds, pos, 0, axis=0)
+            addr = np.insert(addr, pos, 0, axis=0)
+            if vm[n]:
+                op = np.append(op, np.int32(VMEM))
+                arg = np.append(arg, np.int32(vm[n]))
+                lds = np.vstack([lds, np.zeros((1, LANES), lds.dtype)])
+                addr = np.vstack([addr, np.zeros((1, LANES), addr.dtype)])
+        out.append(WaveStream(op=op.astype(np.int32), arg=arg.astype(np.int32), lds=np.ascontiguousarray(lds),
+                              addr=np.ascontiguousarray(addr)))
     return out
 
 
@@ -297,6 +324,8 @@ class LdsMachine:
                         self.lds_read(w, i, ws.lds[i], int(ws.arg[i]))
                     elif op == LDS_WRITE:
                         self.lds_write(w, i, ws.lds[i], int(ws.arg[i]))
+                    elif op == VMEM:
+                        self.issued["vm"][w] += int(ws.arg[i])
                     elif op == WAIT_VM:
                         self.wait(w, "vm", int(ws.arg[i]))
                     elif op == WAIT_LGKM:

@@ -44,6 +44,8 @@ def prog(*ops):
             op.append(sc.WAIT_LGKM); arg.append(o[1]); lds.append(np.zeros(64))
         elif k == "bar":
             op.append(sc.BARRIER); arg.append(0); lds.append(np.zeros(64))
+        elif k == "vmem":
+            op.append(sc.VMEM); arg.append(o[1]); lds.append(np.zeros(64))
         else:
             raise ValueError(k)
     n = len(op)
@@ -135,6 +137,32 @@ def test_load_in_flight_at_exit():
 def test_lds_bounds():
     assert "lds_bounds" in verdict(prog(("load", LDS - 16), ("wvm", 0)))
     assert "lds_bounds" in verdict(prog(("load", 0), ("wvm", 0), ("read8", np.full(64, -8))))
+
+
+def test_global_stores_count_in_the_vector_memory_counter():
+    # a direct load, then 3 global stores: vmcnt(3) retires the load, vmcnt(4) does not
+    assert verdict(prog(("load", 0), ("vmem", 3), ("wvm", 3), ("read", 0), ("wvm", 0))) == set()
+    assert verdict(prog(("load", 0), ("vmem", 3), ("wvm", 4), ("read", 0), ("wvm", 0))) == {"raw"}
+
+
+def test_masked_global_runs_count_their_minimum_over_lanes():
+    """Lane 0 issues 2 stores, the other lanes 3, between a direct load and a
+    wait: the wave stream counts 2, so vmcnt(2) retires the load in the model
+    (as on the hardware, which issued at least 2) but vmcnt(3) does not."""
+    def trace(wait):
+        ev = np.zeros((64, 8), dtype=xg.TRACE_EVENT_DTYPE)
+        counts = np.zeros(64, dtype=np.int64)
+        for lane in range(64):
+            row = [(sc.LDS_LOAD, 16, 0, 0)] + [(sc.STORE, 4, 0, 1 << 40)] * (2 if lane == 0 else 3) + \
+                  [(sc.WAIT_VM, wait, 0, 0), (sc.LDS_READ, 16, 16 * lane, 0), (sc.WAIT_VM, 0, 0, 0)]
+            counts[lane] = len(row)
+            for i, r in enumerate(row):
+                ev[lane, i] = r
+        return sc.wave_streams(ev, counts)
+    waves = trace(2)
+    assert list(waves[0].op[:3]) == [sc.LDS_LOAD, sc.VMEM, sc.WAIT_VM] and waves[0].arg[1] == 2
+    assert sc.check_workgroup_lds(waves, LDS) == []
+    assert {v.kind for v in sc.check_workgroup_lds(trace(3), LDS)} == {"raw"}
 
 
 def test_per_lane_read_granules():
