@@ -275,21 +275,29 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
  *     y[i] = sum over k of A[i][k] * x[k]
  *
  * Products and sums are fp32 (fused multiply-adds); the summation is
- * grouped (per-thread partial sums, then a tree), so for every i, with
- * n = 4 * ceil(K / 1024) + 10 roundings on the longest path,
- *     |y[i] - exact| <= n * 2^-24 * sum_k |A[i][k] x[k]| + (K + 255) * 2^-150
+ * grouped (per-thread partial sums, then a tree, then, with a K split
+ * into s ranges, a sum over the ranges), so for every i, with
+ * n = 4 * ceil(K / 1024) + 10 roundings on the longest path (which bounds
+ * the path 4 * ceil(K / (1024 s)) + 10 + s - 1 of a split, since s never
+ * exceeds ceil(K / 1024)),
+ *     |y[i] - exact| <= n * 2^-24 * sum_k |A[i][k] x[k]| + (K + 256 s) * 2^-150
  * (up to second-order terms; the last term bounds rounding in the
- * subnormal range, summed over the K + 255 operations that form y[i]),
+ * subnormal range, summed over the K + 256 s - 1 operations that form y[i]),
  * where "exact" is the real-number result on the stored inputs.  Subnormal
  * inputs and results are kept, not flushed to zero.
  */
 
 /* GEMV launch configuration: rows of A per 256-thread workgroup (1, 2, 4 or
-   8) and 16-byte chunks of x each thread loads per loop iteration (1, 2 or
-   4; A's rows are loaded the same number of chunks ahead). */
+   8), 16-byte chunks of x each thread loads per loop iteration (1, 2 or 4;
+   A's rows are loaded the same number of chunks ahead), and the number of K
+   ranges (1 .. 256): with split_k > 1 each workgroup sums one range of its
+   rows into the handle's workspace and a second launch adds the ranges'
+   partial sums in ascending order, which keeps the GPU busy when M is
+   small. */
 typedef struct xgemv_config {
     int32_t rows;
     int32_t unroll;
+    int32_t split_k;
 } xgemv_config;
 
 /*
@@ -302,16 +310,19 @@ typedef struct xgemv_config {
  * A pointer may be NULL only when it addresses no element.  16-byte loads
  * need A and x 16-byte aligned and lda a multiple of 4; any other alignment
  * is still correct through 4-byte loads.  The handle supplies the device's
- * CU count; GEMV uses no workspace.  Errors: XGEMM_ERR_INVALID_ARG for a
- * NULL handle, bad sizes or pointers; XGEMM_ERR_HIP if the launch fails.
- * Nothing is enqueued on error.
+ * CU count, and its workspace holds the partial sums of a K split
+ * (split_k * M floats; calls that share a handle must be ordered on one
+ * stream).  Errors: XGEMM_ERR_INVALID_ARG for a NULL handle, bad sizes or
+ * pointers; XGEMM_ERR_ALLOC if the workspace cannot grow; XGEMM_ERR_HIP if a
+ * launch fails.  Nothing is enqueued on error.
  */
 int xgemv_run(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
               void *stream);
 
 /* As xgemv_run with the configuration forced (XGEMM_ERR_INVALID_ARG for an
-   unsupported one).  The result is the same bit for bit for every unroll;
-   rows changes only which workgroup computes a row, not its arithmetic. */
+   unsupported one).  For a given split_k the result is the same bit for bit
+   for every rows and unroll: they change only which workgroup computes a
+   row and how far ahead it loads, not its arithmetic. */
 int xgemv_run_config(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x,
                      float *y, void *stream, const xgemv_config *cfg);
 
@@ -321,12 +332,14 @@ int xgemv_run_config(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int
 int xgemv_select_config(int64_t M, int64_t K, int cu_count, xgemv_config *out);
 
 /*
- * Trace of GEMV workgroup `block` (0 .. ceil(M / cfg->rows) - 1) in the
- * format of xgemm_trace_workgroup (256 threads; A, x and y are only used as
- * addresses).  M and K must be > 0.  XGEMM_ERR_INVALID_ARG for invalid
- * arguments, a block out of range, counts == NULL or an unsupported cfg.
+ * Trace of GEMV workgroup `block` (0 .. ceil(M / cfg->rows) * s - 1, s the
+ * split left after empty K ranges are dropped) in the format of
+ * xgemm_trace_workgroup (256 threads; A, x, y and W, the partial sums of a
+ * split, are only used as addresses).  M and K must be > 0.
+ * XGEMM_ERR_INVALID_ARG for invalid arguments, a block out of range,
+ * counts == NULL, W == NULL with a split, or an unsupported cfg.
  */
-int xgemv_trace_workgroup(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+int xgemv_trace_workgroup(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y, float *W,
                           const xgemv_config *cfg, int64_t block, xgemm_trace_event *out, int64_t capacity,
                           int64_t *counts);
 

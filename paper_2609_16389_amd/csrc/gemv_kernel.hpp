@@ -5,7 +5,9 @@
 // element of A is read once for one multiply-add, so the ideal time is the
 // time to stream A from HBM.
 //
-// Workgroup: 256 threads (4 waves) own R consecutive rows.  The K range is
+// Workgroup: 256 threads (4 waves) own R consecutive rows (and, when the
+// rows alone give too few workgroups to fill the GPU, one of `split` K
+// ranges of them; a second kernel then adds the ranges' partial sums).  The K range is
 // cut into 16-byte chunks of 4 values; thread t takes chunks t, t + 256,
 // t + 512, ... of every one of its R rows, so that each load instruction of
 // a wave reads 1 KiB of one row contiguously.  Per iteration a thread
@@ -31,9 +33,12 @@ struct GemvParams {
     const float *A;
     const float *x;
     float *y;
+    float *part;  // split > 1: partial sums, part[q * M + i] for K range q
     int64_t lda;
     int M, K;
-    int vec;  // A and x 16-byte aligned and lda a multiple of 4: 16-byte loads
+    int k_chunk;  // K values per split, a multiple of 4 (K when split == 1)
+    int split;
+    int vec;      // A and x 16-byte aligned and lda a multiple of 4: 16-byte loads
 };
 
 // Operations of the GEMV kernel on the device (the body below is also run on
@@ -78,30 +83,39 @@ __host__ __device__ __forceinline__ float fma4(f32x4 a, f32x4 b, float acc)
     return acc;
 }
 
-// Rows [block * R, block * R + R) of y, as seen by thread tid.
+// Workgroup `block` is K range q = block / ceil(M / R) (the range's splits
+// outermost, so that the workgroups reading one slice of x run together)
+// and rows [rb * R, rb * R + R) with rb = block % ceil(M / R); thread tid's
+// part of it.  Without a split (q = 0, the whole K range) the rows' sums go
+// to y, otherwise to the partials.
 template <int R, int U, class Ops>
 __host__ __device__ __forceinline__ void gemv_block(const Ops &ops, const GemvParams &p, int block, int tid)
 {
-    const int row0 = block * R;
+    const int row_blocks = (p.M + R - 1) / R;
+    const int q = block / row_blocks;
+    const int row0 = (block - q * row_blocks) * R;
+    const int kb = q * p.k_chunk;
+    const int kn = min(p.K, kb + p.k_chunk) - kb;   // K values of this range
+    const float *xq = p.x + kb;
     const int lane = tid & 63, wave = tid >> 6;
     // rows past M read the last row (their sums are never stored)
     const float *arow[R];
 #pragma unroll
     for (int r = 0; r < R; ++r)
-        arow[r] = p.A + (int64_t)min(row0 + r, p.M - 1) * p.lda;
+        arow[r] = p.A + (int64_t)min(row0 + r, p.M - 1) * p.lda + kb;
     float acc[R];
 #pragma unroll
     for (int r = 0; r < R; ++r)
         acc[r] = 0.0f;
 
-    const int K4 = p.K / 4;  // whole chunks of 4 values
+    const int K4 = kn / 4;  // whole chunks of 4 values
     int c = tid;
     if (p.vec) {
         for (; c + (U - 1) * kThreads < K4; c += U * kThreads) {
             f32x4 xv[U], av[R][U];
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                xv[u] = ops.load4(p.x + 4 * (c + u * kThreads));
+                xv[u] = ops.load4(xq + 4 * (c + u * kThreads));
 #pragma unroll
             for (int r = 0; r < R; ++r)
 #pragma unroll
@@ -114,7 +128,7 @@ __host__ __device__ __forceinline__ void gemv_block(const Ops &ops, const GemvPa
                     acc[r] = fma4(av[r][u], xv[u], acc[r]);
         }
         for (; c < K4; c += kThreads) {
-            const f32x4 xv = ops.load4(p.x + 4 * c);
+            const f32x4 xv = ops.load4(xq + 4 * c);
 #pragma unroll
             for (int r = 0; r < R; ++r)
                 acc[r] = fma4(ops.load4(arow[r] + 4 * c), xv, acc[r]);
@@ -122,10 +136,10 @@ __host__ __device__ __forceinline__ void gemv_block(const Ops &ops, const GemvPa
     } else {
         for (; c < K4; c += kThreads) {
             f32x4 xv;
-            xv.x = ops.load1(p.x + 4 * c);
-            xv.y = ops.load1(p.x + 4 * c + 1);
-            xv.z = ops.load1(p.x + 4 * c + 2);
-            xv.w = ops.load1(p.x + 4 * c + 3);
+            xv.x = ops.load1(xq + 4 * c);
+            xv.y = ops.load1(xq + 4 * c + 1);
+            xv.z = ops.load1(xq + 4 * c + 2);
+            xv.w = ops.load1(xq + 4 * c + 3);
 #pragma unroll
             for (int r = 0; r < R; ++r) {
                 f32x4 av;
@@ -137,10 +151,10 @@ __host__ __device__ __forceinline__ void gemv_block(const Ops &ops, const GemvPa
             }
         }
     }
-    // the last K % 4 values, one per thread
+    // the range's last kn % 4 values, one per thread
     const int kt = 4 * K4 + tid;
-    if (kt < p.K) {
-        const float xs = ops.load1(p.x + kt);
+    if (kt < kn) {
+        const float xs = ops.load1(xq + kt);
 #pragma unroll
         for (int r = 0; r < R; ++r)
             acc[r] = fmaf(ops.load1(arow[r] + kt), xs, acc[r]);
@@ -161,7 +175,19 @@ __host__ __device__ __forceinline__ void gemv_block(const Ops &ops, const GemvPa
     for (int w = 1; w < kWaves; ++w)
         s += ops.lds_read1(red + w * R + r, own);
     if (own)
-        ops.store1(p.y + row0 + tid, s);
+        ops.store1(p.split == 1 ? p.y + row0 + tid : p.part + (int64_t)q * p.M + row0 + tid, s);
+}
+
+// y[i] = sum over q of part[q * M + i], q ascending (a fixed order).
+__global__ void __launch_bounds__(256)
+gemv_reduce(const float *part, int split, int M, float *y)
+{
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += gridDim.x * blockDim.x) {
+        float s = part[i];
+        for (int q = 1; q < split; ++q)
+            s += part[(int64_t)q * M + i];
+        y[i] = s;
+    }
 }
 
 template <int R, int U>

@@ -418,6 +418,35 @@ int make_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const
     return XGEMM_OK;
 }
 
+// Grow the handle's workspace to `bytes` (never shrinks).  The old one may
+// still be in use by work enqueued on this stream, so the stream is
+// synchronised before it is freed.
+int ensure_workspace(xgemm_ctx *h, size_t bytes, hipStream_t s)
+{
+    if (bytes <= h->ws_bytes)
+        return XGEMM_OK;
+    hipError_t e;
+    if (h->workspace) {
+        e = hipStreamSynchronize(s);
+        if (e != hipSuccess) {
+            set_error(h, "hipStreamSynchronize", e);
+            return XGEMM_ERR_HIP;
+        }
+        (void)hipFree(h->workspace);
+        h->workspace = nullptr;
+        h->ws_bytes = 0;
+    }
+    e = hipMalloc(&h->workspace, bytes);
+    if (e != hipSuccess) {
+        h->workspace = nullptr;
+        (void)hipGetLastError();
+        set_error(h, "hipMalloc workspace", e);
+        return XGEMM_ERR_ALLOC;
+    }
+    h->ws_bytes = bytes;
+    return XGEMM_OK;
+}
+
 int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
         int64_t ldb, float *C, int64_t ldc, int dtype, void *stream, const xgemm_config *forced)
 {
@@ -453,27 +482,9 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     if (rc != XGEMM_OK)
         return rc;
 
-    if (plan.ws > h->ws_bytes) {
-        // the old workspace may still be in use by work on this stream
-        if (h->workspace) {
-            e = hipStreamSynchronize(s);
-            if (e != hipSuccess) {
-                set_error(h, "hipStreamSynchronize", e);
-                return XGEMM_ERR_HIP;
-            }
-            (void)hipFree(h->workspace);
-            h->workspace = nullptr;
-            h->ws_bytes = 0;
-        }
-        e = hipMalloc(&h->workspace, plan.ws);
-        if (e != hipSuccess) {
-            h->workspace = nullptr;
-            (void)hipGetLastError();
-            set_error(h, "hipMalloc workspace", e);
-            return XGEMM_ERR_ALLOC;
-        }
-        h->ws_bytes = plan.ws;
-    }
+    rc = ensure_workspace(h, plan.ws, s);
+    if (rc != XGEMM_OK)
+        return rc;
 
     const int vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
     for (int i = 0; i < plan.nseg; ++i) {
@@ -573,7 +584,20 @@ using xgemv_dev::GemvParams;
 bool valid_gemv_config(const xgemv_config *c)
 {
     return c && (c->rows == 1 || c->rows == 2 || c->rows == 4 || c->rows == 8) &&
-           (c->unroll == 1 || c->unroll == 2 || c->unroll == 4);
+           (c->unroll == 1 || c->unroll == 2 || c->unroll == 4) && c->split_k >= 1 && c->split_k <= 256;
+}
+
+// K values per split (a multiple of 4, so that every range starts on a
+// 16-byte boundary of an aligned row) and the split left after trailing
+// empty ranges are dropped.
+int gemv_split(int64_t K, int split, int64_t *k_chunk)
+{
+    *k_chunk = cdiv(cdiv(K, split), 4) * 4;
+    while (split > 1 && *k_chunk * (split - 1) >= K) {
+        --split;
+        *k_chunk = cdiv(cdiv(K, split), 4) * 4;
+    }
+    return split;
 }
 
 // Measured on MI355X (interleaved sweeps over 4096^2 .. 32768^2, 1024 x
@@ -582,11 +606,26 @@ bool valid_gemv_config(const xgemv_config *c)
 // configuration whenever that still leaves at least four workgroups per CU;
 // below that one row per workgroup keeps more CUs streaming (at 256 x
 // 262144 it reads 6.2 TB/s against 4.1 TB/s with two chunks in flight).
+//
+// Fewer than two workgroups per CU leave CUs idle; then K is split so that
+// there are about that many, but with at least 65536 values in every range
+// (shorter ranges cost more in per-workgroup start-up and partial sums
+// than they gain) and at most 256 ranges.  Measured: 64 x 2^20 reads
+// 5.6 TB/s split 8 ways against 1.8 TB/s unsplit; 1 x 2^22 2.9 TB/s split
+// 64 ways (0.09 TB/s unsplit, 1.6 TB/s split 256 ways).
 void select_gemv(int64_t M, int64_t K, int cu_count, xgemv_config *out)
 {
-    (void)K;
     out->rows = M >= 8 * (int64_t)cu_count ? 2 : 1;
     out->unroll = 4;
+    const int64_t blocks = cdiv(M, out->rows);
+    int64_t split = 1;
+    if (blocks < 2 * (int64_t)cu_count) {
+        split = cdiv(2 * (int64_t)cu_count, blocks);
+        split = split < K / 65536 ? split : K / 65536;
+        split = split < 256 ? split : 256;
+        split = split > 1 ? split : 1;
+    }
+    out->split_k = (int)split;
 }
 
 template <class F>
@@ -614,15 +653,20 @@ int check_gemv_args(int64_t M, int64_t K, const float *A, int64_t lda, const flo
     return XGEMM_OK;
 }
 
-GemvParams gemv_params(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y)
+GemvParams gemv_params(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+                       int split_k, float *part)
 {
     GemvParams p;
     p.A = A;
     p.x = x;
     p.y = y;
+    p.part = part;
     p.lda = lda;
     p.M = (int)M;
     p.K = (int)K;
+    int64_t kc;
+    p.split = gemv_split(K, split_k, &kc);
+    p.k_chunk = (int)kc;
     p.vec = ((uintptr_t)A % 16 == 0) && ((uintptr_t)x % 16 == 0) && (lda % 4 == 0);
     return p;
 }
@@ -650,13 +694,24 @@ int run_gemv(xgemm_ctx *h, int64_t M, int64_t K, const float *A, int64_t lda, co
             cfg = *forced;
         else
             select_gemv(M, K, h->cu_count, &cfg);
-        const GemvParams p = gemv_params(M, K, A, lda, x, y);
+        GemvParams p = gemv_params(M, K, A, lda, x, y, cfg.split_k, nullptr);
+        if (p.split > 1) {
+            rc = ensure_workspace(h, (size_t)p.split * (size_t)M * sizeof(float), s);
+            if (rc != XGEMM_OK)
+                return rc;
+            p.part = (float *)h->workspace;
+        }
         with_gemv_config(cfg, [&](auto r, auto u) {
             constexpr int R = decltype(r)::value, U = decltype(u)::value;
-            hipLaunchKernelGGL((xgemv_dev::gemv_kernel<R, U>), dim3((unsigned)cdiv(M, R)),
+            hipLaunchKernelGGL((xgemv_dev::gemv_kernel<R, U>), dim3((unsigned)(cdiv(M, R) * p.split)),
                                dim3(xgemv_dev::kThreads), 0, s, p);
             return 0;
         });
+        if (p.split > 1) {
+            const int grid = (int)(cdiv(M, 256) < 1024 ? cdiv(M, 256) : 1024);
+            hipLaunchKernelGGL(xgemv_dev::gemv_reduce, dim3(grid), dim3(256), 0, s, (const float *)p.part,
+                               p.split, (int)M, y);
+        }
     }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) {
@@ -1007,16 +1062,16 @@ int xgemv_select_config(int64_t M, int64_t K, int cu_count, xgemv_config *out)
     return XGEMM_OK;
 }
 
-int xgemv_trace_workgroup(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+int xgemv_trace_workgroup(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y, float *W,
                           const xgemv_config *cfg, int64_t block, xgemm_trace_event *out, int64_t capacity,
                           int64_t *counts)
 {
     if (!counts || capacity < 0 || (capacity > 0 && !out) || !valid_gemv_config(cfg) || M <= 0 || K <= 0 ||
         check_gemv_args(M, K, A, lda, x, y) != XGEMM_OK)
         return XGEMM_ERR_INVALID_ARG;
-    if (block < 0 || block >= cdiv(M, cfg->rows))
+    const GemvParams p = gemv_params(M, K, A, lda, x, y, cfg->split_k, W);
+    if (block < 0 || block >= cdiv(M, cfg->rows) * p.split || (p.split > 1 && !W))
         return XGEMM_ERR_INVALID_ARG;
-    const GemvParams p = gemv_params(M, K, A, lda, x, y);
     return with_gemv_config(*cfg, [&](auto r, auto u) {
         constexpr int R = decltype(r)::value, U = decltype(u)::value;
         std::vector<float> lds(xgemv_dev::kWaves * R);

@@ -568,7 +568,7 @@ def trace_gemv_workgroup(M, K, lda, cfg, block, capacity=None):
     threads = 256
     counts = np.zeros(threads, dtype=np.int64)
     cptr = counts.ctypes.data_as(ctypes.c_void_p)
-    args = (M, K, BASE_A, lda, BASE_B, BASE_C, ctypes.byref(cfg), block)
+    args = (M, K, BASE_A, lda, BASE_B, BASE_C, BASE_W, ctypes.byref(cfg), block)
     if capacity is None:
         rc = xg.lib.xgemv_trace_workgroup(*args, None, 0, cptr)
         if rc != xg.XGEMM_OK:
@@ -583,20 +583,41 @@ def trace_gemv_workgroup(M, K, lda, cfg, block, capacity=None):
     return ev, counts
 
 
+def gemv_split(K, split):
+    """The K split a GEMV launch runs after empty trailing ranges are
+    dropped, and the K values per range (the library's rule)."""
+    def chunk(s):
+        return -(-(-(-K // s)) // 4) * 4
+    kc = chunk(split)
+    while split > 1 and kc * (split - 1) >= K:
+        split -= 1
+        kc = chunk(split)
+    return split, kc
+
+
 def check_gemv_launch(M, K, cfg, lda=None):
     """Trace every workgroup of the GEMV launch and run the checks: the LDS
     machine on each distinct workgroup stream, global loads inside A and x,
-    and every y[i] stored exactly once."""
+    and every y[i] (or, with a K split, every partial sum) stored exactly
+    once.  The partial sums are added by a later launch on the same stream."""
+    import ctypes
     lda = K if lda is None else lda
     t0 = time.perf_counter()
     violations: list[Violation] = []
     lds_seen = set()
     n_events = 0
-    grid = -(-M // cfg.rows)
+    split, _ = gemv_split(K, cfg.split_k)
+    grid = -(-M // cfg.rows) * split
+    counts = np.zeros(256, dtype=np.int64)
+    beyond = xg.lib.xgemv_trace_workgroup(M, K, BASE_A, lda, BASE_B, BASE_C, BASE_W, ctypes.byref(cfg), grid, None,
+                                          0, counts.ctypes.data_as(ctypes.c_void_p))
+    if beyond != xg.XGEMM_ERR_INVALID_ARG:
+        violations.append(Violation("coverage", -1, -1, "the library runs more than %d workgroups" % grid))
     lds_bytes = 4 * 4 * cfg.rows
     a_lo, a_hi = BASE_A, BASE_A + 4 * ((M - 1) * lda + K)
     x_lo, x_hi = BASE_B, BASE_B + 4 * K
-    cov = np.zeros(M, dtype=np.int64)
+    out_base = BASE_C if split == 1 else BASE_W
+    cov = np.zeros(M * split, dtype=np.int64)
     for block in range(grid):
         ev, counts = trace_gemv_workgroup(M, K, lda, cfg, block)
         n_events += int(counts.sum())
@@ -608,10 +629,11 @@ def check_gemv_launch(M, K, cfg, lda=None):
             violations.append(Violation("global_bounds", -1, -1, "workgroup %d: load outside A and x at %#x"
                                         % (block, int(ga[~inside][0]))))
         st = valid & (ev["op"] == STORE)
-        off = ev["addr"][st] - BASE_C
-        ok = (off >= 0) & (off % 4 == 0) & (off // 4 < M) & (ev["arg"][st] == 4)
+        off = ev["addr"][st] - out_base
+        ok = (off >= 0) & (off % 4 == 0) & (off // 4 < M * split) & (ev["arg"][st] == 4)
         if not ok.all():
-            violations.append(Violation("global_bounds", -1, -1, "workgroup %d: store outside y" % block))
+            violations.append(Violation("global_bounds", -1, -1, "workgroup %d: store outside %s" %
+                                        (block, "y" if split == 1 else "the partial sums")))
         np.add.at(cov, off[ok] // 4, 1)
         key = hashlib.sha1()
         for f in ("op", "arg", "lds"):
@@ -626,8 +648,8 @@ def check_gemv_launch(M, K, cfg, lda=None):
                 v.detail = "workgroup %d: %s" % (block, v.detail)
                 violations.append(v)
     if (cov != 1).any():
-        violations.append(Violation("coverage", -1, -1, "%d entries of y not stored exactly once"
-                                    % int((cov != 1).sum())))
+        violations.append(Violation("coverage", -1, -1, "%d entries of %s not stored exactly once"
+                                    % (int((cov != 1).sum()), "y" if split == 1 else "the partial sums")))
     return LaunchReport(shape=(M, K), config=repr(cfg), segments=1, workgroups=grid, lds_classes=len(lds_seen),
                         events=n_events, seconds=time.perf_counter() - t0, violations=violations)
 

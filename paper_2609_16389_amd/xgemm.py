@@ -54,10 +54,13 @@ XGEMM_TRACE_LOAD = 7
 
 
 class xgemv_config(ctypes.Structure):
-    _fields_ = [("rows", ctypes.c_int32), ("unroll", ctypes.c_int32)]
+    _fields_ = [("rows", ctypes.c_int32), ("unroll", ctypes.c_int32), ("split_k", ctypes.c_int32)]
+
+    def __init__(self, rows=2, unroll=4, split_k=1):
+        super().__init__(rows, unroll, split_k)
 
     def __repr__(self):
-        return "xgemv_config(rows=%d, unroll=%d)" % (self.rows, self.unroll)
+        return "xgemv_config(rows=%d, unroll=%d, split_k=%d)" % (self.rows, self.unroll, self.split_k)
 
 
 class xgemm_trace_event(ctypes.Structure):
@@ -127,8 +130,8 @@ lib.xgemv_run_config.argtypes = [_handle_t, _i64, _i64, _p, _i64, _p, _p, _p, ct
 lib.xgemv_run_config.restype = _i32
 lib.xgemv_select_config.argtypes = [_i64, _i64, _i32, ctypes.POINTER(xgemv_config)]
 lib.xgemv_select_config.restype = _i32
-lib.xgemv_trace_workgroup.argtypes = [_i64, _i64, _p, _i64, _p, _p, ctypes.POINTER(xgemv_config), _i64, _p, _i64,
-                                      _p]
+lib.xgemv_trace_workgroup.argtypes = [_i64, _i64, _p, _i64, _p, _p, _p, ctypes.POINTER(xgemv_config), _i64, _p,
+                                      _i64, _p]
 lib.xgemv_trace_workgroup.restype = _i32
 lib.xgemm_strerror.argtypes = [_i32]
 lib.xgemm_strerror.restype = ctypes.c_char_p

@@ -143,10 +143,20 @@ def test_batched_null_handle():
 
 
 def test_gemv_selector():
-    assert (xg.xgemv_select_config(16384, 16384, 256).rows, xg.xgemv_select_config(16384, 16384, 256).unroll) == (2, 4)
+    c = xg.xgemv_select_config(16384, 16384, 256)
+    assert (c.rows, c.unroll, c.split_k) == (2, 4, 1)
     assert xg.xgemv_select_config(256, 262144, 256).rows == 1
     assert xg.xgemv_select_config(2048, 10, 256).rows == 2
     assert xg.xgemv_select_config(2047, 10, 256).rows == 1
+    # few rows: K is split until there are about two workgroups per CU, each
+    # range keeping at least 65536 values, at most 256 ranges
+    assert xg.xgemv_select_config(64, 1000000, 256).split_k == 8
+    assert xg.xgemv_select_config(1, 4194304, 256).split_k == 64
+    assert xg.xgemv_select_config(1, 300000, 256).split_k == 4
+    assert xg.xgemv_select_config(1, 100000, 256).split_k == 1
+    assert xg.xgemv_select_config(1, 2 ** 30, 256).split_k == 256
+    assert xg.xgemv_select_config(64, 3000, 256).split_k == 1
+    assert xg.xgemv_select_config(512, 10 ** 6, 256).split_k == 1
     with pytest.raises(xg.XgemmError):
         xg.xgemv_select_config(-1, 5, 256)
     with pytest.raises(xg.XgemmError):
@@ -158,12 +168,15 @@ def test_gemv_null_handle_and_trace_arguments():
     import ctypes
     counts = (ctypes.c_int64 * 256)()
     cfg = xg.xgemv_config(2, 4)
-    # block out of range, unsupported config, K == 0
-    assert xg.lib.xgemv_trace_workgroup(4, 4, 16, 4, 16, 16, ctypes.byref(cfg), 2, None, 0, counts) == \
-        xg.XGEMM_ERR_INVALID_ARG
-    bad = xg.xgemv_config(3, 4)
-    assert xg.lib.xgemv_trace_workgroup(4, 4, 16, 4, 16, 16, ctypes.byref(bad), 0, None, 0, counts) == \
-        xg.XGEMM_ERR_INVALID_ARG
-    assert xg.lib.xgemv_trace_workgroup(4, 0, 16, 4, 16, 16, ctypes.byref(cfg), 0, None, 0, counts) == \
-        xg.XGEMM_ERR_INVALID_ARG
-    assert xg.lib.xgemv_trace_workgroup(4, 4, 16, 4, 16, 16, ctypes.byref(cfg), 0, None, 0, counts) == xg.XGEMM_OK
+    tr = xg.lib.xgemv_trace_workgroup
+    # block out of range, unsupported configs, K == 0
+    assert tr(4, 4, 16, 4, 16, 16, 32, ctypes.byref(cfg), 2, None, 0, counts) == xg.XGEMM_ERR_INVALID_ARG
+    for bad in (xg.xgemv_config(3, 4), xg.xgemv_config(2, 4, 0), xg.xgemv_config(2, 4, 257)):
+        assert tr(4, 4, 16, 4, 16, 16, 32, ctypes.byref(bad), 0, None, 0, counts) == xg.XGEMM_ERR_INVALID_ARG
+    assert tr(4, 0, 16, 4, 16, 16, 32, ctypes.byref(cfg), 0, None, 0, counts) == xg.XGEMM_ERR_INVALID_ARG
+    assert tr(4, 4, 16, 4, 16, 16, 32, ctypes.byref(cfg), 0, None, 0, counts) == xg.XGEMM_OK
+    # a K split needs the partials' address and has split x row-block workgroups
+    split = xg.xgemv_config(2, 4, 2)
+    assert tr(4, 4096, 16, 4096, 16, 16, None, ctypes.byref(split), 0, None, 0, counts) == xg.XGEMM_ERR_INVALID_ARG
+    assert tr(4, 4096, 16, 4096, 16, 16, 32, ctypes.byref(split), 3, None, 0, counts) == xg.XGEMM_OK
+    assert tr(4, 4096, 16, 4096, 16, 16, 32, ctypes.byref(split), 4, None, 0, counts) == xg.XGEMM_ERR_INVALID_ARG

@@ -33,15 +33,19 @@ def _oracle_built():
     oracle.build(force=False)
 
 
-def tol(K, s):
-    n = 4 * math.ceil(K / 1024) + 10
-    return (n * 2.0 ** -24 * (1 + 1e-3) + K * 2.0 ** -52) * s + (K + 255) * 2.0 ** -150
+def tol(K, s, split=1):
+    """The bound for a K split into `split` ranges (1: none): each range of
+    at most kc values contributes 4 ceil(kc/1024) + 10 roundings, the sum
+    over ranges split - 1 more."""
+    kc = -(-K // split) if split > 1 else K
+    n = 4 * math.ceil(kc / 1024) + 10 + (split - 1)
+    return (n * 2.0 ** -24 * (1 + 1e-3) + K * 2.0 ** -52) * s + (K + 256 * split) * 2.0 ** -150
 
 
-def check(y, y_ref, s, K, what):
+def check(y, y_ref, s, K, what, split=1):
     y = np.asarray(y, dtype=np.float64)
     assert np.all(np.isfinite(y)), what
-    bad = np.abs(y - y_ref) > tol(K, s)
+    bad = np.abs(y - y_ref) > tol(K, s, split)
     if bad.any():
         i = int(np.argmax(bad))
         raise AssertionError("%s: %d of %d outside the bound; first row %d: gpu=%r ref=%r s=%r"
@@ -72,7 +76,7 @@ def run(A, x, config=None, lda=None, a_offset=0, x_offset=0):
 
 
 SHAPES = [(1, 1), (1, 5), (3, 4), (17, 1023), (255, 1025), (256, 4096), (1000, 3000), (4097, 777),
-          (5, 100003), (3000, 8), (2, 1024 * 9 + 3)]
+          (5, 100003), (3000, 8), (2, 1024 * 9 + 3), (64, 300000), (1, 262147), (200, 65536)]
 
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "%dx%d" % s)
@@ -80,7 +84,25 @@ def test_shapes_default_config(shape):
     M, K = shape
     A, x = wl.make_gemv_inputs(M, K, "uniform", M + 3 * K)
     y_ref, s = oracle.gemv(A, x)
-    check(run(A, x), y_ref, s, K, "gemv %dx%d" % shape)
+    split = xg.xgemv_select_config(M, K, torch.cuda.get_device_properties(0).multi_processor_count).split_k
+    check(run(A, x), y_ref, s, K, "gemv %dx%d" % shape, split)
+
+
+@pytest.mark.parametrize("shape,split", [((64, 100003), 8), ((5, 7), 4), ((300, 5000), 3), ((1, 300000), 64),
+                                         ((700, 4096), 2)], ids=lambda v: str(v))
+def test_forced_k_splits(shape, split):
+    """Every K split in range against the oracle; for a given split the
+    result does not depend on rows, unroll or load width."""
+    M, K = shape
+    A, x = wl.make_gemv_inputs(M, K, "normal", 17 + split)
+    y_ref, s = oracle.gemv(A, x)
+    base = run(A, x, config=xg.xgemv_config(1, 4, split))
+    # (when trailing ranges are empty and dropped, the bound for the
+    # requested split still covers the shorter path)
+    check(base, y_ref, s, K, "split %d" % split, split)
+    for r, u in [(2, 1), (4, 2), (8, 4)]:
+        assert np.array_equal(run(A, x, config=xg.xgemv_config(r, u, split)), base), (r, u)
+    assert np.array_equal(run(A, x, config=xg.xgemv_config(1, 4, split), a_offset=1, lda=K + 3), base)
 
 
 def test_every_config_is_bit_identical():

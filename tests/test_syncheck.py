@@ -412,6 +412,13 @@ def test_gemv_launch_is_race_free(shape, rows, unroll):
     assert rep.ok, [str(v) for v in rep.violations]
 
 
+@pytest.mark.parametrize("shape,split", [((64, 100003), 8), ((5, 7), 4), ((300, 5000), 3), ((1, 300000), 64)])
+def test_gemv_k_split_is_race_free(shape, split):
+    rep = sc.check_gemv_launch(*shape, xg.xgemv_config(1, 4, split))
+    assert rep.ok, [str(v) for v in rep.violations]
+    assert rep.workgroups == shape[0] * sc.gemv_split(shape[1], split)[0]
+
+
 def test_gemv_padded_rows():
     rep = sc.check_gemv_launch(77, 1001, xg.xgemv_config(4, 2), lda=1007)
     assert rep.ok, [str(v) for v in rep.violations]
