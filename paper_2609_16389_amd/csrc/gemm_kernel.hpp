@@ -75,6 +75,23 @@ __device__ __forceinline__ f32x16 mfma32<1>(u32x4 a, u32x4 b, f32x16 c)
                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
 }
 
+template <int DT>
+__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c);
+
+template <>
+__device__ __forceinline__ f32x4 mfma16<0>(u32x4 a, u32x4 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+template <>
+__device__ __forceinline__ f32x4 mfma16<1>(u32x4 a, u32x4 b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
 // 16-byte chunk slot of logical chunk c in tile row r.  Rows r and r^j for
 // j < 16 never share a slot among 8 consecutive rows, nor a (row parity,
 // slot) pair among 16 consecutive rows.
@@ -516,6 +533,11 @@ struct DeviceOps {
     {
         return mfma32<DT>(a, b, c);
     }
+    template <int DT>
+    __device__ __forceinline__ f32x4 mfma(u32x4 a, u32x4 b, f32x4 c) const
+    {
+        return mfma16<DT>(a, b, c);
+    }
     template <int N>
     __device__ __forceinline__ void wait_vm() const
     {
@@ -552,14 +574,25 @@ constexpr int dma_lds_bytes()
 // One workgroup (id `block` of `nblocks`) of the pipelined kernel, as seen
 // by thread `tid`.  The host launches it only when every split has at least
 // STAGES K steps.
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, class Ops>
+//
+// MI is the MFMA block: 32 (v_mfma_f32_32x32x16, 16 k per instruction) or
+// 16 (v_mfma_f32_16x16x32, 32 k per instruction).  Both do the same work per
+// K step from the same LDS bytes; under the power cap the 16 x 16 shape
+// runs the GPU at a higher clock (it moves half as many accumulator
+// registers per flop).
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, int MI, class Ops>
 __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmParams &p_in, int block, int nblocks,
                                                   int tid)
 {
+    static_assert(MI == 16 || MI == 32, "MFMA block");
     constexpr int NW = WGM * WGN;
     constexpr int TM = BM / WGM, TN = BN / WGN;
-    constexpr int FM = TM / 32, FN = TN / 32;
-    constexpr int KS = BK / 16;                  // MFMA k sub-steps per K step
+    constexpr int FM = TM / MI, FN = TN / MI;   // MFMA blocks per wave
+    constexpr int KI = 512 / MI;                 // k per MFMA
+    constexpr int KS = BK / KI;                  // MFMA k sub-steps per K step
+    constexpr int NG = 64 / MI;                  // lane groups along k, 8 values each
+    constexpr int AE = MI * MI / 64;             // accumulators per lane and block
+    typedef float accT __attribute__((ext_vector_type(AE)));
     constexpr int A_ROWB = BK * 2;
     constexpr int B_ROWB = BN * 2;
     constexpr int A_BYTES = BM * A_ROWB;
@@ -571,7 +604,7 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     constexpr int A_ROWS_PER_LD = 1024 / A_ROWB; // tile rows one load instruction fills
     constexpr int B_ROWS_PER_LD = 1024 / B_ROWB;
     static_assert(BK == 32 || BK == 64, "A rows of 64 or 128 bytes");
-    static_assert(BN % 32 == 0 && B_ROWB <= 1024 && 1024 % B_ROWB == 0, "B layout");
+    static_assert(BN % 32 == 0 && B_ROWB >= 256 && B_ROWB <= 1024 && 1024 % B_ROWB == 0, "B layout");
     static_assert(A_LD * NW * 1024 == A_BYTES && B_LD * NW * 1024 == B_BYTES, "load split");
     static_assert(KS >= 2 && STAGES >= 2 && STAGES * STAGE <= 160 * 1024, "pipeline shape");
     static_assert((STAGES - 1) * LD < 64, "vmcnt range");
@@ -589,6 +622,12 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     const int64_t lda = p.lda, ldb = p.ldb;
     char *const smem = ops.lds();
 
+    // B rows keep n contiguous; the 32-byte chunks of row k are permuted by
+    // XOR with bswz(k), so that the transpose reads of one instruction (4
+    // consecutive rows per 16 lanes; with MI 16, rows 8 apart in the other
+    // 16 lanes of a half-wave) fall in distinct banks.
+    auto bswz = [](int k) { return MI == 32 ? (k & 3) << 1 : ((k & 3) << 1) | ((k >> 3) & 1); };
+
     // --- per-lane byte offsets of the direct loads (relative to the tile) ---
     uint32_t a_goff[A_LD], b_goff[B_LD];
     const int mmax = p.M - 1 - m0;               // last valid tile row
@@ -603,8 +642,8 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     for (int j = 0; j < B_LD; ++j) {
         const int k = (wave * B_LD + j) * B_ROWS_PER_LD + lane / (B_ROWB / 16);
         const int q = lane % (B_ROWB / 16);          // physical 16-byte chunk in the row
-        const int lb = (q >> 2) ^ (k & 3);           // logical 64-byte block
-        const int n = lb * 32 + (q & 3) * 8;
+        const int c = (q >> 1) ^ bswz(k);            // logical 32-byte chunk
+        const int n = c * 16 + (q & 1) * 8;
         b_goff[j] = (uint32_t)((k * ldb + min(n, nmax)) * 2);
     }
 
@@ -623,36 +662,37 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     };
 
     // --- fragment addressing ---
-    const int l32 = lane & 31;
-    const int g = lane >> 5;                      // k half of the MFMA operand
-    // A: row wm*TM + i*32 + l32, logical chunk 2*kk + g
-    const int a_x = g ^ aswz<A_ROWB>(l32);
-    const int a_lane = (wm * TM + l32) * A_ROWB;
-    // B: rows kk*16 + 8g + 4c + s/4, columns wn*TN + j*32 + 16h + 4(s%4)
+    const int lr = lane % MI;                     // A row / B column within an MFMA block
+    const int kg = lane / MI;                     // k group of the MFMA operand (8 values)
+    // A: row wm*TM + i*MI + lr, logical chunk (KI/8)*kk + kg
+    const int a_x = kg ^ aswz<A_ROWB>(lr);
+    const int a_lane = (wm * TM + lr) * A_ROWB;
+    // B: rows kk*KI + 8*kg + t4 (and 4 more), columns wn*TN + j*MI + 16*c16 + 4*(s16%4)
     const int s16 = lane & 15;
-    const int h = (lane >> 4) & 1;
+    const int c16 = lr >> 4;                      // 16-column half of a 32-column block
     const int t4 = s16 >> 2;                      // equals row & 3
-    const int b_lane = (8 * g + t4) * B_ROWB + 32 * h + 8 * (s16 & 3);
-    const int b_blk0 = wn * (TN / 32);
+    const int b_lane = (8 * kg + t4) * B_ROWB + 8 * (s16 & 3);
+    const int b_c0 = wn * (TN / 16) + c16;        // logical 32-byte chunk of block 0
+    const int b_sw = bswz(8 * kg + t4);           // the same for every kk and the 4 rows below
 
-    f32x16 acc[FM][FN];
+    accT acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
 #pragma unroll
-            for (int e = 0; e < 16; ++e)
+            for (int e = 0; e < AE; ++e)
                 acc[i][j][e] = 0.0f;
 
     u32x4 fa[2][FM], fb[2][FN];
 
     auto read_A = [&](int stage, int kk, int buf, int i) {
-        const char *sA = smem + stage * STAGE + a_lane + (((2 * kk) ^ a_x) << 4);
-        fa[buf][i] = ops.read16(sA + i * 32 * A_ROWB);
+        const char *sA = smem + stage * STAGE + a_lane + ((((KI / 8) * kk) ^ a_x) << 4);
+        fa[buf][i] = ops.read16(sA + i * MI * A_ROWB);
     };
     auto read_B = [&](int stage, int kk, int buf, int j) {
-        const char *pb = smem + stage * STAGE + A_BYTES + kk * 16 * B_ROWB + b_lane +
-                         (((b_blk0 + j) ^ t4) << 6);
+        const char *pb = smem + stage * STAGE + A_BYTES + kk * KI * B_ROWB + b_lane +
+                         (((b_c0 + j * (MI / 16)) ^ b_sw) << 5);
         const v4i16 lo = ops.read_tr8(pb);
         const v4i16 hi = ops.read_tr8(pb + 4 * B_ROWB);
         u32x4 v;
@@ -799,19 +839,20 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
         }
     }
 
-    // epilogue (same accumulator layout as gemm_kernel)
+    // epilogue: B is the MFMA's first operand, so lane l holds, for block
+    // (i, j), row lr and groups of 4 consecutive columns 4*kg + 4*NG*q
     const OutView ov = out_view<BM, BN>(p, ks, local, m0, n0);
     float *Cb = ov.base;
     const int64_t ldc = ov.ld;
     const bool vec_store = p.tile_major || (p.vec_c && (m0 + BM <= p.M) && (n0 + BN <= p.N));
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-        const int row = m0 + wm * TM + i * 32 + l32;
+        const int row = m0 + wm * TM + i * MI + lr;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int col = n0 + wn * TN + j * 32 + q * 8 + g * 4;
+            for (int q = 0; q < AE / 4; ++q) {
+                const int col = n0 + wn * TN + j * MI + q * 4 * NG + kg * 4;
                 f32x4 v;
                 v.x = acc[i][j][4 * q + 0];
                 v.y = acc[i][j][4 * q + 1];
@@ -830,13 +871,13 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     }
 }
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT>
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, int MI>
 __global__ void __launch_bounds__(WGM * WGN * 64, 1)
 gemm_kernel_dma(GemmParams p_in)
 {
     __shared__ __attribute__((aligned(1024))) char smem[dma_lds_bytes<BM, BN, BK, STAGES>()];
     const DeviceOps ops{smem};
-    dma_tile<BM, BN, BK, STAGES, WGM, WGN, DT>(ops, p_in, blockIdx.x, gridDim.x, threadIdx.x);
+    dma_tile<BM, BN, BK, STAGES, WGM, WGN, DT, MI>(ops, p_in, blockIdx.x, gridDim.x, threadIdx.x);
 }
 
 // C[i][j] = sum over p of W[p][i][j], p ascending (a fixed order, so the

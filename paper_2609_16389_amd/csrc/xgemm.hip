@@ -189,14 +189,14 @@ hipError_t launch_gemm(int dtype, const GemmParams &p, int grid, hipStream_t s)
     return hipGetLastError();
 }
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN>
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int MI>
 hipError_t launch_dma(int dtype, const GemmParams &p, int grid, hipStream_t s)
 {
     if (dtype == XGEMM_BF16)
-        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 0>), dim3(grid),
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 0, MI>), dim3(grid),
                            dim3(WGM * WGN * 64), 0, s, p);
     else
-        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 1>), dim3(grid),
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 1, MI>), dim3(grid),
                            dim3(WGM * WGN * 64), 0, s, p);
     return hipGetLastError();
 }
@@ -207,6 +207,16 @@ constexpr int kDmaStages256x256 = 2;  // 2 x 64 KiB
 constexpr int kDmaStages256x128 = 3;  // 3 x 48 KiB
 constexpr int kDmaStages128x128 = 2;  // 2 x 32 KiB, two workgroups per CU
 constexpr int kDmaMinStages = 3;
+// MFMA block of the pipelined kernels (32: 32x32x16, 16: 16x16x32)
+#ifndef XGEMM_MI_256x256
+#define XGEMM_MI_256x256 16
+#endif
+#ifndef XGEMM_MI_256x128
+#define XGEMM_MI_256x128 16
+#endif
+#ifndef XGEMM_MI_128x128
+#define XGEMM_MI_128x128 16
+#endif
 
 // The pipelined kernels need 16-byte aligned A and B with lda, ldb multiples
 // of 8, N a multiple of 8 (whole 16-byte chunks of B rows), K a multiple of
@@ -221,20 +231,21 @@ bool dma_eligible(const GemmParams &p, int bm)
 }
 
 // Template arguments of the pipelined kernel per tile (tile rows and
-// columns, K step, LDS stages, waves along M and N).  Launches and host
-// traces both take them from here, so a trace follows the kernel that runs.
-template <int BM_, int BN_, int STAGES_>
+// columns, K step, LDS stages, waves along M and N, MFMA block).  Launches
+// and host traces both take them from here, so a trace follows the kernel
+// that runs.
+template <int BM_, int BN_, int STAGES_, int MI_>
 struct DmaTile {
-    static constexpr int BM = BM_, BN = BN_, BK = kDmaBK, STAGES = STAGES_, WGM = 2, WGN = 2;
+    static constexpr int BM = BM_, BN = BN_, BK = kDmaBK, STAGES = STAGES_, WGM = 2, WGN = 2, MI = MI_;
 };
 
 template <class F>
 auto with_dma_tile(int tile, F &&f)
 {
     switch (tile) {
-    case XGEMM_TILE_256x256: return f(DmaTile<256, 256, kDmaStages256x256>{});
-    case XGEMM_TILE_256x128: return f(DmaTile<256, 128, kDmaStages256x128>{});
-    default: return f(DmaTile<128, 128, kDmaStages128x128>{});
+    case XGEMM_TILE_256x256: return f(DmaTile<256, 256, kDmaStages256x256, XGEMM_MI_256x256>{});
+    case XGEMM_TILE_256x128: return f(DmaTile<256, 128, kDmaStages256x128, XGEMM_MI_256x128>{});
+    default: return f(DmaTile<128, 128, kDmaStages128x128, XGEMM_MI_128x128>{});
     }
 }
 
@@ -262,7 +273,7 @@ hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int g
     if (dma)
         return with_dma_tile(tile, [&](auto t) {
             using T = decltype(t);
-            return launch_dma<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN>(dtype, p, grid, s);
+            return launch_dma<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, T::MI>(dtype, p, grid, s);
         });
     return with_general_tile(tile, [&](auto t) {
         using T = decltype(t);
@@ -759,6 +770,11 @@ struct TraceOps {
     {
         return c;
     }
+    template <int DT>
+    xgemm_dev::f32x4 mfma(xgemm_dev::u32x4, xgemm_dev::u32x4, xgemm_dev::f32x4 c) const
+    {
+        return c;
+    }
     template <int N>
     void wait_vm() const
     {
@@ -1028,8 +1044,8 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
             using T = decltype(t);
             return trace_threads(xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>(),
                                  [&](const TraceOps &ops, int tid) {
-                                     xgemm_dev::dma_tile<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, 0>(
-                                         ops, g.p, (int)block, (int)g.grid, tid);
+                                     xgemm_dev::dma_tile<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, 0,
+                                                         T::MI>(ops, g.p, (int)block, (int)g.grid, tid);
                                  });
         });
     return with_general_tile(plan.tile, [&](auto t) {
