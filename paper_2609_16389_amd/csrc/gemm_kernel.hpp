@@ -703,12 +703,12 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
         fb[buf][j] = v;
     };
     // The fragment reads of one sub-step as FM + FN units in the order the
-    // MFMAs below first need them: A0, B0 .. B(FN-1), A1 .. A(FM-1).
+    // MFMAs below first need them: A0, B0 .. B(FN-1), A1 .. A(FM-1).  Unit u
+    // is issued after MFMA u * SP of the sub-step before, so that the reads
+    // spread over the first half of its MFMAs (with 16 x 16 blocks, 16 units
+    // among 64 MFMAs: one every second MFMA).
     constexpr int NU = FM + FN;
-#ifndef XGEMM_READ_UNITS_PER_MFMA
-#define XGEMM_READ_UNITS_PER_MFMA 1
-#endif
-    constexpr int RPM = XGEMM_READ_UNITS_PER_MFMA;  // read units issued after each MFMA
+    constexpr int SP = (FM * FN / 2) / NU > 0 ? (FM * FN / 2) / NU : 1;
     auto read_unit = [&](int stage, int kk, int buf, int u) {
         if (u == 0)
             read_A(stage, kk, buf, 0);
@@ -762,17 +762,15 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     auto kstep = [&]<bool LOAD1, bool LOAD2, int WAIT>(int t) {
         const int stage = t % STAGES;
         const int prev = (t + STAGES - 1) % STAGES;
-        // sub-steps 0 .. KS-2: MFMAs of kk, each followed by one read unit of
-        // kk+1 (and, spread out, the second-half loads), in this order
+        // sub-steps 0 .. KS-2: MFMAs of kk, with the read units of kk+1 (and,
+        // spread out, the second-half loads) between them, in this order
 #pragma unroll
         for (int kk = 0; kk < KS - 1; ++kk) {
 #pragma unroll
             for (int n = 0; n < FM * FN; ++n) {
                 mfma_n(kk & 1, n);
-#pragma unroll
-                for (int q = 0; q < RPM; ++q)
-                    if (n * RPM + q < NU)
-                        read_unit(stage, kk + 1, (kk + 1) & 1, n * RPM + q);
+                if (n % SP == 0 && n / SP < NU)
+                    read_unit(stage, kk + 1, (kk + 1) & 1, n / SP);
                 if constexpr (LOAD2) {
                     const int gi = kk * FM * FN + n;
                     if (gi % STEP2 == 0 && gi / STEP2 < H2)
@@ -795,10 +793,8 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
         for (int n = 0; n < FM * FN; ++n) {
             mfma_n((KS - 1) & 1, n);
             if constexpr (WAIT >= 0) {
-#pragma unroll
-                for (int q = 0; q < RPM; ++q)
-                    if (n * RPM + q < NU)
-                        read_unit(next, 0, 0, n * RPM + q);
+                if (n % SP == 0 && n / SP < NU)
+                    read_unit(next, 0, 0, n / SP);
             }
             if constexpr (LOAD1) {
 #pragma unroll
