@@ -152,8 +152,10 @@ int xgemm_select_config(int64_t M, int64_t N, int64_t K, int dtype, int cu_count
 
 /*
  * Workgroup tile of a tile id: rows (bm), columns (bn), K step (bk) and
- * threads per workgroup.  Host-only.  XGEMM_ERR_INVALID_ARG for an unknown id
- * or a NULL output pointer.
+ * threads per workgroup of its pipelined kernel (the general kernel, taken
+ * for shapes or alignments the pipelined one does not cover, may use another
+ * count: xgemm_trace_plan reports the launched one).  Host-only.
+ * XGEMM_ERR_INVALID_ARG for an unknown id or a NULL output pointer.
  */
 int xgemm_tile_info(int tile, int *bm, int *bn, int *bk, int *threads);
 

@@ -592,6 +592,7 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     constexpr int KS = BK / KI;                  // MFMA k sub-steps per K step
     constexpr int NG = 64 / MI;                  // lane groups along k, 8 values each
     constexpr int AE = MI * MI / 64;             // accumulators per lane and block
+    constexpr bool INPLACE = NW == 8;            // the two-waves-per-SIMD schedule below
     typedef float accT __attribute__((ext_vector_type(AE)));
     constexpr int A_ROWB = BK * 2;
     constexpr int B_ROWB = BN * 2;
@@ -686,6 +687,24 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
 
     u32x4 fa[2][FM], fb[2][FN];
 
+    // A fragment of MFMA block row i and B fragment of block column j for
+    // sub-step kk of the K step held in LDS stage `stage`
+    auto frag_A = [&](int stage, int kk, int i) {
+        const char *sA = smem + stage * STAGE + a_lane + ((((KI / 8) * kk) ^ a_x) << 4);
+        return ops.read16(sA + i * MI * A_ROWB);
+    };
+    auto frag_B = [&](int stage, int kk, int j) {
+        const char *pb = smem + stage * STAGE + A_BYTES + kk * KI * B_ROWB + b_lane +
+                         (((b_c0 + j * (MI / 16)) ^ b_sw) << 5);
+        const v4i16 lo = ops.read_tr8(pb);
+        const v4i16 hi = ops.read_tr8(pb + 4 * B_ROWB);
+        u32x4 v;
+        v.x = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1));
+        v.y = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3));
+        v.z = __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 0, 1));
+        v.w = __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 2, 3));
+        return v;
+    };
     auto read_A = [&](int stage, int kk, int buf, int i) {
         const char *sA = smem + stage * STAGE + a_lane + ((((KI / 8) * kk) ^ a_x) << 4);
         fa[buf][i] = ops.read16(sA + i * MI * A_ROWB);
@@ -808,7 +827,97 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
         }
     };
 
-    if (nk >= STAGES) {
+    if constexpr (INPLACE) {
+        // Two waves per SIMD, 16 x 16 x 32 MFMAs, BK 64 (two sub-steps), two
+        // LDS stages.  The 128 accumulator registers of a wave then fit in
+        // ordinary VGPRs, where the MFMA issues every 16 cycles (with the
+        // accumulators in AGPRs it takes about 19).  To stay within the 256
+        // registers of a wave, the A fragments are single-buffered: block
+        // row i of the next sub-step is read into ga[i] as soon as row i of
+        // the current sub-step has issued its MFMAs.  B fragments are
+        // double-buffered.
+        // One row of sub-step 1 runs before the barrier: 0 rows exposed the
+        // last A read's latency (4.5% slower), 2 or more left fewer MFMAs
+        // to space the direct loads over (1-3% slower).
+        constexpr int R = 1;                      // rows of sub-step 1 issued before the barrier
+        static_assert(MI == 16 && STAGES == 2 && KS == 2 && FN <= FM - R, "in-place schedule shape");
+        constexpr int LSTEP = ((FM - R) * FN) / LD > 0 ? ((FM - R) * FN) / LD : 1;
+        static_assert(LSTEP * (LD - 1) < (FM - R) * FN, "load spacing");
+        u32x4 ga[FM], gb[2][FN];
+        auto row = [&](int b, int i) {
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                acc[i][j] = ops.template mfma<DT>(gb[b][j], ga[i], acc[i][j]);
+        };
+        // One K step t.  Sub-step 0 works from ga / gb[0] and reads sub-step
+        // 1 of the same stage (ga in place, gb[1]).  Before the barrier:
+        // the first R rows of sub-step 1 (registers only, which gives the
+        // last A read time to land), then the waits.  After it: the rest of
+        // sub-step 1 with the reads of step t+1's sub-step 0 (ga in place,
+        // gb[0]) and, if LOAD, the direct loads of step t+2 into the stage
+        // just freed.  WAIT < 0: t is the last step.
+        auto kstep_ip = [&]<bool LOAD, int WAIT>(int t) {
+            const int stage = t & 1, next = stage ^ 1;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                row(0, i);
+                ga[i] = frag_A(stage, 1, i);
+                if (i < FN)
+                    gb[1][i] = frag_B(stage, 1, i);
+                ops.fence();
+            }
+#pragma unroll
+            for (int i = 0; i < R; ++i) {
+                row(1, i);
+                ops.fence();
+            }
+            // stage t fully read by this wave; stage t+1 landed for this wave
+            ops.wait_lgkm0();
+            if constexpr (WAIT >= 0)
+                ops.template wait_vm<0>();
+            ops.barrier();
+            ops.fence();
+            if constexpr (WAIT >= 0) {
+#pragma unroll
+                for (int i = 0; i < R; ++i)
+                    ga[i] = frag_A(next, 0, i);
+            }
+#pragma unroll
+            for (int i = R; i < FM; ++i) {
+#pragma unroll
+                for (int j = 0; j < FN; ++j) {
+                    acc[i][j] = ops.template mfma<DT>(gb[1][j], ga[i], acc[i][j]);
+                    const int g = (i - R) * FN + j;
+                    if constexpr (LOAD) {
+                        if (g % LSTEP == 0 && g / LSTEP < LD)
+                            load_j(t + 2, stage, g / LSTEP);
+                    }
+                }
+                if constexpr (WAIT >= 0) {
+                    ga[i] = frag_A(next, 0, i);
+                    if (i - R < FN)
+                        gb[0][i - R] = frag_B(next, 0, i - R);
+                }
+                ops.fence();
+            }
+        };
+        if (nk >= 2) {
+            issue_loads(0, 0);
+            issue_loads(1, 1);
+            ops.template wait_vm<LD>();
+            ops.barrier();
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                ga[i] = frag_A(0, 0, i);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                gb[0][j] = frag_B(0, 0, j);
+            for (int t = 0; t < nk - 2; ++t)
+                kstep_ip.template operator()<true, 0>(t);
+            kstep_ip.template operator()<false, 0>(nk - 2);
+            kstep_ip.template operator()<false, -1>(nk - 1);
+        }
+    } else if (nk >= STAGES) {
         // prologue: fill every stage, wait for stage 0
 #pragma unroll
         for (int t = 0; t < STAGES; ++t)

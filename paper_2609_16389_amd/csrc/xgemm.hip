@@ -28,15 +28,16 @@ struct xgemm_ctx {
 namespace {
 
 struct TileShape {
-    int bm, bn, bk, threads, wg_per_cu;
+    int bm, bn, bk, wg_per_cu;
 };
 
 // Workgroups per CU follow from LDS use: two stages of (bm + bn) x bk
-// 16-bit values out of 160 KiB.
+// 16-bit values out of 160 KiB.  (Waves per workgroup are in the kernel
+// tables below: DmaTile, GeneralTile.)
 constexpr TileShape kTiles[XGEMM_TILE_COUNT] = {
-    {256, 256, 64, 256, 1},  // XGEMM_TILE_256x256: 4 waves of 128 x 128, 128 KiB LDS
-    {256, 128, 64, 256, 1},  // XGEMM_TILE_256x128: 4 waves of 128 x 64,   96 KiB LDS
-    {128, 128, 64, 256, 2},  // XGEMM_TILE_128x128: 4 waves of 64 x 64,    64 KiB LDS
+    {256, 256, 64, 1},  // XGEMM_TILE_256x256: 128 KiB LDS
+    {256, 128, 64, 1},  // XGEMM_TILE_256x128:  96 KiB LDS
+    {128, 128, 64, 2},  // XGEMM_TILE_128x128:  64 KiB LDS
 };
 
 constexpr int64_t kMaxDim = (int64_t)1 << 31;
@@ -217,6 +218,13 @@ constexpr int kDmaMinStages = 3;
 #ifndef XGEMM_MI_128x128
 #define XGEMM_MI_128x128 16
 #endif
+// Waves along M and N of the 256 x 256 pipelined tile: 8 waves (two per
+// SIMD) of 128 x 64 keep their accumulators in VGPRs, where 16 x 16 x 32
+// MFMAs issue every 16 cycles instead of about 19 from AGPRs.
+#ifndef XGEMM_WGM_256x256
+#define XGEMM_WGM_256x256 2
+#define XGEMM_WGN_256x256 4
+#endif
 
 // The pipelined kernels need 16-byte aligned A and B with lda, ldb multiples
 // of 8, N a multiple of 8 (whole 16-byte chunks of B rows), K a multiple of
@@ -234,16 +242,16 @@ bool dma_eligible(const GemmParams &p, int bm)
 // columns, K step, LDS stages, waves along M and N, MFMA block).  Launches
 // and host traces both take them from here, so a trace follows the kernel
 // that runs.
-template <int BM_, int BN_, int STAGES_, int MI_>
+template <int BM_, int BN_, int STAGES_, int MI_, int WGM_ = 2, int WGN_ = 2>
 struct DmaTile {
-    static constexpr int BM = BM_, BN = BN_, BK = kDmaBK, STAGES = STAGES_, WGM = 2, WGN = 2, MI = MI_;
+    static constexpr int BM = BM_, BN = BN_, BK = kDmaBK, STAGES = STAGES_, WGM = WGM_, WGN = WGN_, MI = MI_;
 };
 
 template <class F>
 auto with_dma_tile(int tile, F &&f)
 {
     switch (tile) {
-    case XGEMM_TILE_256x256: return f(DmaTile<256, 256, kDmaStages256x256, XGEMM_MI_256x256>{});
+    case XGEMM_TILE_256x256: return f(DmaTile<256, 256, kDmaStages256x256, XGEMM_MI_256x256, XGEMM_WGM_256x256, XGEMM_WGN_256x256>{});
     case XGEMM_TILE_256x128: return f(DmaTile<256, 128, kDmaStages256x128, XGEMM_MI_256x128>{});
     default: return f(DmaTile<128, 128, kDmaStages128x128, XGEMM_MI_128x128>{});
     }
@@ -264,6 +272,14 @@ auto with_general_tile(int tile, F &&f)
     case XGEMM_TILE_256x128: return f(GeneralTile<256, 128>{});
     default: return f(GeneralTile<128, 128>{});
     }
+}
+
+// Threads per workgroup of a tile's pipelined (dma) or general kernel.
+int tile_threads(int tile, bool dma)
+{
+    if (dma)
+        return with_dma_tile(tile, [](auto t) { return decltype(t)::WGM * decltype(t)::WGN * 64; });
+    return with_general_tile(tile, [](auto t) { return decltype(t)::WGM * decltype(t)::WGN * 64; });
 }
 
 hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int grid, hipStream_t s)
@@ -945,7 +961,7 @@ int xgemm_tile_info(int tile, int *bm, int *bn, int *bk, int *threads)
     *bm = kTiles[tile].bm;
     *bn = kTiles[tile].bn;
     *bk = kTiles[tile].bk;
-    *threads = kTiles[tile].threads;
+    *threads = tile_threads(tile, true);
     return XGEMM_OK;
 }
 
@@ -989,7 +1005,7 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
     info->segments = plan.nseg;
     info->family = g.dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
     info->reduce = g.reduce;
-    info->threads = kTiles[plan.tile].threads;
+    info->threads = tile_threads(plan.tile, g.dma);
     info->lds_bytes = g.dma ? with_dma_tile(plan.tile, [](auto t) {
         using T = decltype(t);
         return xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>();
@@ -1023,7 +1039,7 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
             return XGEMM_ERR_INVALID_ARG;
         g.p.C = W;
     }
-    const int threads = kTiles[plan.tile].threads;
+    const int threads = tile_threads(plan.tile, g.dma);
     // run `body(ops, tid)` for every thread, collecting each one's events
     auto trace_threads = [&](size_t lds_bytes, auto &&body) {
         std::vector<char> lds(lds_bytes);

@@ -389,8 +389,13 @@ class LaunchReport:
 
 
 def trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, threads, capacity=None):
-    """(events [threads, capacity], counts [threads]) of one workgroup."""
+    """(events [threads, capacity], counts [threads]) of one workgroup.
+    `threads` must be the launch's thread count (xgemm_trace_plan's
+    info.threads): the library writes that many counts."""
     import ctypes
+    info = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, seg)
+    if threads != info.threads:
+        raise ValueError("trace_workgroup: the launch has %d threads per workgroup, not %d" % (info.threads, threads))
     counts = np.zeros(threads, dtype=np.int64)
     cptr = counts.ctypes.data_as(ctypes.c_void_p)
     args = (M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, BASE_W, ctypes.byref(cfg), cu_count, seg, block)

@@ -219,8 +219,12 @@ TRACE_EVENT_DTYPE = [("op", "<i4"), ("arg", "<i4"), ("lds", "<i8"), ("addr", "<i
 def xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, cfg, cu_count, segment, block, threads,
                           capacity=None):
     """Events of every thread of one workgroup: a list of `threads` numpy
-    record arrays (fields op, arg, lds, addr).  Raises XgemmError."""
+    record arrays (fields op, arg, lds, addr).  `threads` must be the
+    launch's thread count (xgemm_trace_plan's info.threads), since the
+    library writes that many counts.  Raises XgemmError."""
     import numpy as np
+    if threads != xgemm_trace_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, cu_count, segment).threads:
+        raise XgemmError(XGEMM_ERR_INVALID_ARG, "threads is not the launch's thread count")
     counts = np.zeros(threads, dtype=np.int64)
     cptr = counts.ctypes.data_as(ctypes.c_void_p)
     if capacity is None:

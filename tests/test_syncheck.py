@@ -260,7 +260,10 @@ def test_general_kernel_traces_are_race_free(shape, c, lds):
 def test_general_kernel_trace_structure():
     """General kernel, n K steps: one barrier after the first tile store and
     one per K step; each K step's tiles written to LDS once."""
-    ev, counts = sc.trace_workgroup(256, 256, 5 * 64 + 1, 5 * 64 + 1, 256, 256, cfg(0), 256, 0, 0, 256)
+    info = xg.xgemm_trace_plan(256, 256, 5 * 64 + 1, sc.BASE_A, 5 * 64 + 1, sc.BASE_B, 256, sc.BASE_C, 256, cfg(0),
+                               256, 0)
+    assert info.family == xg.XGEMM_KERNEL_GENERAL
+    ev, counts = sc.trace_workgroup(256, 256, 5 * 64 + 1, 5 * 64 + 1, 256, 256, cfg(0), 256, 0, 0, info.threads)
     waves = sc.wave_streams(ev, counts)
     nk = 6
     for ws in waves:
@@ -275,10 +278,12 @@ def test_general_kernel_trace_structure():
     ("no LDS wait", lambda op: op != sc.WAIT_LGKM),
 ])
 def test_general_kernel_planted_mistakes(name, keep):
-    ev, counts = sc.trace_workgroup(256, 256, 320, 320, 256, 256, cfg(0), 256, 0, 0, 256)
+    # K = 321 is not a multiple of the K step, so the general kernel runs
+    info = xg.xgemm_trace_plan(256, 256, 321, sc.BASE_A, 321, sc.BASE_B, 256, sc.BASE_C, 256, cfg(0), 256, 0)
+    assert info.family == xg.XGEMM_KERNEL_GENERAL
+    ev, counts = sc.trace_workgroup(256, 256, 321, 321, 256, 256, cfg(0), 256, 0, 0, info.threads)
     waves = sc.wave_streams(ev, counts)
-    lds = xg.xgemm_trace_plan(256, 256, 320, sc.BASE_A, 320, sc.BASE_B, 256, sc.BASE_C, 256, cfg(0), 256,
-                              0).lds_bytes
+    lds = info.lds_bytes
     assert sc.check_workgroup_lds(waves, lds) == []
     mutated = [edit(ws, keep=keep) for ws in waves]
     assert sc.check_workgroup_lds(mutated, lds), name
