@@ -436,18 +436,22 @@ __host__ __device__ __forceinline__ void general_tile(const Ops &ops, const Gemm
 //      ds_read_b64_tr_b16 -- within each group of 16 lanes, lane i receives
 //      element (i % 4) of the 8 bytes addressed by lane 4e + i / 4 as its
 //      element e, which turns a 4 (k) x 16 (n) block into the k-packed
-//      MFMA operand; 64-byte block b of row k is stored at block
-//      b ^ (k & 3) so the four rows of one read fall in different banks.
+//      MFMA operand; 32-byte chunk c of row k is stored at chunk
+//      c ^ bswz(k) so the rows one read instruction touches fall in
+//      different banks.
 // M and N edges: rows and columns beyond the matrix are clamped to the last
 // valid one (they only feed outputs that are never stored).
 //
-// Schedule of K step t (fragment buffers alternate between K sub-steps):
+// Schedule of K step t with one wave per SIMD (fragment buffers alternate
+// between K sub-steps):
 //   read fragments of the last sub-step of t         (LDS stage t)
 //   MFMAs of the other sub-steps of t
 //   wait: own fragment reads done, own loads of stage t+1 landed; barrier
 //   issue direct loads of step t+STAGES into stage t (now free)
 //   read fragments of sub-step 0 of t+1               (LDS stage t+1)
 //   MFMAs of the last sub-step of t
+// With eight waves (two per SIMD) the same order holds, with A fragments
+// read in place row by row (see kstep_ip below).
 // ---------------------------------------------------------------------------
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -577,9 +581,10 @@ constexpr int dma_lds_bytes()
 //
 // MI is the MFMA block: 32 (v_mfma_f32_32x32x16, 16 k per instruction) or
 // 16 (v_mfma_f32_16x16x32, 32 k per instruction).  Both do the same work per
-// K step from the same LDS bytes; under the power cap the 16 x 16 shape
-// runs the GPU at a higher clock (it moves half as many accumulator
-// registers per flop).
+// K step from the same LDS bytes.  On random data the GPU is power-capped;
+// there the 16 x 16 shape sustains more flops (measured 1864 against 1753
+// TFLOP/s MFMA-only with accumulators in AGPRs, about 2050 with them in
+// VGPRs, where it issues every 16 cycles instead of about 19).
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, int MI, class Ops>
 __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmParams &p_in, int block, int nblocks,
                                                   int tid)
