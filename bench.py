@@ -396,7 +396,10 @@ def main():
     traffic = stored_traffic(w.name)
     counters = stored_counters(w.name)
     out = {
-        "metric": METRIC,
+        # the headline metric for the 8192^3 workload; the same quantity,
+        # named for its shape, for the others
+        "metric": METRIC if w.name == "gemm8192_bf16" else
+        "GEMM TFLOP/s and %% of MI355X dense MFMA peak (%s, %dx%dx%d) on 1 GPU" % (w.dtype, w.M, w.N, w.K),
         "value": round(value, 2),
         "unit": "TFLOP/s",
         "n_gpus": 1,
