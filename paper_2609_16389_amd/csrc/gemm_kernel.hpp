@@ -556,6 +556,12 @@ struct DeviceOps {
     __device__ __forceinline__ u32x4 gload16(const uint16_t *q) const { return *(const u32x4 *)q; }
     __device__ __forceinline__ uint16_t gload2(const uint16_t *q) const { return *q; }
     __device__ __forceinline__ void lds_write16(char *q, u32x4 v) const { *(u32x4 *)q = v; }
+    // lane-masked: only lanes with `on` write
+    __device__ __forceinline__ void lds_write16(char *q, u32x4 v, bool on) const
+    {
+        if (on)
+            *(u32x4 *)q = v;
+    }
     __device__ __forceinline__ void sync() const { __syncthreads(); }
 };
 
@@ -620,7 +626,15 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = ks * p.k_chunk;
     const int kend = min(p.K, kbeg + p.k_chunk);
-    const int nk = kend > kbeg ? (kend - kbeg) / BK : 0;
+    // A K range that is not a whole number of steps (K a multiple of 8, so
+    // every 16-byte chunk is wholly inside or outside it) ends in a partial
+    // step of tk values.  It runs first, as step 0: its loads read clamped,
+    // valid addresses, and the prologue zeroes the LDS chunks of A and rows
+    // of B beyond K before any fragment read.  Full steps follow from kbeg.
+    const int klen = kend > kbeg ? kend - kbeg : 0;
+    const int tk = klen % BK;
+    const int nk = klen / BK + (tk > 0 ? 1 : 0);
+    auto step_k0 = [&](int u) { return tk > 0 ? (u == 0 ? kend - tk : kbeg + (u - 1) * BK) : kbeg + u * BK; };
 
     const int lane = tid & 63;
     const int wave = ops.uniform(tid >> 6);
@@ -654,17 +668,47 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     }
 
     auto issue_loads = [&](int kstep, int stage) {
-        const int k0 = kbeg + kstep * BK;
+        const int k0 = step_k0(kstep);
         const uint16_t *Ab = p.A + (int64_t)m0 * lda + k0;
         const uint16_t *Bb = p.B + (int64_t)k0 * ldb + n0;
         const uint32_t sA = ops.lds_addr(smem) + stage * STAGE;
         const uint32_t sB = sA + A_BYTES;
+        const bool partial = tk > 0 && kstep == 0;
 #pragma unroll
-        for (int j = 0; j < A_LD; ++j)
-            ops.load16(Ab, a_goff[j], sA + (wave * A_LD + j) * 1024);
+        for (int j = 0; j < A_LD; ++j) {
+            // a chunk beyond K reads the row's first chunk instead
+            const int r = (wave * A_LD + j) * A_ROWS_PER_LD + lane / (A_ROWB / 16);
+            const int c = (lane % (A_ROWB / 16)) ^ aswz<A_ROWB>(r);
+            const uint32_t off = partial && c * 8 >= tk ? a_goff[j] - (uint32_t)(c * 16) : a_goff[j];
+            ops.load16(Ab, off, sA + (wave * A_LD + j) * 1024);
+        }
 #pragma unroll
-        for (int j = 0; j < B_LD; ++j)
-            ops.load16(Bb, b_goff[j], sB + (wave * B_LD + j) * 1024);
+        for (int j = 0; j < B_LD; ++j) {
+            // a row beyond K reads row tk - 1 instead
+            const int k = (wave * B_LD + j) * B_ROWS_PER_LD + lane / (B_ROWB / 16);
+            const uint32_t off =
+                partial && k >= tk ? b_goff[j] - (uint32_t)((int64_t)(k - tk + 1) * ldb * 2) : b_goff[j];
+            ops.load16(Bb, off, sB + (wave * B_LD + j) * 1024);
+        }
+    };
+    // After the partial step has landed in stage 0 (and a barrier): zero the
+    // A chunks and B rows beyond K, then a barrier before the fragment reads.
+    auto zero_partial = [&]() {
+        if (tk > 0) {
+            constexpr int NT = NW * 64;
+            const u32x4 z = {0u, 0u, 0u, 0u};
+            static_assert((BM * (BK / 8)) % NT == 0 && (BK * (B_ROWB / 16)) % NT == 0, "whole passes");
+#pragma unroll
+            for (int idx = tid; idx < BM * (BK / 8); idx += NT) {
+                const int r = idx / (BK / 8), c = idx % (BK / 8);
+                ops.lds_write16(smem + r * A_ROWB + ((c ^ aswz<A_ROWB>(r)) << 4), z, c * 8 >= tk);
+            }
+#pragma unroll
+            for (int idx = tid; idx < BK * (B_ROWB / 16); idx += NT)
+                ops.lds_write16(smem + A_BYTES + idx * 16, z, idx / (B_ROWB / 16) >= tk);
+            ops.wait_lgkm0();
+            ops.barrier();
+        }
     };
 
     // --- fragment addressing ---
@@ -754,7 +798,7 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
 
     // Direct load j (0 .. LD-1) of K step u into LDS stage `stage`.
     auto load_j = [&](int u, int stage, int j) {
-        const int k0 = kbeg + u * BK;
+        const int k0 = step_k0(u);
         const uint32_t sA = ops.lds_addr(smem) + stage * STAGE;
         if (j < A_LD) {
             const uint16_t *Ab = p.A + (int64_t)m0 * lda + k0;
@@ -911,6 +955,7 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
             issue_loads(1, 1);
             ops.template wait_vm<LD>();
             ops.barrier();
+            zero_partial();
 #pragma unroll
             for (int i = 0; i < FM; ++i)
                 ga[i] = frag_A(0, 0, i);
@@ -929,6 +974,7 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
             issue_loads(t, t);
         ops.template wait_vm<(STAGES - 1) * LD>();
         ops.barrier();
+        zero_partial();
         read_frags(0, 0, 0);
         if (nk > STAGES) {
             // step 0: the prologue issued all of step STAGES-1's loads

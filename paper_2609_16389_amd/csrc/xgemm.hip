@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <new>
 #include <type_traits>
 #include <vector>
@@ -81,7 +82,10 @@ double model_cost(int64_t M, int64_t N, int64_t K, int cu_count, int tile, int s
     const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
     const int64_t waves = cdiv(tiles * split, slots);
     // one CU retires 4096 flops per cycle at peak; a workgroup shares its CU
-    const double wg_cycles = 2.0 * t.bm * t.bn * (double)kc * t.wg_per_cu / 4096.0 / kTileEff[tile];
+    // with the others resident there, which are fewer than wg_per_cu when
+    // the launch does not fill every CU that many times
+    const int64_t share = std::min<int64_t>(t.wg_per_cu, cdiv(tiles * split, cu_count));
+    const double wg_cycles = 2.0 * t.bm * t.bn * (double)kc * (double)share / 4096.0 / kTileEff[tile];
     double cost = (double)waves * wg_cycles;
     if (split > 1) {
         // partials written once and read once, C written once, plus a launch
@@ -227,14 +231,15 @@ constexpr int kDmaMinStages = 3;
 #endif
 
 // The pipelined kernels need 16-byte aligned A and B with lda, ldb multiples
-// of 8, N a multiple of 8 (whole 16-byte chunks of B rows), K a multiple of
-// their K step, at least as many K steps in every split as the deepest
-// pipeline has stages, and per-tile byte offsets that fit in 32 bits.
+// of 8, N and K multiples of 8 (whole 16-byte chunks of B rows and of A rows
+// within K; a last partial K step is zero-filled), at least as many K steps
+// (counting a partial one) in every split as the deepest pipeline has
+// stages, and per-tile byte offsets that fit in 32 bits.
 bool dma_eligible(const GemmParams &p, int bm)
 {
     const int64_t last = (int64_t)p.K - (int64_t)(p.split - 1) * p.k_chunk;
-    const int64_t min_steps = (p.k_chunk < last ? p.k_chunk : last) / kDmaBK;
-    return p.vec_ab && p.N % 8 == 0 && p.K % kDmaBK == 0 && min_steps >= kDmaMinStages &&
+    const int64_t min_steps = cdiv(p.k_chunk < last ? p.k_chunk : last, kDmaBK);
+    return p.vec_ab && p.N % 8 == 0 && p.K % 8 == 0 && min_steps >= kDmaMinStages &&
            (int64_t)bm * p.lda * 2 < ((int64_t)1 << 32) && (int64_t)kDmaBK * p.ldb * 2 < ((int64_t)1 << 32);
 }
 
@@ -812,6 +817,10 @@ struct TraceOps {
         return 0;
     }
     void lds_write16(char *q, xgemm_dev::u32x4) const { push(XGEMM_TRACE_LDS_WRITE, 16, q - base, 0); }
+    void lds_write16(char *q, xgemm_dev::u32x4, bool on) const
+    {
+        push(XGEMM_TRACE_LDS_WRITE, 16, on ? (int64_t)(q - base) : -1, 0);
+    }
     // __syncthreads: the compiler emits s_waitcnt lgkmcnt(0) and s_barrier
     void sync() const
     {

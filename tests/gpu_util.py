@@ -12,23 +12,26 @@ TORCH_DT = {"bf16": torch.bfloat16, "fp16": torch.float16}
 CODE = {"bf16": xg.XGEMM_BF16, "fp16": xg.XGEMM_FP16}
 
 
-def to_device(bits: np.ndarray, dtype: str, ld: int | None = None, offset: int = 0) -> torch.Tensor:
+def to_device(bits: np.ndarray, dtype: str, ld: int | None = None, offset: int = 0,
+              pad: int | None = None) -> torch.Tensor:
     """uint16 bit patterns (rows x cols) -> a device tensor view with row stride
-    ``ld`` (>= cols; padding filled with a large value that must never be read)
-    starting ``offset`` elements into its allocation."""
+    ``ld`` (>= cols; padding filled with ``pad``, by default a large value,
+    that must never be read) starting ``offset`` elements into its
+    allocation."""
     rows, cols = bits.shape
     ld = max(cols, 1) if ld is None else ld
-    buf = np.full(offset + rows * ld + 1, 0x7BFF if dtype == "fp16" else 0x7F7F, dtype=np.uint16)
+    pad = (0x7BFF if dtype == "fp16" else 0x7F7F) if pad is None else pad
+    buf = np.full(offset + rows * ld + 1, pad, dtype=np.uint16)
     if rows and cols:
         buf[offset:offset + rows * ld].reshape(rows, ld)[:, :cols] = bits
     t = torch.from_numpy(buf.view(np.int16)).to("cuda").view(TORCH_DT[dtype])
     return t.as_strided((rows, cols), (ld, 1), offset)
 
 
-def run_gpu(A_bits, B_bits, dtype, config=None, out=None, lda=None, ldb=None, offset=0):
+def run_gpu(A_bits, B_bits, dtype, config=None, out=None, lda=None, ldb=None, offset=0, pad=None):
     """C = A*B on the GPU through xgemm_run / xgemm_run_config; returns fp32 numpy."""
-    A = to_device(A_bits, dtype, lda, offset)
-    B = to_device(B_bits, dtype, ldb, offset)
+    A = to_device(A_bits, dtype, lda, offset, pad)
+    B = to_device(B_bits, dtype, ldb, offset, pad)
     C = xg.gemm(A, B, out=out, config=config)
     torch.cuda.synchronize()
     return C.cpu().numpy()

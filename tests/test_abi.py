@@ -123,9 +123,12 @@ def test_kernel_family_rules():
     assert fam(8192, 8192, 8192) == P
     assert fam(1000, 1000, 1024) == P          # ragged M and N, N % 8 == 0
     assert fam(1000, 1001, 1024) == G          # N % 8 != 0
-    assert fam(1000, 1000, 1000) == G          # K % 64 != 0
+    assert fam(1000, 1000, 1000) == P          # K % 64 != 0 but K % 8 == 0: a partial last step
+    assert fam(1000, 1000, 1056) == P          # the same
+    assert fam(1000, 1000, 1004, lda=1008) == G  # K % 8 != 0
     assert fam(1000, 1000, 128) == G           # fewer than 3 K steps of 64
-    assert fam(1000, 1000, 1056) == G          # K % 64 != 0
+    assert fam(1000, 1000, 136) == P           # 2 full steps and a partial one
+    assert fam(1000, 1000, 120) == G           # 1 full step and a partial one
     assert fam(1000, 1000, 1024, a=al + 2) == G  # misaligned A
     assert fam(1000, 1000, 1024, lda=1028) == G  # lda % 8 != 0
     assert fam(1000, 1000, 1024, ldb=1004) == G  # ldb % 8 != 0

@@ -85,6 +85,51 @@ def test_pipelined_shapes(tile, shape):
                     "pipelined tile %d %s %s" % (tile, dtype, shape))
 
 
+# K a multiple of 8 but not of the K step: the pipelined kernels run the
+# partial last step first and zero the LDS beyond K
+PARTIAL_SHAPES = [(256, 256, 200), (1000, 1000, 1000), (300, 264, 3000), (777, 136, 4104)]
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("shape", PARTIAL_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_partial_k_step(tile, shape):
+    M, N, K = shape
+    assert _family(M, N, K, config(tile)) == xg.XGEMM_KERNEL_PIPELINED
+    for dtype in ("bf16", "fp16"):
+        A, B, C_ref, S = _case(M, N, K, dtype, seed=K + tile)
+        check_close(run_gpu(A, B, dtype, config=config(tile)), C_ref, S,
+                    "partial step tile %d %s %s" % (tile, dtype, shape))
+
+
+@pytest.mark.parametrize("tile", TILES)
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_partial_k_step_never_reads_past_k(tile, dtype):
+    """A's row padding past K holds NaN: any read of it would poison C."""
+    M, N, K = 384, 320, 1000
+    A, B, C_ref, S = _case(M, N, K, dtype, seed=31 + tile)
+    nan = 0x7E00 if dtype == "fp16" else 0x7FC0
+    C = run_gpu(A, B, dtype, config=config(tile), lda=K + 24, ldb=N + 8, pad=nan)
+    check_close(C, C_ref, S, "NaN padding past K, tile %d" % tile)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_partial_k_step_integer_bit_exact(dtype):
+    M, N, K = 520, 264, 2056
+    A, B = wl.make_int_inputs(M, N, K, dtype, seed=32)
+    assert _family(M, N, K, config(0)) == xg.XGEMM_KERNEL_PIPELINED
+    C_ref, _ = oracle.gemm(A, B, dtype)
+    check_exact(run_gpu(A, B, dtype), C_ref, "integer, partial step")
+
+
+@pytest.mark.parametrize("tile,split", [(0, 3), (1, 8), (2, 4)])
+def test_partial_k_step_in_last_split(tile, split):
+    M, N, K = 384, 320, 8200
+    assert _family(M, N, K, config(tile, split)) == xg.XGEMM_KERNEL_PIPELINED
+    A, B, C_ref, S = _case(M, N, K, "bf16", seed=33 + split)
+    check_close(run_gpu(A, B, "bf16", config=config(tile, split)), C_ref, S,
+                "partial last split tile %d split %d" % (tile, split))
+
+
 @pytest.mark.parametrize("split", [1, 2, 4, 8, 16])
 @pytest.mark.parametrize("tile", TILES)
 def test_pipelined_split_k(split, tile):

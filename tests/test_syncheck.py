@@ -353,6 +353,58 @@ def test_read_hoisted_above_its_barrier_is_caught(tile):
     assert {v.kind for v in sc.check_workgroup_lds(out, lds)} & {"raw", "war"}
 
 
+# ---------------------------------------------------------------------------
+# a partial last K step (K a multiple of 8, not of the K step)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("tile", [0, 1, 2])
+@pytest.mark.parametrize("shape", [(256, 256, 3 * 64 + 8), (300, 264, 4 * 64 + 56), (520, 136, 2 * 64 + 32)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_partial_k_step_traces_are_race_free(tile, shape):
+    """The partial step runs first; its clamped loads stay inside A and B,
+    the zero fill of the LDS beyond K is ordered before every fragment read,
+    and the output is still covered once."""
+    M, N, K = shape
+    assert xg.xgemm_kernel_family(M, N, K, 1 << 20, K, 1 << 20, N, cfg(tile)) == xg.XGEMM_KERNEL_PIPELINED
+    rep = sc.check_launch(M, N, K, cfg(tile))
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+@pytest.mark.parametrize("tile", [0, 1])
+def test_partial_k_step_with_split_k(tile):
+    # K = 1224 in 3 splits: 448, 448 and a last one of 328 (5 full steps and 8)
+    rep = sc.check_launch(384, 256, 1224, cfg(tile, 3))
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+def partial_waves(tile):
+    bm, bn, bk, _ = xg.xgemm_tile_info(tile)
+    K = 4 * bk + 24
+    info = xg.xgemm_trace_plan(bm, bn, K, sc.BASE_A, K, sc.BASE_B, bn, sc.BASE_C, bn, cfg(tile), 256, 0)
+    ev, counts = sc.trace_workgroup(bm, bn, K, K, bn, bn, cfg(tile), 256, 0, 0, info.threads)
+    return sc.wave_streams(ev, counts), info.lds_bytes
+
+
+@pytest.mark.parametrize("tile", [0, 1])
+def test_partial_k_step_zero_fill_is_traced(tile):
+    waves, lds = partial_waves(tile)
+    assert sc.check_workgroup_lds(waves, lds) == []
+    for ws in waves:
+        # the zero fill: LDS writes between the first barrier and the second
+        b0, b1 = nth(ws.op, sc.BARRIER, 0), nth(ws.op, sc.BARRIER, 1)
+        assert (ws.op[b0:b1] == sc.LDS_WRITE).sum() > 0
+        assert (ws.op[b1:] == sc.LDS_WRITE).sum() == 0
+
+
+@pytest.mark.parametrize("tile", [0, 1])
+def test_partial_k_step_missing_barrier_is_caught(tile):
+    """Without the barrier after the zero fill, a wave could read fragments
+    before another wave has zeroed them."""
+    waves, lds = partial_waves(tile)
+    mutated = [edit(ws, keep=lambda op: np.arange(len(op)) != nth(op, sc.BARRIER, 1)) for ws in waves]
+    assert {v.kind for v in sc.check_workgroup_lds(mutated, lds)} & {"raw", "war", "waw"}
+
+
 def test_duplicate_workgroup_output_is_caught(monkeypatch):
     real = sc.trace_workgroup
     monkeypatch.setattr(sc, "trace_workgroup",
