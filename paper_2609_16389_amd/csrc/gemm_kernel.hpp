@@ -698,12 +698,10 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
             constexpr int NT = NW * 64;
             const u32x4 z = {0u, 0u, 0u, 0u};
             static_assert((BM * (BK / 8)) % NT == 0 && (BK * (B_ROWB / 16)) % NT == 0, "whole passes");
-#pragma unroll
             for (int idx = tid; idx < BM * (BK / 8); idx += NT) {
                 const int r = idx / (BK / 8), c = idx % (BK / 8);
                 ops.lds_write16(smem + r * A_ROWB + ((c ^ aswz<A_ROWB>(r)) << 4), z, c * 8 >= tk);
             }
-#pragma unroll
             for (int idx = tid; idx < BK * (B_ROWB / 16); idx += NT)
                 ops.lds_write16(smem + A_BYTES + idx * 16, z, idx / (B_ROWB / 16) >= tk);
             ops.wait_lgkm0();
