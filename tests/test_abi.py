@@ -183,3 +183,18 @@ def test_gemv_null_handle_and_trace_arguments():
     assert tr(4, 4096, 16, 4096, 16, 16, None, ctypes.byref(split), 0, None, 0, counts) == xg.XGEMM_ERR_INVALID_ARG
     assert tr(4, 4096, 16, 4096, 16, 16, 32, ctypes.byref(split), 3, None, 0, counts) == xg.XGEMM_OK
     assert tr(4, 4096, 16, 4096, 16, 16, 32, ctypes.byref(split), 4, None, 0, counts) == xg.XGEMM_ERR_INVALID_ARG
+
+
+def test_sweep_candidates_host_logic():
+    """The selector sweep (a GPU tool) enumerates configurations on the host:
+    the selector's choice is always timed, splits shorter than 3 K steps and
+    launches above the workgroup cap are left out."""
+    from paper_2609_16389_amd import sweep
+    c = sweep.candidates(1024, 1024, 65536, (1, 8))
+    assert (1, 8) in c and (0, 1) in c and (2, 16) in c and len(c) == len(set(c))
+    small = sweep.candidates(256, 256, 256, (2, 1))
+    assert all(s == 1 for _, s in small)          # K = 256: every split would be under 3 steps
+    big = sweep.candidates(16384, 16384, 4096, (0, 1))
+    for t, s in big:
+        bm, bn, _, _ = xg.xgemm_tile_info(t)
+        assert (16384 // bm) * (16384 // bn) * s <= sweep.MAX_WORKGROUPS or (t, s) == (0, 1)
