@@ -101,11 +101,17 @@ int xgemm_destroy(xgemm_handle_t h);
  *                A or B
  *   dtype        XGEMM_BF16 or XGEMM_FP16 (applies to A and B)
  * A pointer may be NULL only when its matrix has no elements.  Aligned fast
- * path: A, B, C 16-byte aligned, lda and ldb multiples of 8, ldc a multiple of
- * 4; any other alignment is still correct, through a slower element-wise
- * path.  Sizes are limited to M, N, K < 2^31 with every matrix addressable in
- * 64-bit element offsets.  A handle holds one workspace: calls that share a
- * handle must be ordered on one stream.
+ * path: A, B 16-byte aligned, lda, ldb, K and N multiples of 8 (C: 16-byte
+ * aligned with ldc a multiple of 4 for vector stores).  Any other layout is
+ * still correct: above M * N * K = 2^26 the operands that miss these
+ * conditions are first copied, zero-padded, into the handle's workspace
+ * (M x K rounded up to 8 for A, K x N both rounded up to 8 for B; both when K
+ * is not a multiple of 8), below it a slower element-wise kernel reads them
+ * in place.  Sizes are limited to M, N, K < 2^31 with every matrix
+ * addressable in 64-bit element offsets.  A handle holds one workspace
+ * (split-k partials and operand copies), grown on demand with hipMalloc
+ * (XGEMM_ERR_ALLOC if that fails): calls that share a handle must be ordered
+ * on one stream.
  */
 int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
               const void *A, int64_t lda, const void *B, int64_t ldb,
@@ -238,6 +244,11 @@ typedef struct xgemm_trace_info {
     int64_t workspace_bytes; /* bytes of W the whole plan writes */
     int32_t tile_base;       /* the launch covers logical tiles [tile_base, tile_base + tile_count) */
     int32_t tile_count;
+    int32_t packed;          /* bit 0: A, bit 1: B is read from a copy in W (see xgemm_run) */
+    int32_t k;               /* K as the GEMM kernel sees it (K rounded up to 8 when packed) */
+    int64_t lda, ldb;        /* leading dimensions the kernel reads A and B with */
+    int64_t a_offset;        /* byte offset of the packed A (M x k, leading dimension lda) in W, or -1 */
+    int64_t b_offset;        /* byte offset of the packed B (k x ldb) in W, or -1 */
 } xgemm_trace_info;
 
 /*
@@ -257,7 +268,8 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
  * counts[t] (counts has `threads` entries, the caller owns both arrays).  A
  * count above capacity means the trace was cut; call again with a larger
  * capacity (capacity 0 with out == NULL only counts).  W is the workspace
- * address for launches that write partials (reduce != 0), else unused.
+ * address for launches that write partials (reduce != 0) or read packed
+ * operands (packed != 0), else unused.
  * Both kernel families are traced.  XGEMM_ERR_INVALID_ARG as
  * xgemm_trace_plan, or for a block out of range, counts == NULL, or W ==
  * NULL where it is needed.

@@ -15,6 +15,7 @@
 #include "xgemm.h"
 #include "gemm_kernel.hpp"
 #include "gemv_kernel.hpp"
+#include "pack_kernel.hpp"
 
 using xgemm_dev::GemmParams;
 
@@ -239,14 +240,15 @@ constexpr int kDmaMinStages = 3;
 
 // The pipelined kernels need 16-byte aligned A and B with lda, ldb multiples
 // of 8, N and K multiples of 8 (whole 16-byte chunks of B rows and of A rows
-// within K; a last partial K step is zero-filled), at least as many K steps
-// (counting a partial one) in every split as the deepest pipeline has
-// stages, and per-tile byte offsets that fit in 32 bits.
-bool dma_eligible(const GemmParams &p, int bm)
+// within K; a last partial K step is zero-filled; N may be ragged when B's
+// rows are padded to a multiple of 8 columns, as packed copies are), at
+// least as many K steps (counting a partial one) in every split as the
+// deepest pipeline has stages, and per-tile byte offsets that fit in 32 bits.
+bool dma_eligible(const GemmParams &p, int bm, bool b_padded = false)
 {
     const int64_t last = (int64_t)p.K - (int64_t)(p.split - 1) * p.k_chunk;
     const int64_t min_steps = cdiv(p.k_chunk < last ? p.k_chunk : last, kDmaBK);
-    return p.vec_ab && p.N % 8 == 0 && p.K % 8 == 0 && min_steps >= kDmaMinStages &&
+    return p.vec_ab && (p.N % 8 == 0 || b_padded) && p.K % 8 == 0 && min_steps >= kDmaMinStages &&
            (int64_t)bm * p.lda * 2 < ((int64_t)1 << 32) && (int64_t)kDmaBK * p.ldb * 2 < ((int64_t)1 << 32);
 }
 
@@ -360,13 +362,28 @@ struct Segment {
     int reduce;  // 0: writes C; 1: full-matrix partials + splitk_reduce; 2: tile partials + tile reduce
 };
 
+// Operands copied into the workspace (pack16) so that the pipelined kernels
+// can run: A as M x k8 (leading dimension k8), B as k8 x n8 (leading
+// dimension n8), with k8 and n8 the K and N rounded up to multiples of 8 and
+// zero padding.  Offsets are bytes from the workspace base.
+struct Pack {
+    bool a = false, b = false;
+    int64_t k8 = 0, n8 = 0;
+    size_t a_off = 0, b_off = 0;
+};
+
+// Copy work below which the general kernel runs unaligned operands directly
+// (multiply-adds: M * N * K).
+constexpr double kPackMinWork = 64.0 * 1024 * 1024;
+
 // Everything about a call that follows from the arguments on the host.
 struct Plan {
     int tile;
     Segment seg[2];
     int nseg;
-    size_t ws;      // workspace bytes
+    size_t ws;      // workspace bytes (split partials, then packed operands)
     int64_t ldw;    // full-matrix workspace row stride (floats)
+    Pack pack;
 };
 
 // K range per split with trailing empty splits dropped; returns the split.
@@ -382,29 +399,62 @@ int trim_split(int64_t K, int split, int bk, int64_t *kc)
 
 // Plan a call for K > 0 and M, N > 0 with configuration cfg on a device
 // with cu_count CUs.  Device pointers are only inspected for alignment.
+int make_plan_with(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+                   const float *C, int64_t ldc, const xgemm_config &cfg, int cu_count, Pack pk, Plan *out);
+
+// With allow_pack, operands the pipelined kernels cannot read in place are
+// copied into the workspace when the call is large enough and the copies
+// make the pipelined kernel eligible (the packed operands' addresses in the
+// plan are then byte offsets from the workspace base, rebased at launch).
 int make_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
-              const float *C, int64_t ldc, const xgemm_config &cfg, int cu_count, Plan *out)
+              const float *C, int64_t ldc, const xgemm_config &cfg, int cu_count, Plan *out, bool allow_pack)
+{
+    const int rc = make_plan_with(M, N, K, A, lda, B, ldb, C, ldc, cfg, cu_count, Pack{}, out);
+    if (rc != XGEMM_OK || !allow_pack || out->seg[0].dma || (double)M * (double)N * (double)K < kPackMinWork)
+        return rc;
+    Pack pk;
+    pk.k8 = cdiv(K, 8) * 8;
+    pk.n8 = cdiv(N, 8) * 8;
+    const bool k_ok = K % 8 == 0;
+    pk.a = !(k_ok && (uintptr_t)A % 16 == 0 && lda % 8 == 0);
+    pk.b = !(k_ok && (uintptr_t)B % 16 == 0 && ldb % 8 == 0 && N % 8 == 0);
+    if (!pk.a && !pk.b)
+        return rc;  // aligned operands: the general kernel runs for another reason
+    Plan packed;
+    const int rc2 = make_plan_with(M, N, K, A, lda, B, ldb, C, ldc, cfg, cu_count, pk, &packed);
+    if (rc2 == XGEMM_OK && packed.seg[0].dma)
+        *out = packed;
+    return XGEMM_OK;
+}
+
+int make_plan_with(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+                   const float *C, int64_t ldc, const xgemm_config &cfg, int cu_count, Pack pk, Plan *out)
 {
     const TileShape &t = kTiles[cfg.tile];
     const int64_t tiles_m = cdiv(M, t.bm), tiles_n = cdiv(N, t.bn);
     const int64_t tiles = tiles_m * tiles_n;
+    if (pk.a || pk.b)
+        K = pk.k8;  // zero-padded K (both operands are packed when K % 8 != 0)
     int64_t kc;
     const int split = trim_split(K, cfg.split_k, t.bk, &kc);
     if (tiles * split > 0x7fffffff || tiles * 8 > 0x7fffffff)
         return XGEMM_ERR_INVALID_ARG;
 
     GemmParams base;
-    base.A = (const uint16_t *)A;
-    base.B = (const uint16_t *)B;
-    base.lda = lda;
-    base.ldb = ldb;
+    // a packed operand's address is its byte offset in the (256-byte aligned)
+    // workspace, set below once the split partials' bytes are known
+    base.A = pk.a ? nullptr : (const uint16_t *)A;
+    base.B = pk.b ? nullptr : (const uint16_t *)B;
+    base.lda = pk.a ? pk.k8 : lda;
+    base.ldb = pk.b ? pk.n8 : ldb;
     base.M = (int)M;
     base.N = (int)N;
     base.K = (int)K;
     base.tiles_m = (int)tiles_m;
     base.tiles_n = (int)tiles_n;
     base.group_m = cfg.group_m;
-    base.vec_ab = ((uintptr_t)A % 16 == 0) && ((uintptr_t)B % 16 == 0) && (lda % 8 == 0) && (ldb % 8 == 0);
+    base.vec_ab = ((uintptr_t)base.A % 16 == 0) && ((uintptr_t)base.B % 16 == 0) && (base.lda % 8 == 0) &&
+                  (base.ldb % 8 == 0);
     base.tile_base = 0;
     base.tile_major = 0;
     base.batch = 1;
@@ -413,6 +463,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const
     out->ldw = cdiv(N, 4) * 4;
     out->ws = 0;
     out->nseg = 0;
+    out->pack = pk;
 
     auto add = [&](int64_t first, int64_t count, int sp, int64_t kchunk, int reduce) {
         Segment &g = out->seg[out->nseg++];
@@ -435,13 +486,30 @@ int make_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const
             g.p.tile_major = reduce == 2;
         }
         g.grid = count * sp;
-        g.dma = dma_eligible(g.p, t.bm);
+        g.dma = dma_eligible(g.p, t.bm, pk.b);
     };
 
+    // packed operands follow the split partials in the workspace
+    auto finish = [&]() {
+        if (pk.a || pk.b) {
+            pk.a_off = (out->ws + 255) / 256 * 256;
+            const size_t a_bytes = pk.a ? (size_t)M * (size_t)pk.k8 * 2 : 0;
+            pk.b_off = (pk.a_off + a_bytes + 255) / 256 * 256;
+            out->ws = pk.b ? pk.b_off + (size_t)pk.k8 * (size_t)pk.n8 * 2 : pk.a_off + a_bytes;
+            for (int i = 0; i < out->nseg; ++i) {
+                if (pk.a)
+                    out->seg[i].p.A = (const uint16_t *)(uintptr_t)pk.a_off;
+                if (pk.b)
+                    out->seg[i].p.B = (const uint16_t *)(uintptr_t)pk.b_off;
+            }
+            out->pack = pk;
+        }
+        return (int)XGEMM_OK;
+    };
     if (split > 1) {
         add(0, tiles, split, kc, 1);
         out->ws = workspace_bytes(M, N, split);
-        return XGEMM_OK;
+        return finish();
     }
     const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
     int64_t kct = 0;
@@ -454,7 +522,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const
     } else {
         add(0, tiles, 1, kc, 0);
     }
-    return XGEMM_OK;
+    return finish();
 }
 
 // Grow the handle's workspace to `bytes` (never shrinks).  The old one may
@@ -517,7 +585,7 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     else
         select_config(M, N, K, h->cu_count, &cfg);
     Plan plan;
-    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan);
+    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan, true);
     if (rc != XGEMM_OK)
         return rc;
 
@@ -525,9 +593,33 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     if (rc != XGEMM_OK)
         return rc;
 
+    // operand copies for the pipelined kernels
+    char *const ws = (char *)h->workspace;
+    const Pack &pk = plan.pack;
+    auto pack = [&](const void *src, int64_t ld, int64_t src_rows, int64_t src_cols, size_t off, int64_t rows,
+                    int64_t cols) {
+        const int64_t items = rows * cdiv(cols, xgemm_dev::kPackSeg);  // (row, segment) pairs
+        const int grid = (int)(items < 8192 ? items : 8192);
+        hipLaunchKernelGGL(xgemm_dev::pack16, dim3(grid), dim3(256), 0, s, (const uint16_t *)src, ld, (int)src_rows,
+                           (int)src_cols, (uint16_t *)(ws + off), (int64_t)cols, (int)rows, (int)(cols / 8));
+        return hipGetLastError();
+    };
+    if (pk.a && (e = pack(A, lda, M, K, pk.a_off, M, pk.k8)) != hipSuccess) {
+        set_error(h, "pack A launch", e);
+        return XGEMM_ERR_HIP;
+    }
+    if (pk.b && (e = pack(B, ldb, K, N, pk.b_off, pk.k8, pk.n8)) != hipSuccess) {
+        set_error(h, "pack B launch", e);
+        return XGEMM_ERR_HIP;
+    }
+
     const int vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
     for (int i = 0; i < plan.nseg; ++i) {
         Segment &g = plan.seg[i];
+        if (pk.a)
+            g.p.A = (const uint16_t *)(ws + pk.a_off);
+        if (pk.b)
+            g.p.B = (const uint16_t *)(ws + pk.b_off);
         if (g.reduce)
             g.p.C = (float *)h->workspace;
         e = launch_tile(plan.tile, g.dma, dtype, g.p, (int)g.grid, s);
@@ -590,7 +682,7 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
     xgemm_config cfg;
     select_config_batched(batch, M, N, K, h->cu_count, &cfg);
     Plan plan;
-    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan);
+    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan, false);
     if (rc != XGEMM_OK)
         return rc;
     Segment &g = plan.seg[0];
@@ -886,7 +978,7 @@ int trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, cons
     if (!valid_config(cfg) || cu_count < 1 || M <= 0 || N <= 0 || K <= 0 || M >= kMaxDim || N >= kMaxDim ||
         K >= kMaxDim || lda < K || ldb < N || ldc < N || !A || !B || !C)
         return XGEMM_ERR_INVALID_ARG;
-    const int rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, *cfg, cu_count, plan);
+    const int rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, *cfg, cu_count, plan, true);
     if (rc != XGEMM_OK)
         return rc;
     if (segment < 0 || segment >= plan->nseg)
@@ -989,7 +1081,7 @@ int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t 
         return -1;
     Plan plan;
     // C's alignment does not affect the choice; the tail split needs a CU count
-    if (make_plan(M, N, K, A, lda, B, ldb, nullptr, N, *cfg, 256, &plan) != XGEMM_OK)
+    if (make_plan(M, N, K, A, lda, B, ldb, nullptr, N, *cfg, 256, &plan, true) != XGEMM_OK)
         return -1;
     return plan.seg[0].dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
 }
@@ -1002,7 +1094,7 @@ size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, cons
     if (M == 0 || N == 0 || K == 0)
         return 0;
     Plan plan;
-    if (make_plan(M, N, K, nullptr, K, nullptr, N, nullptr, N, *cfg, cu_count, &plan) != XGEMM_OK)
+    if (make_plan(M, N, K, nullptr, K, nullptr, N, nullptr, N, *cfg, cu_count, &plan, true) != XGEMM_OK)
         return 0;
     return plan.ws;
 }
@@ -1034,6 +1126,13 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
     info->workspace_bytes = (int64_t)plan.ws;
     info->tile_base = g.p.tile_base;
     info->tile_count = g.p.tile_count;
+    const Pack &pk = plan.pack;
+    info->packed = (pk.a ? 1 : 0) | (pk.b ? 2 : 0);
+    info->k = g.p.K;
+    info->lda = g.p.lda;
+    info->ldb = g.p.ldb;
+    info->a_offset = pk.a ? (int64_t)pk.a_off : -1;
+    info->b_offset = pk.b ? (int64_t)pk.b_off : -1;
     return XGEMM_OK;
 }
 
@@ -1050,10 +1149,16 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
     Segment &g = plan.seg[segment];
     if (block < 0 || block >= g.grid)
         return XGEMM_ERR_INVALID_ARG;
-    if (g.reduce) {
+    const Pack &pk = plan.pack;
+    if (g.reduce || pk.a || pk.b) {
         if (!W)
             return XGEMM_ERR_INVALID_ARG;
-        g.p.C = W;
+        if (g.reduce)
+            g.p.C = W;
+        if (pk.a)
+            g.p.A = (const uint16_t *)((char *)W + pk.a_off);
+        if (pk.b)
+            g.p.B = (const uint16_t *)((char *)W + pk.b_off);
     }
     const int threads = tile_threads(plan.tile, g.dma);
     // run `body(ops, tid)` for every thread, collecting each one's events

@@ -479,9 +479,19 @@ def check_launch(M, N, K, cfg, cu_count=256, lda=None, ldb=None, ldc=None, max_b
     n_events = 0
     n_blocks = 0
     bm, bn, _, _ = xg.xgemm_tile_info(cfg.tile)
-    a_lo, a_hi = BASE_A, BASE_A + 2 * ((M - 1) * lda + K)
-    b_lo, b_hi = BASE_B, BASE_B + 2 * ((K - 1) * ldb + N)
     info0 = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, 0)
+    # the operands as the kernels read them: the caller's A and B, or their
+    # zero-padded copies in the workspace (M x k and k x ldb)
+    if info0.packed & 1:
+        a_lo = BASE_W + info0.a_offset
+        a_hi = a_lo + 2 * ((M - 1) * info0.lda + info0.k)
+    else:
+        a_lo, a_hi = BASE_A, BASE_A + 2 * ((M - 1) * lda + K)
+    if info0.packed & 2:
+        b_lo = BASE_W + info0.b_offset
+        b_hi = b_lo + 2 * info0.k * info0.ldb
+    else:
+        b_lo, b_hi = BASE_B, BASE_B + 2 * ((K - 1) * ldb + N)
     c_cov = None
     for seg in range(info0.segments):
         info = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, seg)
@@ -494,13 +504,13 @@ def check_launch(M, N, K, cfg, cu_count=256, lda=None, ldb=None, ldc=None, max_b
             n_blocks += 1
             n_events += int(counts.sum())
             valid = np.arange(ev.shape[1])[None, :] < counts[:, None]
-            # global reads of the direct loads
-            ld = valid & (ev["op"] == LDS_LOAD)
+            # global reads: direct (to LDS) and register loads
+            ld = valid & ((ev["op"] == LDS_LOAD) | (ev["op"] == LOAD))
             ga = ev["addr"][ld]
             nb = ev["arg"][ld]
             inside = ((ga >= a_lo) & (ga + nb <= a_hi)) | ((ga >= b_lo) & (ga + nb <= b_hi))
             if not inside.all():
-                violations.append(Violation("global_bounds", -1, -1, "launch %d workgroup %d: direct load "
+                violations.append(Violation("global_bounds", -1, -1, "launch %d workgroup %d: load "
                                             "reads outside A and B at address %#x" %
                                             (seg, block, int(ga[~inside][0]))))
             # global stores

@@ -72,7 +72,9 @@ class xgemm_trace_info(ctypes.Structure):
     _fields_ = [("segments", ctypes.c_int32), ("family", ctypes.c_int32), ("reduce", ctypes.c_int32),
                 ("threads", ctypes.c_int32), ("lds_bytes", ctypes.c_int32), ("split", ctypes.c_int32),
                 ("grid", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
-                ("tile_base", ctypes.c_int32), ("tile_count", ctypes.c_int32)]
+                ("tile_base", ctypes.c_int32), ("tile_count", ctypes.c_int32),
+                ("packed", ctypes.c_int32), ("k", ctypes.c_int32), ("lda", ctypes.c_int64), ("ldb", ctypes.c_int64),
+                ("a_offset", ctypes.c_int64), ("b_offset", ctypes.c_int64)]
 
 
 class XgemmError(RuntimeError):

@@ -122,16 +122,19 @@ def test_kernel_family_rules():
     P, G = xg.XGEMM_KERNEL_PIPELINED, xg.XGEMM_KERNEL_GENERAL
     assert fam(8192, 8192, 8192) == P
     assert fam(1000, 1000, 1024) == P          # ragged M and N, N % 8 == 0
-    assert fam(1000, 1001, 1024) == G          # N % 8 != 0
     assert fam(1000, 1000, 1000) == P          # K % 64 != 0 but K % 8 == 0: a partial last step
     assert fam(1000, 1000, 1056) == P          # the same
-    assert fam(1000, 1000, 1004, lda=1008) == G  # K % 8 != 0
     assert fam(1000, 1000, 128) == G           # fewer than 3 K steps of 64
     assert fam(1000, 1000, 136) == P           # 2 full steps and a partial one
     assert fam(1000, 1000, 120) == G           # 1 full step and a partial one
-    assert fam(1000, 1000, 1024, a=al + 2) == G  # misaligned A
-    assert fam(1000, 1000, 1024, lda=1028) == G  # lda % 8 != 0
-    assert fam(1000, 1000, 1024, ldb=1004) == G  # ldb % 8 != 0
+    # operands the pipelined kernels cannot read in place: below 2^26
+    # multiply-adds the general kernel reads them; above, they are copied
+    small, large = (300, 301, 304), (1000, 1001, 1024)
+    assert fam(*small) == G and fam(*large) == P                  # N % 8 != 0
+    assert fam(300, 304, 301, lda=304) == G and fam(1000, 1000, 1004, lda=1008) == P  # K % 8 != 0
+    assert fam(300, 304, 304, a=al + 2) == G and fam(1000, 1000, 1024, a=al + 2) == P  # misaligned A
+    assert fam(300, 304, 304, lda=308) == G and fam(1000, 1000, 1024, lda=1028) == P  # lda % 8 != 0
+    assert fam(300, 304, 304, ldb=308) == G and fam(1000, 1000, 1024, ldb=1004) == P  # ldb % 8 != 0
     cfg16 = xg.xgemm_config(tile=0, split_k=16, group_m=4, tail_split=0)
     assert fam(1024, 1024, 65536, c=cfg16) == P
     assert fam(1024, 1024, 1024, c=cfg16) == G   # 64-element splits are too short
@@ -198,3 +201,27 @@ def test_sweep_candidates_host_logic():
     for t, s in big:
         bm, bn, _, _ = xg.xgemm_tile_info(t)
         assert (16384 // bm) * (16384 // bn) * s <= sweep.MAX_WORKGROUPS or (t, s) == (0, 1)
+
+
+def test_packed_plan_layout():
+    """Packed operands sit after the split partials in the workspace, 256-byte
+    aligned, with K and N rounded up to 8 and the kernel reading them with
+    those leading dimensions."""
+    cfg = xg.xgemm_config(tile=0, split_k=2, group_m=4, tail_split=0)
+    M, N, K = 1000, 1001, 2003
+    info = xg.xgemm_trace_plan(M, N, K, 1 << 20, K, 1 << 21, N, 1 << 22, N, cfg, 256, 0)
+    assert info.family == xg.XGEMM_KERNEL_PIPELINED and info.packed == 3   # K % 8 != 0: both
+    assert info.k == 2008 and info.lda == 2008 and info.ldb == 1008
+    split_bytes = 2 * M * 1004 * 4                     # two partials of M x ceil4(N) floats
+    assert info.a_offset == (split_bytes + 255) // 256 * 256
+    assert info.b_offset == (info.a_offset + M * 2008 * 2 + 255) // 256 * 256
+    assert info.workspace_bytes == info.b_offset + 2008 * 1008 * 2
+    assert xg.xgemm_workspace_bytes(M, N, K, 256, cfg) == info.workspace_bytes
+    # only B misses the layout: A is read in place
+    info = xg.xgemm_trace_plan(M, N, 2000, 1 << 20, 2000, 1 << 21, N, 1 << 22, N,
+                               xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0), 256, 0)
+    assert info.packed == 2 and info.a_offset == -1 and info.lda == 2000 and info.ldb == 1008
+    # aligned operands: nothing packed
+    info = xg.xgemm_trace_plan(1024, 1024, 1024, 1 << 20, 1024, 1 << 21, 1024, 1 << 22, 1024,
+                               xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0), 256, 0)
+    assert info.packed == 0 and info.a_offset == -1 and info.b_offset == -1 and info.workspace_bytes == 0

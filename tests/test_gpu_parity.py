@@ -130,6 +130,56 @@ def test_partial_k_step_in_last_split(tile, split):
                 "partial last split tile %d split %d" % (tile, split))
 
 
+# Layouts the pipelined kernels cannot read in place, above 2^26 multiply-adds:
+# the library copies the operand(s) into its workspace, zero-padded
+PACKED_CASES = {
+    "n_odd": ((1000, 1001, 1024), {}),
+    "k_odd": ((1000, 1000, 1003), {}),
+    "lda_not_x8": ((1024, 1000, 1024), {"lda": 1028}),
+    "ldb_not_x8": ((1000, 1024, 1024), {"ldb": 1027}),
+    "misaligned_pointers": ((1000, 1000, 1024), {"offset": 1}),
+    "everything_odd": ((1023, 1021, 1019), {"lda": 1022, "ldb": 1024}),
+}
+
+
+@pytest.mark.parametrize("name", sorted(PACKED_CASES))
+@pytest.mark.parametrize("dtype", ["bf16", "fp16"])
+def test_packed_operands(name, dtype):
+    (M, N, K), kw = PACKED_CASES[name]
+    lda, ldb, off = kw.get("lda", K), kw.get("ldb", N), kw.get("offset", 0)
+    base = (1 << 20) + 2 * off
+    assert xg.xgemm_kernel_family(M, N, K, base, lda, base, ldb, xg.xgemm_select_config(M, N, K, CODE[dtype], 256)) \
+        == xg.XGEMM_KERNEL_PIPELINED
+    A, B, C_ref, S = _case(M, N, K, dtype, seed=M + N + K)
+    nan = 0x7E00 if dtype == "fp16" else 0x7FC0
+    check_close(run_gpu(A, B, dtype, lda=lda, ldb=ldb, offset=off, pad=nan), C_ref, S,
+                "packed %s %s" % (name, dtype))
+
+
+@pytest.mark.parametrize("tile,split", [(0, 2), (1, 3), (2, 4)])
+def test_packed_operands_split_k(tile, split):
+    M, N, K = 520, 601, 1533
+    A, B, C_ref, S = _case(M, N, K, "bf16", seed=41 + split)
+    check_close(run_gpu(A, B, "bf16", config=config(tile, split), lda=K + 3), C_ref, S,
+                "packed split tile %d split %d" % (tile, split))
+
+
+def test_packed_operands_integer_bit_exact():
+    M = N = K = 2047
+    A, B = wl.make_int_inputs(M, N, K, "bf16", seed=42)
+    C_ref, _ = oracle.gemm(A, B, "bf16")
+    check_exact(run_gpu(A, B, "bf16"), C_ref, "integer, packed 2047^3")
+
+
+def test_packed_then_aligned_calls_share_a_handle():
+    """A packed call grows the workspace; aligned calls after it (and another
+    packed call with a smaller shape) still see their own operands."""
+    cases = [(1000, 1001, 1024, 1), (512, 512, 512, 2), (700, 703, 705, 3)]
+    for M, N, K, seed in cases:
+        A, B, C_ref, S = _case(M, N, K, "fp16", seed=seed)
+        check_close(run_gpu(A, B, "fp16"), C_ref, S, "sequence %dx%dx%d" % (M, N, K))
+
+
 @pytest.mark.parametrize("split", [1, 2, 4, 8, 16])
 @pytest.mark.parametrize("tile", TILES)
 def test_pipelined_split_k(split, tile):
@@ -179,7 +229,10 @@ def test_tail_split(tail_split, shape):
     M, N, K = shape  # 9 x 31 = 279 tiles of 256 x 256: a tail of 23
     A, B, C_ref, S = _case(M, N, K, "bf16", seed=tail_split)
     cfg = config(xg.XGEMM_TILE_256x256, 1, 4, tail_split)
-    assert xg.xgemm_workspace_bytes(M, N, K, 256, cfg) == 23 * tail_split * 256 * 256 * 4
+    partials = 23 * tail_split * 256 * 256 * 4
+    # N % 8 != 0 (2300 x 7930): B is also copied, padded to 8 columns, after the partials
+    packed_b = 0 if N % 8 == 0 else (partials + 255) // 256 * 256 - partials + K * ((N + 7) // 8 * 8) * 2
+    assert xg.xgemm_workspace_bytes(M, N, K, 256, cfg) == partials + packed_b
     check_close(run_gpu(A, B, "bf16", config=cfg), C_ref, S, "tail split %d %s" % (tail_split, shape))
 
 

@@ -405,6 +405,48 @@ def test_partial_k_step_missing_barrier_is_caught(tile):
     assert {v.kind for v in sc.check_workgroup_lds(mutated, lds)} & {"raw", "war", "waw"}
 
 
+# ---------------------------------------------------------------------------
+# operands packed into the workspace (unaligned layouts above 2^26 MACs)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("shape,lds,tile,split", [
+    ((1000, 1001, 1024), {}, 0, 1),                      # N % 8 != 0: B packed
+    ((1000, 1000, 1003), {"lda": 1003, "ldb": 1000}, 0, 1),   # K % 8 != 0: both packed
+    ((520, 600, 1536), {"lda": 1540}, 1, 2),             # lda % 8 != 0 with split-k: A packed
+    ((1030, 512, 1290), {"ldb": 516}, 2, 1),             # ldb % 8 != 0, partial K step: B packed
+], ids=["n_odd", "k_odd", "lda_split", "ldb_partial"])
+def test_packed_operand_traces(shape, lds, tile, split):
+    """The pipelined kernel reads the packed copies (inside the workspace)
+    and never the caller's arrays; the checker takes their bounds from the
+    plan.  Large shapes: the first workgroups of each launch are traced."""
+    M, N, K = shape
+    c = cfg(tile, split)
+    info = xg.xgemm_trace_plan(M, N, K, sc.BASE_A, lds.get("lda", K), sc.BASE_B, lds.get("ldb", N), sc.BASE_C, N,
+                               c, 256, 0)
+    assert info.family == xg.XGEMM_KERNEL_PIPELINED and info.packed != 0
+    rep = sc.check_launch(M, N, K, c, max_blocks=3, **lds)
+    assert rep.ok, [str(v) for v in rep.violations]
+
+
+def test_packed_operand_bounds_are_enforced(monkeypatch):
+    """A load of the caller's B where the plan reads a packed copy is flagged."""
+    real = sc.trace_workgroup
+
+    def to_caller_b(*args, **kw):
+        ev, counts = real(*args, **kw)
+        ev = ev.copy()
+        moved = (ev["op"] == sc.LDS_LOAD) & (ev["addr"] >= sc.BASE_W)
+        ev["addr"] = np.where(moved, sc.BASE_B, ev["addr"])
+        return ev, counts
+    monkeypatch.setattr(sc, "trace_workgroup", to_caller_b)
+    # B is packed (N % 8 != 0) and A read in place, so the caller's B is not
+    # an operand of the kernel at all
+    info = xg.xgemm_trace_plan(1000, 1001, 1024, sc.BASE_A, 1024, sc.BASE_B, 1001, sc.BASE_C, 1001, cfg(0), 256, 0)
+    assert info.packed == 2
+    rep = sc.check_launch(1000, 1001, 1024, cfg(0), max_blocks=1)
+    assert "global_bounds" in {v.kind for v in rep.violations}
+
+
 def test_duplicate_workgroup_output_is_caught(monkeypatch):
     real = sc.trace_workgroup
     monkeypatch.setattr(sc, "trace_workgroup",
