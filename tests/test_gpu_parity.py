@@ -532,3 +532,33 @@ def test_strided_batched_arguments():
     assert bad == xg.XGEMM_ERR_INVALID_ARG
     torch.cuda.synchronize()
     assert torch.all(C == 0)
+
+
+# ---------------------------------------------------------------------------
+# seeded random layouts: shapes, padding, offsets and forced configurations
+# ---------------------------------------------------------------------------
+
+def _random_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for _ in range(n):
+        big = rng.random() < 0.4   # above the copy threshold (2^26 multiply-adds) in part
+        hi = 900 if big else 300
+        M, N, K = (int(v) for v in rng.integers(1, hi, size=3))
+        lda = K + int(rng.choice([0, 0, 1, 3, 8]))
+        ldb = N + int(rng.choice([0, 0, 1, 5, 8]))
+        ldc = N + int(rng.choice([0, 0, 1, 4]))
+        off = int(rng.choice([0, 0, 0, 1]))
+        cfg = None if rng.random() < 0.5 else config(int(rng.integers(0, 3)), int(rng.choice([1, 1, 2, 4])))
+        cases.append((M, N, K, lda, ldb, ldc, off, cfg, str(rng.choice(["bf16", "fp16"]))))
+    return cases
+
+
+@pytest.mark.parametrize("case", _random_cases(40, 2024), ids=lambda c: "%dx%dx%d" % c[:3])
+def test_random_layouts(case):
+    M, N, K, lda, ldb, ldc, off, cfg, dtype = case
+    A, B, C_ref, S = _case(M, N, K, dtype, seed=M * 7 + N * 3 + K)
+    out = empty_out(M, N, ldc=ldc, offset=off)
+    C = run_gpu(A, B, dtype, config=cfg, out=out, lda=lda, ldb=ldb, offset=off, pad=0x7FC0 if dtype == "bf16"
+                else 0x7E00)
+    check_close(C, C_ref, S, "random %s" % (case,))

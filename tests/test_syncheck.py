@@ -558,3 +558,16 @@ def test_gemv_duplicate_rows_are_caught(monkeypatch):
                         real(M, K, lda, cfg, 0, capacity))
     rep = sc.check_gemv_launch(64, 256, xg.xgemv_config(4, 2))
     assert "coverage" in {v.kind for v in rep.violations}
+
+
+def test_random_small_plans_are_race_free():
+    """Seeded random shapes, leading dimensions and configurations, every
+    workgroup of every launch traced."""
+    rng = np.random.default_rng(7)
+    for _ in range(12):
+        M, N = (int(v) for v in rng.integers(1, 400, size=2))
+        K = int(rng.integers(1, 600))
+        lda, ldb = K + int(rng.choice([0, 3, 8])), N + int(rng.choice([0, 5, 8]))
+        c = cfg(int(rng.integers(0, 3)), int(rng.choice([1, 2, 4])))
+        rep = sc.check_launch(M, N, K, c, lda=lda, ldb=ldb)
+        assert rep.ok, ((M, N, K, lda, ldb, c.tile, c.split_k), [str(v) for v in rep.violations][:3])
