@@ -103,11 +103,11 @@ int xgemm_destroy(xgemm_handle_t h);
  * A pointer may be NULL only when its matrix has no elements.  Aligned fast
  * path: A, B 16-byte aligned, lda, ldb, K and N multiples of 8 (C: 16-byte
  * aligned with ldc a multiple of 4 for vector stores).  Any other layout is
- * still correct: above M * N * K = 2^26 the operands that miss these
- * conditions are first copied, zero-padded, into the handle's workspace
- * (M x K rounded up to 8 for A, K x N both rounded up to 8 for B; both when K
- * is not a multiple of 8), below it a slower element-wise kernel reads them
- * in place.  Sizes are limited to M, N, K < 2^31 with every matrix
+ * still correct: the operands that miss these conditions are first copied,
+ * zero-padded, into the handle's workspace (M x K rounded up to 8 for A, K x N
+ * both rounded up to 8 for B; both when K is not a multiple of 8), or, where
+ * K is too short for the pipelined kernels (under about 3 steps of 64 per
+ * split), read in place by a slower element-wise kernel.  Sizes are limited to M, N, K < 2^31 with every matrix
  * addressable in 64-bit element offsets.  A handle holds one workspace
  * (split-k partials and operand copies), grown on demand with hipMalloc
  * (XGEMM_ERR_ALLOC if that fails): calls that share a handle must be ordered

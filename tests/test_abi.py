@@ -74,7 +74,8 @@ def test_workspace_bytes():
     assert xg.xgemm_workspace_bytes(1024, 1024, 4096, 256, cfg) == 0
     cfg.split_k = 16
     assert xg.xgemm_workspace_bytes(1024, 1024, 65536, 256, cfg) == 16 * 1024 * 1024 * 4
-    assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 16 * 10 * 8 * 4  # rows padded to 4 floats
+    # rows of partials padded to 4 floats; N = 5 also copies B (65536 x 8, after the partials)
+    assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 16 * 10 * 8 * 4 + 65536 * 8 * 2
     cfg.tail_split = 2                      # tail split needs split_k == 1
     assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 0
     cfg.tail_split, cfg.tile = 0, 99
@@ -127,14 +128,15 @@ def test_kernel_family_rules():
     assert fam(1000, 1000, 128) == G           # fewer than 3 K steps of 64
     assert fam(1000, 1000, 136) == P           # 2 full steps and a partial one
     assert fam(1000, 1000, 120) == G           # 1 full step and a partial one
-    # operands the pipelined kernels cannot read in place: below 2^26
-    # multiply-adds the general kernel reads them; above, they are copied
-    small, large = (300, 301, 304), (1000, 1001, 1024)
-    assert fam(*small) == G and fam(*large) == P                  # N % 8 != 0
-    assert fam(300, 304, 301, lda=304) == G and fam(1000, 1000, 1004, lda=1008) == P  # K % 8 != 0
-    assert fam(300, 304, 304, a=al + 2) == G and fam(1000, 1000, 1024, a=al + 2) == P  # misaligned A
-    assert fam(300, 304, 304, lda=308) == G and fam(1000, 1000, 1024, lda=1028) == P  # lda % 8 != 0
-    assert fam(300, 304, 304, ldb=308) == G and fam(1000, 1000, 1024, ldb=1004) == P  # ldb % 8 != 0
+    # operands the pipelined kernels cannot read in place are copied into
+    # the workspace when that makes the pipelined kernel eligible; with too
+    # few K steps the general kernel reads them in place
+    short = 120   # one full K step and a partial one
+    assert fam(300, 301, 304) == P and fam(300, 301, short) == G                  # N % 8 != 0
+    assert fam(300, 304, 301, lda=304) == P and fam(300, 304, 117, lda=120) == G  # K % 8 != 0
+    assert fam(300, 304, 304, a=al + 2) == P and fam(300, 304, short, a=al + 2) == G  # misaligned A
+    assert fam(300, 304, 304, lda=308) == P and fam(300, 304, short, lda=124) == G  # lda % 8 != 0
+    assert fam(300, 304, 304, ldb=308) == P and fam(300, 304, short, ldb=308) == G  # ldb % 8 != 0
     cfg16 = xg.xgemm_config(tile=0, split_k=16, group_m=4, tail_split=0)
     assert fam(1024, 1024, 65536, c=cfg16) == P
     assert fam(1024, 1024, 1024, c=cfg16) == G   # 64-element splits are too short

@@ -130,7 +130,7 @@ def test_partial_k_step_in_last_split(tile, split):
                 "partial last split tile %d split %d" % (tile, split))
 
 
-# Layouts the pipelined kernels cannot read in place, above 2^26 multiply-adds:
+# Layouts the pipelined kernels cannot read in place:
 # the library copies the operand(s) into its workspace, zero-padded
 PACKED_CASES = {
     "n_odd": ((1000, 1001, 1024), {}),
@@ -474,6 +474,27 @@ def test_strided_batched(dtype, shape):
         check_close(C[b], C_ref, S, "batch %d of %s" % (b, shape))
 
 
+def test_strided_batched_general_kernel():
+    """Batched calls read unaligned operands in place (no copies): odd N and
+    an odd leading dimension at K = 1000 run the general kernel."""
+    L, M, N, K = 3, 300, 201, 1000
+    As, Bs, refs = [], [], []
+    for b in range(L):
+        A, B, C_ref, S = _case(M, N, K, "bf16", seed=60 + b)
+        As.append(A); Bs.append(B); refs.append((C_ref, S))
+    lda = K + 3
+    abuf = np.full((L, M, lda), 0x7FC0, dtype=np.uint16)   # NaN row padding, never read
+    for b in range(L):
+        abuf[b, :, :K] = As[b]
+    Ad = torch.from_numpy(abuf.view(np.int16)).cuda().view(torch.bfloat16)[:, :, :K]
+    Bd = torch.from_numpy(np.stack(Bs).view(np.int16)).cuda().view(torch.bfloat16)
+    assert Ad.stride(1) == lda and Bd.stride(1) == N
+    C = xg.bmm(Ad, Bd)
+    torch.cuda.synchronize()
+    for b in range(L):
+        check_close(C[b].cpu().numpy(), *refs[b], "batched general %d" % b)
+
+
 def test_strided_batched_shared_a_and_padding():
     L, M, N, K = 3, 260, 136, 448
     As, Bs = _batched_case(L, M, N, K, "bf16", seed=7, shared_a=True)
@@ -542,7 +563,7 @@ def _random_cases(n, seed):
     rng = np.random.default_rng(seed)
     cases = []
     for _ in range(n):
-        big = rng.random() < 0.4   # above the copy threshold (2^26 multiply-adds) in part
+        big = rng.random() < 0.4   # a share of larger shapes
         hi = 900 if big else 300
         M, N, K = (int(v) for v in rng.integers(1, hi, size=3))
         lda = K + int(rng.choice([0, 0, 1, 3, 8]))

@@ -244,10 +244,10 @@ def test_kernel_tail_split():
 
 @pytest.mark.parametrize("shape,c,lds", [
     ((100, 100, 100), cfg(2), {}),                    # K not a multiple of 64
-    ((300, 260, 448), cfg(0), {}),                    # N not a multiple of 8
+    ((300, 260, 120), cfg(0), {}),                    # N not a multiple of 8, K too short to copy for
     ((256, 256, 128), cfg(1), {}),                    # 2 K steps: too few for the pipeline
     ((129, 136, 320), cfg(2, 2), {"lda": 323}),       # lda not a multiple of 8
-    ((200, 130, 1000), cfg(1, 4), {"ldb": 131}),      # split-k over the general kernel
+    ((200, 130, 400), cfg(1, 4), {"ldb": 131}),       # split-k over the general kernel (2 steps per split)
 ])
 def test_general_kernel_traces_are_race_free(shape, c, lds):
     info = xg.xgemm_trace_plan(*shape[:3], sc.BASE_A, lds.get("lda", shape[2]), sc.BASE_B, lds.get("ldb", shape[1]),
@@ -406,7 +406,7 @@ def test_partial_k_step_missing_barrier_is_caught(tile):
 
 
 # ---------------------------------------------------------------------------
-# operands packed into the workspace (unaligned layouts above 2^26 MACs)
+# operands packed into the workspace (layouts the kernels cannot read in place)
 # ---------------------------------------------------------------------------
 
 @pytest.mark.parametrize("shape,lds,tile,split", [
