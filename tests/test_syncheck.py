@@ -260,10 +260,12 @@ def test_general_kernel_traces_are_race_free(shape, c, lds):
 def test_general_kernel_trace_structure():
     """General kernel, n K steps: one barrier after the first tile store and
     one per K step; each K step's tiles written to LDS once."""
-    info = xg.xgemm_trace_plan(256, 256, 5 * 64 + 1, sc.BASE_A, 5 * 64 + 1, sc.BASE_B, 256, sc.BASE_C, 256, cfg(0),
-                               256, 0)
-    assert info.family == xg.XGEMM_KERNEL_GENERAL
-    ev, counts = sc.trace_workgroup(256, 256, 5 * 64 + 1, 5 * 64 + 1, 256, 256, cfg(0), 256, 0, 0, info.threads)
+    # lda = 2^23: a tile's byte offsets exceed 32 bits, so the general kernel
+    # runs (the layout is aligned, so no copy is made); K = 328: 6 K steps
+    K, lda = 5 * 64 + 8, 1 << 23
+    info = xg.xgemm_trace_plan(256, 256, K, sc.BASE_A, lda, sc.BASE_B, 256, sc.BASE_C, 256, cfg(0), 256, 0)
+    assert info.family == xg.XGEMM_KERNEL_GENERAL and info.packed == 0
+    ev, counts = sc.trace_workgroup(256, 256, K, lda, 256, 256, cfg(0), 256, 0, 0, info.threads)
     waves = sc.wave_streams(ev, counts)
     nk = 6
     for ws in waves:
@@ -278,10 +280,11 @@ def test_general_kernel_trace_structure():
     ("no LDS wait", lambda op: op != sc.WAIT_LGKM),
 ])
 def test_general_kernel_planted_mistakes(name, keep):
-    # K = 321 is not a multiple of the K step, so the general kernel runs
-    info = xg.xgemm_trace_plan(256, 256, 321, sc.BASE_A, 321, sc.BASE_B, 256, sc.BASE_C, 256, cfg(0), 256, 0)
+    # lda = 2^23 keeps the general kernel (32-bit tile offsets overflow)
+    K, lda = 5 * 64 + 8, 1 << 23
+    info = xg.xgemm_trace_plan(256, 256, K, sc.BASE_A, lda, sc.BASE_B, 256, sc.BASE_C, 256, cfg(0), 256, 0)
     assert info.family == xg.XGEMM_KERNEL_GENERAL
-    ev, counts = sc.trace_workgroup(256, 256, 321, 321, 256, 256, cfg(0), 256, 0, 0, info.threads)
+    ev, counts = sc.trace_workgroup(256, 256, K, lda, 256, 256, cfg(0), 256, 0, 0, info.threads)
     waves = sc.wave_streams(ev, counts)
     lds = info.lds_bytes
     assert sc.check_workgroup_lds(waves, lds) == []
