@@ -137,8 +137,11 @@ int xgemm_run_config(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
  * stride_c >= (M-1)*ldc + N when batch > 1.  batch == 0: no-op.  The
  * paper's benchmarks include such batched products (its comparison uses a
  * strided-batched vendor GEMM with batch count L, Section 6).  All problems
- * run in one launch without split-k; 16-byte vector paths additionally
- * need stride_a and stride_b multiples of 8 and stride_c a multiple of 4.
+ * run in one launch without split-k; the pipelined path additionally needs
+ * stride_a and stride_b multiples of 8 (vector stores of C: stride_c a
+ * multiple of 4).  Operands that miss the layout are copied into the
+ * handle's workspace as in xgemm_run, one copy per problem (one in all for
+ * a stride of 0), which needs batch times the operand's padded size.
  * Errors as xgemm_run, plus XGEMM_ERR_INVALID_ARG for negative batch or
  * strides, overlapping outputs or batch > 2^31 - 1.
  */

@@ -19,9 +19,11 @@ typedef uint32_t pack_u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kPackSeg = 2048;  // destination columns per workgroup iteration (256 threads x 8)
 
-// dst[r * ldd + c] = src[r * lds + c] for r < src_rows and c < src_cols, and 0
-// elsewhere in the rows x (8 * cols8) destination.  dst is 16-byte aligned
-// and ldd a multiple of 8; src is 2-byte aligned with any leading dimension.
+// dst[b * dst_stride + r * ldd + c] = src[b * src_stride + r * lds + c] for
+// r < src_rows and c < src_cols, and 0 elsewhere in each of the `batch`
+// rows x (8 * cols8) destinations.  dst and dst_stride keep every destination
+// 16-byte aligned, ldd is a multiple of 8; src is 2-byte aligned with any
+// leading dimension and batch stride.
 //
 // A workgroup copies one segment of kPackSeg destination columns of one row
 // per iteration of a grid-stride loop.  Its source elements are staged in
@@ -30,24 +32,26 @@ constexpr int kPackSeg = 2048;  // destination columns per workgroup iteration (
 // reach outside it, are read element by element), so every global load
 // stays inside the source row; then each thread writes one 16-byte chunk of
 // the destination row from LDS, shifted by the source's misalignment.
-__global__ void __launch_bounds__(256) pack16(const uint16_t *__restrict__ src, int64_t lds, int src_rows,
-                                              int src_cols, uint16_t *__restrict__ dst, int64_t ldd, int rows,
-                                              int cols8)
+__global__ void __launch_bounds__(256) pack16(const uint16_t *__restrict__ src, int64_t lds, int64_t src_stride,
+                                              int src_rows, int src_cols, uint16_t *__restrict__ dst, int64_t ldd,
+                                              int64_t dst_stride, int rows, int cols8, int batch)
 {
     __shared__ __attribute__((aligned(16))) uint16_t span[kPackSeg + 16];
     const int tid = threadIdx.x;
     const int cols = cols8 * 8;
     const int segs = (cols + kPackSeg - 1) / kPackSeg;
-    const int64_t items = (int64_t)rows * segs;
+    const int64_t per = (int64_t)rows * segs;
+    const int64_t items = per * batch;
     for (int64_t w = blockIdx.x; w < items; w += gridDim.x) {
-        const int r = (int)(w / segs);
-        const int c_begin = (int)(w % segs) * kPackSeg;
+        const int64_t b = w / per;
+        const int r = (int)((w - b * per) / segs);
+        const int c_begin = (int)((w - b * per) % segs) * kPackSeg;
         const int c_end = min(c_begin + kPackSeg, cols);
         // valid source columns of this segment: [c_begin, v_end)
         const int v_end = r < src_rows ? min(c_end, src_cols) : c_begin;
         int shift = 0;  // elements of the first aligned chunk before c_begin
         if (v_end > c_begin) {
-            const uint16_t *s0 = src + (int64_t)r * lds + c_begin;
+            const uint16_t *s0 = src + b * src_stride + (int64_t)r * lds + c_begin;
             const uintptr_t a0 = (uintptr_t)s0, a_end = (uintptr_t)(s0 + (v_end - c_begin));
             const uintptr_t a_lo = a0 & ~(uintptr_t)15;
             shift = (int)(a0 - a_lo) / 2;
@@ -77,7 +81,7 @@ __global__ void __launch_bounds__(256) pack16(const uint16_t *__restrict__ src, 
                 v[e] = lo | (hi << 16);
             }
             pack_u32x4 out = {v[0], v[1], v[2], v[3]};
-            *(pack_u32x4 *)(dst + (int64_t)r * ldd + c) = out;
+            *(pack_u32x4 *)(dst + b * dst_stride + (int64_t)r * ldd + c) = out;
         }
         __syncthreads();
     }

@@ -552,6 +552,20 @@ int ensure_workspace(xgemm_ctx *h, size_t bytes, hipStream_t s)
     return XGEMM_OK;
 }
 
+// Copy `batch` src_rows x src_cols operands (leading dimension ld, batch
+// stride src_stride) into dense rows x cols copies at dst (rows, cols
+// multiples of 8 where padded; the copies follow each other).
+hipError_t launch_pack(const void *src, int64_t ld, int64_t src_stride, int64_t src_rows, int64_t src_cols, char *dst,
+                       int64_t rows, int64_t cols, int64_t batch, hipStream_t s)
+{
+    const int64_t items = batch * rows * cdiv(cols, xgemm_dev::kPackSeg);  // (problem, row, segment)
+    const int grid = (int)(items < 8192 ? items : 8192);
+    hipLaunchKernelGGL(xgemm_dev::pack16, dim3(grid), dim3(256), 0, s, (const uint16_t *)src, ld, src_stride,
+                       (int)src_rows, (int)src_cols, (uint16_t *)dst, (int64_t)cols, rows * cols, (int)rows,
+                       (int)(cols / 8), (int)batch);
+    return hipGetLastError();
+}
+
 int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
         int64_t ldb, float *C, int64_t ldc, int dtype, void *stream, const xgemm_config *forced)
 {
@@ -594,19 +608,11 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     // operand copies for the pipelined kernels
     char *const ws = (char *)h->workspace;
     const Pack &pk = plan.pack;
-    auto pack = [&](const void *src, int64_t ld, int64_t src_rows, int64_t src_cols, size_t off, int64_t rows,
-                    int64_t cols) {
-        const int64_t items = rows * cdiv(cols, xgemm_dev::kPackSeg);  // (row, segment) pairs
-        const int grid = (int)(items < 8192 ? items : 8192);
-        hipLaunchKernelGGL(xgemm_dev::pack16, dim3(grid), dim3(256), 0, s, (const uint16_t *)src, ld, (int)src_rows,
-                           (int)src_cols, (uint16_t *)(ws + off), (int64_t)cols, (int)rows, (int)(cols / 8));
-        return hipGetLastError();
-    };
-    if (pk.a && (e = pack(A, lda, M, K, pk.a_off, M, pk.k8)) != hipSuccess) {
+    if (pk.a && (e = launch_pack(A, lda, 0, M, K, ws + pk.a_off, M, pk.k8, 1, s)) != hipSuccess) {
         set_error(h, "pack A launch", e);
         return XGEMM_ERR_HIP;
     }
-    if (pk.b && (e = pack(B, ldb, K, N, pk.b_off, pk.k8, pk.n8)) != hipSuccess) {
+    if (pk.b && (e = launch_pack(B, ldb, 0, K, N, ws + pk.b_off, pk.k8, pk.n8, 1, s)) != hipSuccess) {
         set_error(h, "pack B launch", e);
         return XGEMM_ERR_HIP;
     }
@@ -683,6 +689,51 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
     rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan, false);
     if (rc != XGEMM_OK)
         return rc;
+    // Operands the pipelined kernel cannot read in place (for every problem:
+    // alignment, leading dimension, batch stride, N or K) are copied into the
+    // workspace, one copy per problem (a single one for a shared operand,
+    // stride 0), when that makes the pipelined kernel eligible.
+    const bool k_ok = K % 8 == 0;
+    Pack pk;
+    pk.a = !(k_ok && (uintptr_t)A % 16 == 0 && lda % 8 == 0 && sa % 8 == 0);
+    pk.b = !(k_ok && (uintptr_t)B % 16 == 0 && ldb % 8 == 0 && sb % 8 == 0 && N % 8 == 0);
+    if (!k_ok)
+        pk.a = pk.b = true;
+    pk.k8 = cdiv(K, 8) * 8;
+    pk.n8 = cdiv(N, 8) * 8;
+    const int64_t na = sa == 0 ? 1 : batch, nb = sb == 0 ? 1 : batch;
+    Plan packed;
+    if ((pk.a || pk.b) &&
+        make_plan_with(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, pk, &packed) == XGEMM_OK &&
+        packed.seg[0].dma) {
+        const size_t a_bytes = pk.a ? (size_t)na * (size_t)M * (size_t)pk.k8 * 2 : 0;
+        pk.a_off = 0;
+        pk.b_off = (a_bytes + 255) / 256 * 256;
+        const size_t ws = pk.b ? pk.b_off + (size_t)nb * (size_t)pk.k8 * (size_t)pk.n8 * 2 : a_bytes;
+        rc = ensure_workspace(h, ws, s);
+        if (rc != XGEMM_OK)
+            return rc;
+        char *const w = (char *)h->workspace;
+        if (pk.a && (e = launch_pack(A, lda, sa, M, K, w + pk.a_off, M, pk.k8, na, s)) != hipSuccess) {
+            set_error(h, "pack A launch", e);
+            return XGEMM_ERR_HIP;
+        }
+        if (pk.b && (e = launch_pack(B, ldb, sb, K, N, w + pk.b_off, pk.k8, pk.n8, nb, s)) != hipSuccess) {
+            set_error(h, "pack B launch", e);
+            return XGEMM_ERR_HIP;
+        }
+        plan = packed;
+        if (pk.a) {
+            plan.seg[0].p.A = (const uint16_t *)(w + pk.a_off);
+            sa = sa == 0 ? 0 : M * pk.k8;
+        }
+        if (pk.b) {
+            plan.seg[0].p.B = (const uint16_t *)(w + pk.b_off);
+            sb = sb == 0 ? 0 : pk.k8 * pk.n8;
+        }
+    } else {
+        pk = Pack{};
+    }
     Segment &g = plan.seg[0];
     if (plan.nseg != 1 || g.reduce != 0 || g.p.split != 1)
         return XGEMM_ERR_INVALID_ARG;  // batched plans are single unsplit launches
@@ -695,7 +746,7 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
     // 16-byte vector paths need every problem's matrices aligned
     g.p.vec_ab = g.p.vec_ab && (sa % 8 == 0) && (sb % 8 == 0);
     g.p.vec_c = g.p.vec_c && (sc % 4 == 0);
-    g.dma = dma_eligible(g.p, kTiles[plan.tile].bm);
+    g.dma = dma_eligible(g.p, kTiles[plan.tile].bm, pk.b);
     e = launch_tile(plan.tile, g.dma, dtype, g.p, (int)(g.grid * batch), s);
     if (e != hipSuccess) {
         set_error(h, "gemm launch", e);

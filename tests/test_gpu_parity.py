@@ -474,10 +474,12 @@ def test_strided_batched(dtype, shape):
         check_close(C[b], C_ref, S, "batch %d of %s" % (b, shape))
 
 
-def test_strided_batched_general_kernel():
-    """Batched calls read unaligned operands in place (no copies): odd N and
-    an odd leading dimension at K = 1000 run the general kernel."""
-    L, M, N, K = 3, 300, 201, 1000
+@pytest.mark.parametrize("K", [1000, 100], ids=["copied", "general"])
+def test_strided_batched_unaligned(K):
+    """Odd N and a padded, odd lda: at K = 1000 every problem's operands are
+    copied into the workspace and the pipelined kernel runs; at K = 100 (two
+    K steps) the general kernel reads them in place."""
+    L, M, N = 3, 300, 201
     As, Bs, refs = [], [], []
     for b in range(L):
         A, B, C_ref, S = _case(M, N, K, "bf16", seed=60 + b)
@@ -492,7 +494,24 @@ def test_strided_batched_general_kernel():
     C = xg.bmm(Ad, Bd)
     torch.cuda.synchronize()
     for b in range(L):
-        check_close(C[b].cpu().numpy(), *refs[b], "batched general %d" % b)
+        check_close(C[b].cpu().numpy(), *refs[b], "batched unaligned K=%d problem %d" % (K, b))
+
+
+def test_strided_batched_unaligned_shared_b():
+    """A shared B (stride 0) with odd N is copied once; A per problem."""
+    L, M, N, K = 4, 256, 129, 512
+    As, refs = [], []
+    _, B, _, _ = _case(M, N, K, "fp16", seed=70)
+    for b in range(L):
+        A, _, _, _ = _case(M, N, K, "fp16", seed=71 + b)
+        C_ref, S = oracle.gemm(A, B, "fp16")
+        As.append(A); refs.append((C_ref, S))
+    Ad = torch.from_numpy(np.stack(As).view(np.int16)).cuda().view(torch.float16)
+    Bd = torch.from_numpy(B.view(np.int16)).cuda().view(torch.float16).unsqueeze(0).expand(L, K, N)
+    C = xg.bmm(Ad, Bd)
+    torch.cuda.synchronize()
+    for b in range(L):
+        check_close(C[b].cpu().numpy(), *refs[b], "batched shared B problem %d" % b)
 
 
 def test_strided_batched_shared_a_and_padding():
