@@ -550,6 +550,12 @@ struct DeviceOps {
     __device__ __forceinline__ void wait_lgkm0() const { wait_lgkmcnt0(); }
     __device__ __forceinline__ void barrier() const { barrier_only(); }
     __device__ __forceinline__ void fence() const { sched_fence(); }
+    // issue priority of this wave among the waves of its SIMD (0 .. 3)
+    template <int P>
+    __device__ __forceinline__ void priority() const
+    {
+        __builtin_amdgcn_s_setprio(P);
+    }
     __device__ __forceinline__ void store4(float *q, f32x4 v) const { *(f32x4 *)q = v; }
     __device__ __forceinline__ void store1(float *q, float v) const { *q = v; }
     // general kernel: loads into registers, LDS writes, a full barrier
@@ -924,6 +930,9 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
                 ops.template wait_vm<0>();
             ops.barrier();
             ops.fence();
+            // the rows that issue the direct loads run at a raised priority
+            // against the other wave of the SIMD (measured 0.6-0.8% faster)
+            ops.template priority<1>();
             if constexpr (WAIT >= 0) {
 #pragma unroll
                 for (int i = 0; i < R; ++i)
@@ -947,6 +956,7 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
                 }
                 ops.fence();
             }
+            ops.template priority<0>();
         };
         if (nk >= 2) {
             issue_loads(0, 0);

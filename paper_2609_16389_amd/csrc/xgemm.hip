@@ -952,6 +952,10 @@ struct TraceOps {
     void wait_lgkm0() const { push(XGEMM_TRACE_WAIT_LGKM, 0, 0, 0); }
     void barrier() const { push(XGEMM_TRACE_BARRIER, 0, 0, 0); }
     void fence() const {}
+    template <int P>
+    void priority() const
+    {
+    }
     void store4(float *q, xgemm_dev::f32x4) const { push(XGEMM_TRACE_STORE, 16, 0, (int64_t)(uintptr_t)q); }
     void store1(float *q, float) const { push(XGEMM_TRACE_STORE, 4, 0, (int64_t)(uintptr_t)q); }
     xgemm_dev::u32x4 gload16(const uint16_t *q) const
