@@ -363,6 +363,35 @@ def test_invalid_arguments_on_gpu():
     assert torch.all(C == 0)  # nothing was enqueued
 
 
+def test_workspace_allocation_failure():
+    """A call whose operand copies would need about 4 TiB of workspace fails
+    with XGEMM_ERR_ALLOC before anything is enqueued, and the handle stays
+    usable.  (The pointers are never dereferenced: no kernel is launched.)"""
+    h = xg.xgemm_create()
+    try:
+        A = torch.zeros((16, 16), dtype=torch.bfloat16, device="cuda")
+        C = torch.full((16, 16), 7.0, dtype=torch.float32, device="cuda")
+        s = torch.cuda.current_stream().cuda_stream
+        big = (1 << 20) + 1           # K and N odd: both operands would be copied
+        need = xg.xgemm_workspace_bytes(1 << 20, big, big, 256, xg.xgemm_select_config(1 << 20, big, big, 0, 256))
+        assert need > 1 << 41
+        rc = xg.xgemm_run(h, 1 << 20, big, big, A.data_ptr(), big, A.data_ptr(), big, C.data_ptr(), big, 0, s)
+        assert rc == xg.XGEMM_ERR_ALLOC
+        assert "workspace" in xg.xgemm_last_error(h)
+        torch.cuda.synchronize()
+        assert torch.all(C == 7.0)
+        # still usable
+        Ab, Bb, C_ref, S = _case(100, 101, 103, "bf16", seed=90)
+        Ad, Bd = to_device(Ab, "bf16"), to_device(Bb, "bf16")
+        out = torch.empty((100, 101), dtype=torch.float32, device="cuda")
+        assert xg.xgemm_run(h, 100, 101, 103, Ad.data_ptr(), 103, Bd.data_ptr(), 101, out.data_ptr(), 101, 0,
+                            s) == xg.XGEMM_OK
+        torch.cuda.synchronize()
+        check_close(out.cpu().numpy(), C_ref, S, "after an allocation failure")
+    finally:
+        xg.xgemm_destroy(h)
+
+
 def test_own_handle_lifecycle_and_stream():
     h = xg.xgemm_create()
     try:
