@@ -17,7 +17,9 @@ namespace xgemm_dev {
 
 typedef uint32_t pack_u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kPackSeg = 2048;  // destination columns per workgroup iteration (256 threads x 8)
+// destination columns per workgroup iteration: 256 threads x 4 chunks of 8,
+// which keeps 16 KiB per workgroup in flight before each barrier
+constexpr int kPackSeg = 8192;
 
 // dst[b * dst_stride + r * ldd + c] = src[b * src_stride + r * lds + c] for
 // r < src_rows and c < src_cols, and 0 elsewhere in each of the `batch`
@@ -30,8 +32,8 @@ constexpr int kPackSeg = 2048;  // destination columns per workgroup iteration (
 // LDS through 16-byte aligned loads (the 16-byte chunks that lie wholly
 // inside the segment's source span; the first and last chunk, which may
 // reach outside it, are read element by element), so every global load
-// stays inside the source row; then each thread writes one 16-byte chunk of
-// the destination row from LDS, shifted by the source's misalignment.
+// stays inside the source row; then the threads write the destination row's
+// 16-byte chunks from LDS, shifted by the source's misalignment.
 __global__ void __launch_bounds__(256) pack16(const uint16_t *__restrict__ src, int64_t lds, int64_t src_stride,
                                               int src_rows, int src_cols, uint16_t *__restrict__ dst, int64_t ldd,
                                               int64_t dst_stride, int rows, int cols8, int batch)
@@ -70,8 +72,7 @@ __global__ void __launch_bounds__(256) pack16(const uint16_t *__restrict__ src, 
             }
         }
         __syncthreads();
-        const int c = c_begin + 8 * tid;
-        if (c < c_end) {
+        for (int c = c_begin + 8 * tid; c < c_end; c += 8 * 256) {
             uint32_t v[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
