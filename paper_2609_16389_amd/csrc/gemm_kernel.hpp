@@ -594,9 +594,8 @@ constexpr int dma_lds_bytes()
 // MI is the MFMA block: 32 (v_mfma_f32_32x32x16, 16 k per instruction) or
 // 16 (v_mfma_f32_16x16x32, 32 k per instruction).  Both do the same work per
 // K step from the same LDS bytes.  On random data the GPU is power-capped;
-// there the 16 x 16 shape sustains more flops (measured 1864 against 1753
-// TFLOP/s MFMA-only with accumulators in AGPRs, about 2050 with them in
-// VGPRs, where it issues every 16 cycles instead of about 19).
+// there the 16 x 16 shape sustains more flops (MFMA-only, about 2100
+// against 1840 TFLOP/s, with the accumulators in VGPRs or AGPRs alike).
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, int MI, class Ops>
 __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmParams &p_in, int block, int nblocks,
                                                   int tid)
@@ -882,9 +881,10 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
 
     if constexpr (INPLACE) {
         // Two waves per SIMD, 16 x 16 x 32 MFMAs, BK 64 (two sub-steps), two
-        // LDS stages.  The 128 accumulator registers of a wave then fit in
-        // ordinary VGPRs, where the MFMA issues every 16 cycles (with the
-        // accumulators in AGPRs it takes about 19).  To stay within the 256
+        // LDS stages; each wave owns 128 accumulator registers, and the two
+        // waves of a SIMD cover each other's waits (measured 1-4.5% faster
+        // than one wave per SIMD owning a 128 x 128 block, although the
+        // waves read 1.5 times the LDS bytes).  To stay within the 256
         // registers of a wave, the A fragments are single-buffered: block
         // row i of the next sub-step is read into ga[i] as soon as row i of
         // the current sub-step has issued its MFMAs.  B fragments are
