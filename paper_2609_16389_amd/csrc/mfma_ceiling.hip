@@ -6,11 +6,12 @@
 //   mfma_ceiling            prints one markdown table row per configuration
 //
 // Each wave keeps NACC independent accumulators and 8 + 8 distinct operand
-// registers (loaded once from a buffer of bf16 values, uniform on [-1, 1] or
-// all zero) and issues NACC MFMAs per loop iteration, so consecutive MFMAs
-// never depend on each other and every instruction sees new operand bits.
+// registers (loaded once from a buffer of 16-bit values: random, drawn like
+// a workload's inputs, or all zero) and issues NACC MFMAs per loop
+// iteration, so consecutive MFMAs never depend on each other and every
+// instruction sees new operand bits.
 // Configurations:
-//   shape     16x16x32 or 32x32x16 bf16 -> fp32
+//   shape     16x16x32 or 32x32x16 bf16 -> fp32, 16x16x32 fp16 -> fp32
 //   place     where the accumulators live: "vgpr" / "agpr" place them by an
 //             inline-asm register constraint (operands in VGPRs); "builtin"
 //             uses the compiler builtin with twice the accumulators, so that
@@ -18,12 +19,16 @@
 //             accumulators in AGPRs itself (the situation of a 4-wave GEMM
 //             tile whose waves each own a 128 x 128 block)
 //   waves     waves per SIMD (1 or 2)
+// A second table runs the 16 x 16 x 32 instruction of each GEMM workload's
+// type on operands drawn like that workload's inputs (two waves per SIMD,
+// accumulators in VGPRs, as in the 256 x 256 GEMM tile).
 // The clock comes from s_memtime cycles over s_memrealtime (100 MHz) ticks
 // around the loop of the first wave; TFLOP/s from HIP events over the last of
 // 20 back-to-back launches of a few milliseconds each (the power limit
 // settles within the first launches); cycles per MFMA per SIMD from the
 // event time at that clock, divided by the MFMAs one SIMD issues.
 #include <hip/hip_runtime.h>
+#include <math.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <stdlib.h>
@@ -41,7 +46,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kBufQuads = 4096;  // operand source: 4096 x 16 bytes
 constexpr int kCUs = 256;        // one workgroup per CU
 
-enum { SHAPE16 = 0, SHAPE32 = 1 };
+enum { SHAPE16 = 0, SHAPE32 = 1, SHAPE16H = 2 };  // bf16, bf16, fp16
 enum { PLACE_VGPR = 0, PLACE_AGPR = 1, PLACE_BUILTIN = 2 };
 
 template <int SHAPE, int PLACE>
@@ -50,7 +55,7 @@ constexpr int nacc()
     // asm placements: 128 accumulator registers per wave (fits two waves
     // per SIMD); builtin: 256, so that they cannot share the 256 VGPRs with
     // the operands
-    return SHAPE == SHAPE16 ? (PLACE == PLACE_BUILTIN ? 64 : 32) : (PLACE == PLACE_BUILTIN ? 16 : 8);
+    return SHAPE != SHAPE32 ? (PLACE == PLACE_BUILTIN ? 64 : 32) : (PLACE == PLACE_BUILTIN ? 16 : 8);
 }
 
 template <int SHAPE, int PLACE, int WPS>
@@ -58,7 +63,8 @@ __global__ void __launch_bounds__(256 * WPS, 1)
 mfma_loop(const u32x4 *__restrict__ src, float *__restrict__ out, int iters, long long *__restrict__ clk)
 {
     constexpr int N = nacc<SHAPE, PLACE>();
-    typedef typename std::conditional<SHAPE == SHAPE16, f32x4, f32x16>::type acc_t;
+    typedef typename std::conditional<SHAPE != SHAPE32, f32x4, f32x16>::type acc_t;
+    static_assert(SHAPE != SHAPE16H || PLACE == PLACE_VGPR, "fp16: VGPR placement only");
     const int tid = threadIdx.x;
     u32x4 a[8], b[8];
 #pragma unroll
@@ -86,6 +92,8 @@ mfma_loop(const u32x4 *__restrict__ src, float *__restrict__ out, int iters, lon
                 else
                     acc[n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, x),
                                                                      __builtin_bit_cast(bf16x8, y), acc[n], 0, 0, 0);
+            } else if constexpr (SHAPE == SHAPE16H) {
+                asm volatile("v_mfma_f32_16x16x32_f16 %0, %1, %2, %0" : "+v"(acc[n]) : "v"(x), "v"(y));
             } else if constexpr (SHAPE == SHAPE16) {
                 if constexpr (PLACE == PLACE_VGPR)
                     asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+v"(acc[n]) : "v"(x), "v"(y));
@@ -107,7 +115,7 @@ mfma_loop(const u32x4 *__restrict__ src, float *__restrict__ out, int iters, lon
 #pragma unroll
     for (int n = 0; n < N; ++n)
 #pragma unroll
-        for (int e = 0; e < (SHAPE == SHAPE16 ? 4 : 16); ++e)
+        for (int e = 0; e < (SHAPE != SHAPE32 ? 4 : 16); ++e)
             s += acc[n][e];
     out[blockIdx.x * blockDim.x + tid] = s;
     if (tid == 0 && blockIdx.x == 0) {
@@ -132,13 +140,45 @@ bool check(hipError_t e, const char *what)
     return true;
 }
 
+enum { DATA_ZERO, DATA_UNIFORM_BF16, DATA_NORMAL1_BF16, DATA_UNIFORM_FP16, DATA_NORMAL002_FP16 };
+
+// kBufQuads x 8 16-bit operands: zeros, or values drawn from splitmix64
+// uniforms (normals by Box-Muller), rounded to nearest even in bf16 or fp16.
+void fill(uint16_t *h, int data)
+{
+    uint64_t x = 0x9e3779b97f4a7c15ull;
+    auto uni = [&x]() {
+        x += 0x9e3779b97f4a7c15ull;
+        uint64_t z = x;
+        z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+        z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+        z ^= z >> 31;
+        return (double)(z >> 11) * (1.0 / 9007199254740992.0);  // [0, 1)
+    };
+    for (int i = 0; i < kBufQuads * 8; ++i) {
+        double v = 0.0;
+        if (data == DATA_UNIFORM_BF16 || data == DATA_UNIFORM_FP16) {
+            v = 2.0 * uni() - 1.0;
+        } else if (data != DATA_ZERO) {
+            const double u1 = 1.0 - uni(), u2 = uni();
+            v = sqrt(-2.0 * log(u1)) * cos(6.283185307179586 * u2) * (data == DATA_NORMAL1_BF16 ? 1.0 : 0.02);
+        }
+        if (data == DATA_UNIFORM_FP16 || data == DATA_NORMAL002_FP16) {
+            const _Float16 f = (_Float16)(float)v;
+            memcpy(&h[i], &f, 2);
+        } else {
+            h[i] = bf16_rne((float)v);
+        }
+    }
+}
+
 template <int SHAPE, int PLACE, int WPS>
 bool run(const u32x4 *src, float *out, long long *clk, const char *data)
 {
     constexpr int N = nacc<SHAPE, PLACE>();
-    constexpr double kFlopsPerMfma = 16384.0 * (SHAPE == SHAPE16 ? 1 : 2);
+    constexpr double kFlopsPerMfma = 16384.0 * (SHAPE != SHAPE32 ? 1 : 2);
     // about 4 ms per launch at 2 GHz
-    const int iters = (int)(8.0e6 / (N * WPS * 16.0 * (SHAPE == SHAPE16 ? 1 : 2)));
+    const int iters = (int)(8.0e6 / (N * WPS * 16.0 * (SHAPE != SHAPE32 ? 1 : 2)));
     const dim3 grid(kCUs), block(256 * WPS);
     hipEvent_t e0, e1;
     if (!check(hipEventCreate(&e0), "event") || !check(hipEventCreate(&e1), "event"))
@@ -160,7 +200,8 @@ bool run(const u32x4 *src, float *out, long long *clk, const char *data)
     const double mfmas = (double)kCUs * 4 * WPS * iters * N;  // per launch
     const double ghz = (double)h[0] / ((double)h[1] / 100e6) / 1e9;
     const double cyc = ms * 1e-3 * ghz * 1e9 / ((double)iters * N * WPS);  // per MFMA per SIMD
-    printf("| %s | %s | %s | %d | %.2f | %.3f | %.1f |\n", SHAPE == SHAPE16 ? "16x16x32" : "32x32x16",
+    printf("| %s | %s | %s | %d | %.2f | %.3f | %.1f |\n",
+           SHAPE == SHAPE16 ? "16x16x32 bf16" : SHAPE == SHAPE32 ? "32x32x16 bf16" : "16x16x32 fp16",
            PLACE == PLACE_VGPR ? "vgpr (asm)" : PLACE == PLACE_AGPR ? "agpr (asm)" : "builtin, >256 live", data, WPS,
            cyc, ghz, mfmas * kFlopsPerMfma / (ms * 1e-3) / 1e12);
     fflush(stdout);
@@ -189,16 +230,7 @@ int main()
     printf("| MFMA | accumulators | operands | waves per SIMD | cycles per MFMA per SIMD | clock (GHz) | TFLOP/s |\n");
     printf("|---|---|---|---|---|---|---|\n");
     for (int pass = 0; pass < 2; ++pass) {
-        uint64_t x = 0x9e3779b97f4a7c15ull;  // splitmix64, for the random operands
-        for (int i = 0; i < kBufQuads * 8; ++i) {
-            x += 0x9e3779b97f4a7c15ull;
-            uint64_t z = x;
-            z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
-            z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
-            z ^= z >> 31;
-            const float u = (float)((z >> 11) * (1.0 / 9007199254740992.0)) * 2.0f - 1.0f;
-            h[i] = pass == 0 ? bf16_rne(u) : 0;
-        }
+        fill(h, pass == 0 ? DATA_UNIFORM_BF16 : DATA_ZERO);
         if (!check(hipMemcpy(src, h, kBufQuads * sizeof(u32x4), hipMemcpyHostToDevice), "copy"))
             return 1;
         const char *d = pass == 0 ? "uniform[-1,1]" : "zeros";
@@ -206,6 +238,26 @@ int main()
                   run<SHAPE16, PLACE_BUILTIN, 1>(src, out, clk, d) && run<SHAPE16, PLACE_VGPR, 2>(src, out, clk, d) &&
                   run<SHAPE16, PLACE_AGPR, 2>(src, out, clk, d) && run<SHAPE32, PLACE_VGPR, 1>(src, out, clk, d) &&
                   run<SHAPE32, PLACE_AGPR, 1>(src, out, clk, d) && run<SHAPE32, PLACE_BUILTIN, 1>(src, out, clk, d);
+        if (!ok)
+            return 1;
+    }
+    // the operand distributions of the GEMM workloads
+    printf("\n| MFMA | accumulators | operands | waves per SIMD | cycles per MFMA per SIMD | clock (GHz) | TFLOP/s |\n");
+    printf("|---|---|---|---|---|---|---|\n");
+    const struct {
+        int data;
+        const char *name;
+    } wl[] = {{DATA_UNIFORM_BF16, "uniform[-1,1] bf16"},
+              {DATA_NORMAL1_BF16, "normal(0,1) bf16"},
+              {DATA_UNIFORM_FP16, "uniform[-1,1] fp16"},
+              {DATA_NORMAL002_FP16, "normal(0,0.02) fp16"}};
+    for (const auto &w : wl) {
+        fill(h, w.data);
+        if (!check(hipMemcpy(src, h, kBufQuads * sizeof(u32x4), hipMemcpyHostToDevice), "copy"))
+            return 1;
+        const bool ok = (w.data == DATA_UNIFORM_FP16 || w.data == DATA_NORMAL002_FP16)
+                            ? run<SHAPE16H, PLACE_VGPR, 2>(src, out, clk, w.name)
+                            : run<SHAPE16, PLACE_VGPR, 2>(src, out, clk, w.name);
         if (!ok)
             return 1;
     }
