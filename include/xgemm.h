@@ -22,7 +22,8 @@
  * enqueued on a stream when a call fails; no entry point aborts or throws.
  * Memory ownership: A, B and C are device pointers owned by the caller; the
  * library never frees them nor keeps them past the call.  The library owns
- * only the handle and the split-k workspace inside it.
+ * only the handle and the workspace inside it (split-k partials and copies
+ * of operands the fast kernels cannot read in place).
  */
 #ifndef XGEMM_H
 #define XGEMM_H
@@ -46,7 +47,7 @@ enum xgemm_status {
     XGEMM_OK = 0,
     XGEMM_ERR_INVALID_ARG = 1, /* bad size, leading dimension, pointer, dtype or config */
     XGEMM_ERR_UNSUPPORTED = 2, /* the current device is not a gfx950 GPU */
-    XGEMM_ERR_ALLOC = 3,       /* the split-k workspace could not be allocated */
+    XGEMM_ERR_ALLOC = 3,       /* the handle's workspace could not be allocated */
     XGEMM_ERR_HIP = 4          /* a HIP runtime call failed; see xgemm_last_error */
 };
 
@@ -107,8 +108,8 @@ int xgemm_destroy(xgemm_handle_t h);
  * zero-padded, into the handle's workspace (M x K rounded up to 8 for A, K x N
  * both rounded up to 8 for B; both when K is not a multiple of 8), or, where
  * K is too short for the pipelined kernels (under about 3 steps of 64 per
- * split), read in place by a slower element-wise kernel.  Sizes are limited to M, N, K < 2^31 with every matrix
- * addressable in 64-bit element offsets.  A handle holds one workspace
+ * split), read in place by a slower element-wise kernel.  Sizes are limited
+ * to M, N, K < 2^31 with every matrix addressable in 64-bit element offsets.  A handle holds one workspace
  * (split-k partials and operand copies), grown on demand with hipMalloc
  * (XGEMM_ERR_ALLOC if that fails): calls that share a handle must be ordered
  * on one stream.
@@ -120,8 +121,9 @@ int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
 /*
  * As xgemm_run, with the launch configuration forced to *cfg (validated:
  * XGEMM_ERR_INVALID_ARG for an unknown tile, split_k, group_m or tail_split
- * out of range, or tail_split > 1 together with split_k > 1).  Results agree with xgemm_run within
- * the accuracy contract; only the summation grouping differs.
+ * out of range, or tail_split > 1 together with split_k > 1).  Results agree
+ * with xgemm_run within the accuracy contract; only the summation grouping
+ * differs.
  */
 int xgemm_run_config(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
                      const void *A, int64_t lda, const void *B, int64_t ldb,
@@ -177,19 +179,25 @@ enum xgemm_kernel_family_id {
 /*
  * Which kernel family xgemm_run_config would launch for these arguments
  * (host-only; A and B are only inspected for their alignment).  The
- * pipelined family needs A and B 16-byte aligned, lda and ldb multiples of
- * 8, N a multiple of 8, K a multiple of 64 and at least 192 K values in
- * every split; everything else runs on the general family.  Returns -1 for
- * M, N or K <= 0, leading dimensions too small, or an invalid cfg.
+ * pipelined family reads A and B 16-byte aligned with lda, ldb, N and K
+ * multiples of 8 (B's rows readable to a multiple of 8 columns) and needs
+ * at least 3 K steps of 64 in every split, a partial last step counting;
+ * operands that miss the layout are first copied into the workspace
+ * (xgemm_run), so the general family remains only for too few K steps or
+ * tiles whose byte offsets exceed 32 bits.  Returns -1 for M, N or K <= 0,
+ * leading dimensions too small, or an invalid cfg.
  */
 int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
                         const void *B, int64_t ldb, const xgemm_config *cfg);
 
 /*
  * Bytes of workspace xgemm_run_config needs for this problem and cfg on a
- * device with cu_count compute units: split_k * M * ceil(N/4)*4 floats when
- * split_k > 1, the tail tiles' partials when tail_split > 1 applies, else 0.
- * Host-only.  Returns 0 for invalid arguments.
+ * device with cu_count compute units, for 16-byte aligned A and B with
+ * lda = K and ldb = N: split_k * M * ceil(N/4)*4 floats when split_k > 1, the
+ * tail tiles' partials when tail_split > 1 applies, plus the operand copies
+ * when K or N is not a multiple of 8 (each 256-byte aligned, after the
+ * partials); 0 when nothing is needed.  Host-only.  Returns 0 for invalid
+ * arguments.
  */
 size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, const xgemm_config *cfg);
 
