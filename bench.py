@@ -9,7 +9,8 @@ One step is one call of xgemm_run on the 8192 x 8192 x 8192 bf16 workload
 one JSON line.  ``value`` is the whole-job throughput over the K timed steps,
 bracketed by device synchronisation; ``roofline.achieved`` uses the average
 duration of the GEMM kernel from HIP events recorded on the stream the kernel
-is launched on.  The paper's own protocol (5 warm-up + 100 timed iterations,
+is launched on (for a call the selector cuts into a body and a band of C,
+both launches: ``config.band`` then describes the band).  The paper's own protocol (5 warm-up + 100 timed iterations,
 mean of the inter-quartile range; Section 6) is reported beside it.
 
 Usage: python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--workload NAME]
@@ -303,7 +304,8 @@ def main():
     stream = torch.cuda.current_stream(dev)
     h = xg.handle(0)
     code = xg.XGEMM_BF16 if w.dtype == "bf16" else xg.XGEMM_FP16
-    cfg = xg.xgemm_select_config(w.M, w.N, w.K, code, torch.cuda.get_device_properties(dev).multi_processor_count)
+    plan = xg.xgemm_select_band(w.M, w.N, w.K, code, torch.cuda.get_device_properties(dev).multi_processor_count)
+    cfg = plan.body  # the whole call's configuration, or the body's when C is cut in two
 
     def step():
         rc = xg.xgemm_run(h, w.M, w.N, w.K, A.data_ptr(), w.K, B.data_ptr(), w.N, C.data_ptr(), w.N,
@@ -412,8 +414,12 @@ def main():
         "dtype": w.dtype,
         "data": "synthetic (seeded uniform[-1,1], seed %d)" % w.seed if w.dist == "uniform"
                 else "synthetic (seeded normal(0,%g), seed %d)" % (w.param, w.seed),
-        "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "out": "fp32",
-                   "tile": cfg.tile, "split_k": cfg.split_k},
+        "config": dict({"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "out": "fp32",
+                        "tile": cfg.tile, "split_k": cfg.split_k},
+                       **({} if plan.axis == xg.XGEMM_BAND_NONE else {"band": {
+                           "axis": "columns" if plan.axis == xg.XGEMM_BAND_COLUMNS else "rows",
+                           "body_extent": plan.extent, "tile": plan.band.tile,
+                           "split_k": plan.band.split_k}})),
         "pct_of_peak": round(100.0 * value / peak, 2),
         "paper_protocol_iqr_mean_tflops": round(flops / iqr_mean / 1e12, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",

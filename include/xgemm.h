@@ -112,7 +112,9 @@ int xgemm_destroy(xgemm_handle_t h);
  * to M, N, K < 2^31 with every matrix addressable in 64-bit element offsets.  A handle holds one workspace
  * (split-k partials and operand copies), grown on demand with hipMalloc
  * (XGEMM_ERR_ALLOC if that fails): calls that share a handle must be ordered
- * on one stream.
+ * on one stream.  The configuration comes from the problem shape and the
+ * device's CU count (xgemm_select_band: one plan, or a body and a band of C
+ * launched one after the other).
  */
 int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
               const void *A, int64_t lda, const void *B, int64_t ldb,
@@ -160,6 +162,37 @@ int xgemm_run_strided_batched(xgemm_handle_t h, int64_t batch, int64_t M, int64_
  */
 int xgemm_select_config(int64_t M, int64_t N, int64_t K, int dtype, int cu_count,
                         xgemm_config *out);
+
+/*
+ * Body + band plans.  xgemm_run may cut C in two when the selected
+ * configuration would end in a partial round of workgroups: a body of whole
+ * rounds of one tile shape, and a band (the columns on the right or the rows
+ * at the bottom) with a configuration of its own.  The two run one after the
+ * other on the stream, each as xgemm_run_config would run it on that
+ * sub-matrix, so each output element is still a single sum over K.
+ * xgemm_run_config never bands.
+ */
+enum xgemm_band_axis {
+    XGEMM_BAND_NONE = 0,    /* one plan over all of C */
+    XGEMM_BAND_COLUMNS = 1, /* body: columns [0, extent); band: columns [extent, N) */
+    XGEMM_BAND_ROWS = 2     /* body: rows [0, extent); band: rows [extent, M) */
+};
+
+typedef struct xgemm_band {
+    int32_t axis;       /* an xgemm_band_axis value */
+    int32_t reserved;   /* 0 */
+    int64_t extent;     /* columns or rows of C in the body (0 with XGEMM_BAND_NONE) */
+    xgemm_config body;  /* the body's configuration; with XGEMM_BAND_NONE, the whole call's
+                           (as xgemm_select_config) */
+    xgemm_config band;  /* the band's configuration (zeros with XGEMM_BAND_NONE) */
+} xgemm_band;
+
+/*
+ * The plan xgemm_run would use for this problem on a device with cu_count
+ * compute units (host-only; touches no GPU).  XGEMM_ERR_INVALID_ARG for
+ * negative sizes, an unknown dtype, cu_count < 1 or out == NULL.
+ */
+int xgemm_select_band(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, xgemm_band *out);
 
 /*
  * Workgroup tile of a tile id: rows (bm), columns (bn), K step (bk) and

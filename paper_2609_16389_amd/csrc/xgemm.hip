@@ -182,6 +182,83 @@ void select_config_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int c
     out->tail_split = 0;
 }
 
+// Body + band plans.  When the output tiles of the chosen configuration end
+// in a partial round of workgroups, C may instead be cut into a body of
+// whole rounds of one tile shape and a band (the columns on the right, or
+// the rows at the bottom) that the band's own configuration covers in fewer
+// rounds; the two are launched one after the other, each an ordinary call on
+// a sub-matrix.  Measured: 4096 x 14336 x 4096 (3.5 rounds of 256 x 256
+// tiles) 379 against 396 us with a 2048-column band of 256 x 128 tiles;
+// 6144^3 365 against 438 us; 3-28% on 23 shapes of 2 to 5 rounds.  The
+// time model charges each plan its rounds;
+// a banded plan must come out kBandMargin cheaper (the model does not see
+// that a partial round runs at a higher clock), plus the second launch.
+constexpr double kBandMargin = 0.08;
+constexpr double kBandLaunchUs = 3.0;
+
+struct BandPlan {
+    int axis = XGEMM_BAND_NONE;
+    int64_t extent = 0;  // columns (XGEMM_BAND_COLUMNS) or rows (XGEMM_BAND_ROWS) of C in the body
+    xgemm_config body{}, band{};
+};
+
+BandPlan select_band(int64_t M, int64_t N, int64_t K, int cu_count)
+{
+    BandPlan out;
+    xgemm_config whole;
+    select_config(M, N, K, cu_count, &whole);
+    out.body = whole;
+    if (whole.split_k > 1)
+        return out;  // a K split already spreads the problem over the GPU
+    {
+        // one round or less: the call already takes one tile time, and a
+        // partial round runs at a higher clock than the model charges
+        // (measured: 2048 x 5120 x 4096, 160 tiles, 83 us in one launch
+        // against 92 us as a body and a band)
+        const TileShape &t = kTiles[whole.tile];
+        if (cdiv(M, t.bm) * cdiv(N, t.bn) <= (int64_t)cu_count * t.wg_per_cu)
+            return out;
+    }
+    const double unbanded = model_cost(M, N, K, cu_count, whole.tile, 1);
+    double best = unbanded * (1.0 - kBandMargin);
+    for (int axis = XGEMM_BAND_COLUMNS; axis <= XGEMM_BAND_ROWS; ++axis) {
+        const int64_t along = axis == XGEMM_BAND_COLUMNS ? N : M;   // the dimension the band cuts
+        const int64_t across = axis == XGEMM_BAND_COLUMNS ? M : N;
+        for (int tb = 0; tb < XGEMM_TILE_COUNT; ++tb) {
+            const TileShape &t = kTiles[tb];
+            const int64_t step = axis == XGEMM_BAND_COLUMNS ? t.bn : t.bm;
+            const int64_t tiles_across = cdiv(across, axis == XGEMM_BAND_COLUMNS ? t.bm : t.bn);
+            const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
+            // bodies of r whole rounds (as many tile columns or rows as fit)
+            for (int64_t r = 1;; ++r) {
+                const int64_t j = r * slots / tiles_across;
+                if (j < 1)
+                    continue;
+                const int64_t ext = j * step;
+                if (ext >= along || r > 64)
+                    break;
+                const int64_t bm = axis == XGEMM_BAND_COLUMNS ? M : ext, bn = axis == XGEMM_BAND_COLUMNS ? ext : N;
+                const int64_t rm = axis == XGEMM_BAND_COLUMNS ? M : M - ext, rn = axis == XGEMM_BAND_COLUMNS ? N - ext : N;
+                xgemm_config bandcfg;
+                select_config(rm, rn, K, cu_count, &bandcfg);
+                const double c = model_cost(bm, bn, K, cu_count, tb, 1) +
+                                 model_cost(rm, rn, K, cu_count, bandcfg.tile, bandcfg.split_k) + kBandLaunchUs;
+                if (c < best) {
+                    best = c;
+                    out.axis = axis;
+                    out.extent = ext;
+                    out.body.tile = tb;
+                    out.body.split_k = 1;
+                    out.body.group_m = choose_group_m(cdiv(bm, t.bm), cdiv(bn, t.bn), 1);
+                    out.body.tail_split = 0;
+                    out.band = bandcfg;
+                }
+            }
+        }
+    }
+    return out;
+}
+
 size_t workspace_bytes(int64_t M, int64_t N, int split)
 {
     if (split <= 1)
@@ -566,6 +643,13 @@ hipError_t launch_pack(const void *src, int64_t ld, int64_t src_stride, int64_t 
     return hipGetLastError();
 }
 
+int run_one(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
+            int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s, const xgemm_config &cfg);
+int launch_plan(xgemm_ctx *h, Plan plan, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                const void *B, int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s);
+
+// A call of xgemm_run (forced == nullptr: the selected plan, banded or not)
+// or xgemm_run_config (one launch plan with the forced configuration).
 int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
         int64_t ldb, float *C, int64_t ldc, int dtype, void *stream, const xgemm_config *forced)
 {
@@ -591,20 +675,54 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
         return XGEMM_OK;
     }
 
-    xgemm_config cfg;
     if (forced)
-        cfg = *forced;
-    else
-        select_config(M, N, K, h->cu_count, &cfg);
+        return run_one(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, s, *forced);
+    const BandPlan band = select_band(M, N, K, h->cu_count);
+    if (band.axis == XGEMM_BAND_NONE)
+        return run_one(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, s, band.body);
+    // body, then band: two ordinary calls on sub-matrices of A, B and C,
+    // ordered on the stream (they share the workspace).  Both are planned
+    // and the workspace grown before anything is enqueued.
+    const int64_t ext = band.extent;
+    const bool cols = band.axis == XGEMM_BAND_COLUMNS;
+    const int64_t M1 = cols ? M : ext, N1 = cols ? ext : N;
+    const int64_t M2 = cols ? M : M - ext, N2 = cols ? N - ext : N;
+    const void *A2 = cols ? A : (const void *)((const char *)A + 2 * ext * lda);
+    const void *B2 = cols ? (const void *)((const char *)B + 2 * ext) : B;
+    float *C2 = cols ? C + ext : C + ext * ldc;
+    Plan p1, p2;
+    rc = make_plan(M1, N1, K, A, lda, B, ldb, C, ldc, band.body, h->cu_count, &p1, true);
+    if (rc == XGEMM_OK)
+        rc = make_plan(M2, N2, K, A2, lda, B2, ldb, C2, ldc, band.band, h->cu_count, &p2, true);
+    if (rc == XGEMM_OK)
+        rc = ensure_workspace(h, p1.ws > p2.ws ? p1.ws : p2.ws, s);
+    if (rc == XGEMM_OK)
+        rc = launch_plan(h, p1, M1, N1, K, A, lda, B, ldb, C, ldc, dtype, s);
+    if (rc == XGEMM_OK)
+        rc = launch_plan(h, p2, M2, N2, K, A2, lda, B2, ldb, C2, ldc, dtype, s);
+    return rc;
+}
+
+// One planned call (K > 0, M, N > 0, arguments already checked) with
+// configuration cfg.
+int run_one(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
+            int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s, const xgemm_config &cfg)
+{
     Plan plan;
-    rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan, true);
-    if (rc != XGEMM_OK)
-        return rc;
+    int rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan, true);
+    if (rc == XGEMM_OK)
+        rc = ensure_workspace(h, plan.ws, s);
+    if (rc == XGEMM_OK)
+        rc = launch_plan(h, plan, M, N, K, A, lda, B, ldb, C, ldc, dtype, s);
+    return rc;
+}
 
-    rc = ensure_workspace(h, plan.ws, s);
-    if (rc != XGEMM_OK)
-        return rc;
-
+// Enqueue a plan whose workspace is in place: operand copies, the GEMM
+// launches and their split-k reductions.
+int launch_plan(xgemm_ctx *h, Plan plan, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                const void *B, int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s)
+{
+    hipError_t e;
     // operand copies for the pipelined kernels
     char *const ws = (char *)h->workspace;
     const Pack &pk = plan.pack;
@@ -1112,6 +1230,24 @@ int xgemm_select_config(int64_t M, int64_t N, int64_t K, int dtype, int cu_count
     if (!out || M < 0 || N < 0 || K < 0 || cu_count < 1 || (dtype != XGEMM_BF16 && dtype != XGEMM_FP16))
         return XGEMM_ERR_INVALID_ARG;
     select_config(M, N, K, cu_count, out);
+    return XGEMM_OK;
+}
+
+int xgemm_select_band(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, xgemm_band *out)
+{
+    if (!out || M < 0 || N < 0 || K < 0 || cu_count < 1 || (dtype != XGEMM_BF16 && dtype != XGEMM_FP16))
+        return XGEMM_ERR_INVALID_ARG;
+    *out = xgemm_band{};
+    if (M == 0 || N == 0 || K == 0 || M >= kMaxDim || N >= kMaxDim || K >= kMaxDim) {
+        select_config(M, N, K, cu_count, &out->body);
+        return XGEMM_OK;
+    }
+    const BandPlan b = select_band(M, N, K, cu_count);
+    out->axis = b.axis;
+    out->extent = b.extent;
+    out->body = b.body;
+    if (b.axis != XGEMM_BAND_NONE)
+        out->band = b.band;
     return XGEMM_OK;
 }
 

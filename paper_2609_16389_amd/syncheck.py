@@ -669,6 +669,23 @@ def check_gemv_launch(M, K, cfg, lda=None):
                         events=n_events, seconds=time.perf_counter() - t0, violations=violations)
 
 
+def check_call(M, N, K, dtype=0, cu_count=256, max_blocks=None):
+    """Check the launches xgemm_run makes for a call with 16-byte aligned A,
+    B and C at lda = K, ldb = ldc = N: one plan, or a body and a band of C
+    (xgemm_select_band), each checked as its own call on the sub-matrix.
+    Returns one LaunchReport per part."""
+    band = xg.xgemm_select_band(M, N, K, dtype, cu_count)
+    if band.axis == xg.XGEMM_BAND_NONE:
+        return [check_launch(M, N, K, band.body, cu_count, max_blocks=max_blocks)]
+    e = band.extent
+    if band.axis == xg.XGEMM_BAND_COLUMNS:
+        parts = [((M, e), band.body), ((M, N - e), band.band)]
+    else:
+        parts = [((e, N), band.body), ((M - e, N), band.band)]
+    return [check_launch(m, n, K, c, cu_count, lda=K, ldb=N, ldc=N, max_blocks=max_blocks)
+            for (m, n), c in parts]
+
+
 def main(argv=None):
     import argparse
     ap = argparse.ArgumentParser(description="synchronisation check of the GEMM kernels for one call")
@@ -682,6 +699,16 @@ def main(argv=None):
     ap.add_argument("--cu-count", type=int, default=256)
     ap.add_argument("--max-blocks", type=int, default=None)
     args = ap.parse_args(argv)
+    if all(v is None for v in (args.tile, args.split, args.group_m)) and args.tail_split == 0:
+        # the selector's plan, as xgemm_run makes it (possibly a body and a band)
+        reps = check_call(args.M, args.N, args.K, xg.XGEMM_BF16, args.cu_count, args.max_blocks)
+        for rep in reps:
+            print("%s %s: %d launch(es), %d workgroups, %d LDS streams, %d events, %.2f s: %s" % (
+                rep.shape, rep.config, rep.segments, rep.workgroups, rep.lds_classes, rep.events, rep.seconds,
+                "OK" if rep.ok else "%d violation(s)" % len(rep.violations)))
+            for v in rep.violations[:20]:
+                print("  ", v)
+        return 0 if all(r.ok for r in reps) else 1
     cfg = xg.xgemm_select_config(args.M, args.N, args.K, xg.XGEMM_BF16, args.cu_count)
     if args.tile is not None:
         cfg.tile = args.tile

@@ -43,6 +43,19 @@ class xgemm_config(ctypes.Structure):
             self.tile, self.split_k, self.group_m, self.tail_split)
 
 
+XGEMM_BAND_NONE = 0
+XGEMM_BAND_COLUMNS = 1
+XGEMM_BAND_ROWS = 2
+
+
+class xgemm_band(ctypes.Structure):
+    _fields_ = [("axis", ctypes.c_int32), ("reserved", ctypes.c_int32), ("extent", ctypes.c_int64),
+                ("body", xgemm_config), ("band", xgemm_config)]
+
+    def __repr__(self):
+        return "xgemm_band(axis=%d, extent=%d, body=%r, band=%r)" % (self.axis, self.extent, self.body, self.band)
+
+
 XGEMM_TRACE_LDS_LOAD = 0
 XGEMM_TRACE_LDS_READ = 1
 XGEMM_TRACE_WAIT_VM = 2
@@ -114,6 +127,8 @@ lib.xgemm_run_strided_batched.argtypes = [_handle_t, _i64, _i64, _i64, _i64, _p,
 lib.xgemm_run_strided_batched.restype = _i32
 lib.xgemm_select_config.argtypes = [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(xgemm_config)]
 lib.xgemm_select_config.restype = _i32
+lib.xgemm_select_band.argtypes = [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(xgemm_band)]
+lib.xgemm_select_band.restype = _i32
 lib.xgemm_tile_info.argtypes = [_i32] + [ctypes.POINTER(ctypes.c_int)] * 4
 lib.xgemm_tile_info.restype = _i32
 lib.xgemm_kernel_family.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, ctypes.POINTER(xgemm_config)]
@@ -186,6 +201,14 @@ def xgemm_select_config(M, N, K, dtype, cu_count) -> xgemm_config:
     if rc != XGEMM_OK:
         raise XgemmError(rc)
     return cfg
+
+
+def xgemm_select_band(M, N, K, dtype, cu_count) -> xgemm_band:
+    out = xgemm_band()
+    rc = lib.xgemm_select_band(M, N, K, dtype, cu_count, ctypes.byref(out))
+    if rc != XGEMM_OK:
+        raise XgemmError(rc)
+    return out
 
 
 def xgemm_tile_info(tile):

@@ -227,3 +227,69 @@ def test_packed_plan_layout():
     info = xg.xgemm_trace_plan(1024, 1024, 1024, 1 << 20, 1024, 1 << 21, 1024, 1 << 22, 1024,
                                xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0), 256, 0)
     assert info.packed == 0 and info.a_offset == -1 and info.b_offset == -1 and info.workspace_bytes == 0
+
+
+# ---------------------------------------------------------------------------
+# body + band plans (host-only selection)
+# ---------------------------------------------------------------------------
+
+def _band(M, N, K, dtype=xg.XGEMM_BF16, cu=256):
+    return xg.xgemm_select_band(M, N, K, dtype, cu)
+
+
+def test_band_selection_on_workloads():
+    # 4096 x 14336 x 4096: 896 tiles of 256 x 256 are 3.5 rounds on 256 CUs;
+    # the body takes 3 whole rounds (12288 columns) and a 256 x 128 band
+    # the last 2048 columns in one round
+    b = _band(4096, 14336, 4096, xg.XGEMM_FP16)
+    assert (b.axis, b.extent, b.body.tile, b.body.split_k) == (xg.XGEMM_BAND_COLUMNS, 12288, 0, 1)
+    assert (b.band.tile, b.band.split_k) == (1, 1)
+    # whole rounds, one round or less, and split-k plans are not banded
+    for shape in [(8192, 8192, 8192), (16384, 5120, 4096), (4096, 4096, 4096), (1024, 1024, 65536),
+                  (256, 256, 256), (2048, 5120, 4096), (3072, 3072, 4096)]:
+        b = _band(*shape)
+        assert b.axis == xg.XGEMM_BAND_NONE and b.extent == 0, shape
+        whole = xg.xgemm_select_config(*shape, xg.XGEMM_BF16, 256)
+        assert (b.body.tile, b.body.split_k, b.body.group_m) == (whole.tile, whole.split_k, whole.group_m)
+        assert (b.band.tile, b.band.split_k, b.band.group_m, b.band.tail_split) == (0, 0, 0, 0)
+    # a band of rows
+    b = _band(9472, 2048, 1000)
+    assert (b.axis, b.extent) == (xg.XGEMM_BAND_ROWS, 8192)
+
+
+@pytest.mark.parametrize("cu", [256, 304, 80])
+def test_band_plan_invariants(cu):
+    """Every banded plan cuts C at a whole number of the body's tiles, leaves
+    a non-empty band, runs the body without split-k, and names valid
+    configurations, the band's being the selector's for its shape."""
+    seen = 0
+    for M in (1000, 2048, 3000, 5120, 7168, 9472):
+        for N in (1000, 2048, 3584, 6656, 10240, 14336):
+            for K in (256, 1000, 4096):
+                b = _band(M, N, K, xg.XGEMM_BF16, cu)
+                assert b.axis in (xg.XGEMM_BAND_NONE, xg.XGEMM_BAND_COLUMNS, xg.XGEMM_BAND_ROWS)
+                if b.axis == xg.XGEMM_BAND_NONE:
+                    continue
+                seen += 1
+                bm, bn, _, _ = xg.xgemm_tile_info(b.body.tile)
+                along, step = (N, bn) if b.axis == xg.XGEMM_BAND_COLUMNS else (M, bm)
+                assert 0 < b.extent < along and b.extent % step == 0
+                assert b.body.split_k == 1 and b.body.tail_split == 0 and b.body.group_m >= 1
+                assert 0 <= b.band.tile < xg.XGEMM_TILE_COUNT and 1 <= b.band.split_k <= 16
+                assert b.band.tail_split == 0 and b.band.group_m >= 1
+                # the band's configuration is the selector's for the band's shape
+                rm, rn = (M, N - b.extent) if b.axis == xg.XGEMM_BAND_COLUMNS else (M - b.extent, N)
+                whole = xg.xgemm_select_config(rm, rn, K, xg.XGEMM_BF16, cu)
+                assert (b.band.tile, b.band.split_k) == (whole.tile, whole.split_k)
+    assert seen > 0
+
+
+def test_band_selection_rejects_bad_arguments():
+    out = xg.xgemm_band()
+    assert xg.lib.xgemm_select_band(-1, 1, 1, 0, 256, ctypes.byref(out)) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.lib.xgemm_select_band(1, 1, 1, 5, 256, ctypes.byref(out)) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.lib.xgemm_select_band(1, 1, 1, 0, 0, ctypes.byref(out)) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.lib.xgemm_select_band(1, 1, 1, 0, 256, None) == xg.XGEMM_ERR_INVALID_ARG
+    # empty problems: no band
+    assert xg.lib.xgemm_select_band(0, 4096, 4096, 0, 256, ctypes.byref(out)) == xg.XGEMM_OK
+    assert out.axis == xg.XGEMM_BAND_NONE

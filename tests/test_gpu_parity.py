@@ -473,6 +473,87 @@ def test_full_size_8192_integer_exact_sampled():
 
 
 # ---------------------------------------------------------------------------
+# body + band plans: xgemm_run cutting C in two launches
+# ---------------------------------------------------------------------------
+
+# (M, N, K, dtype): bands of columns, of rows, and one with both operands
+# copied (N and M odd)
+BANDED = [(2560, 6656, 1000, "bf16"), (3072, 5632, 1024, "fp16"), (9472, 2048, 1000, "bf16"),
+          (2047, 10239, 1000, "fp16")]
+
+
+def _band_or_skip(M, N, K, dtype):
+    cu = torch.cuda.get_device_properties(0).multi_processor_count
+    b = xg.xgemm_select_band(M, N, K, CODE[dtype], cu)
+    if b.axis == xg.XGEMM_BAND_NONE:
+        pytest.skip("the selector takes no band for this shape on a %d-CU device" % cu)
+    return b
+
+
+def _cut_samples(b, M, N, rng):
+    """Rows and columns to check: the edges of C, both sides of the cut and
+    a few random ones."""
+    rows = [0, M - 1] + list(rng.integers(0, M, 4))
+    cols = [0, N - 1] + list(rng.integers(0, N, 4))
+    if b.axis == xg.XGEMM_BAND_ROWS:
+        rows += [b.extent - 1, b.extent]
+    else:
+        cols += [b.extent - 1, b.extent]
+    return np.unique(rows), np.unique(cols)
+
+
+@pytest.mark.parametrize("shape", BANDED, ids=lambda s: "%dx%dx%d_%s" % s)
+def test_band_plan_sampled(shape):
+    M, N, K, dtype = shape
+    b = _band_or_skip(M, N, K, dtype)
+    A, B = wl.make_inputs(M, N, K, dtype, "uniform", seed=M + N)
+    C = run_gpu(A, B, dtype)
+    rng = np.random.default_rng(M * 7 + N)
+    rows, cols = _cut_samples(b, M, N, rng)
+    Cr, Sr = oracle.gemm_rows(A, B, dtype, rows)
+    check_close(C[rows], Cr, Sr, "band rows")
+    ri = np.repeat(np.arange(M), cols.size)
+    ci = np.tile(cols, M)
+    c, s = oracle.gemm_entries(A, B, dtype, ri, ci)
+    check_close(C[ri, ci].reshape(M, cols.size), c.reshape(M, cols.size), s.reshape(M, cols.size), "band cols")
+    ri, ci = rng.integers(0, M, 4096), rng.integers(0, N, 4096)
+    c, s = oracle.gemm_entries(A, B, dtype, ri, ci)
+    check_close(C[ri, ci][None], c[None], s[None], "band entries")
+
+
+def test_band_plan_integer_exact():
+    M, N, K = 2560, 6656, 1000
+    b = _band_or_skip(M, N, K, "bf16")
+    A, B = wl.make_int_inputs(M, N, K, "bf16", seed=17)
+    C = run_gpu(A, B, "bf16")
+    rng = np.random.default_rng(3)
+    rows, cols = _cut_samples(b, M, N, rng)
+    Cr, _ = oracle.gemm_rows(A, B, "bf16", rows)
+    check_exact(C[rows], Cr, "int band rows")
+    ri = np.repeat(np.arange(M), cols.size)
+    ci = np.tile(cols, M)
+    c, _ = oracle.gemm_entries(A, B, "bf16", ri, ci)
+    check_exact(C[ri, ci].reshape(M, cols.size), c.reshape(M, cols.size), "int band cols")
+
+
+@pytest.mark.parametrize("shape", [BANDED[0], BANDED[2], BANDED[3]], ids=lambda s: "%dx%dx%d_%s" % s)
+def test_band_plan_equals_one_launch(shape):
+    """With no K split in either part, a banded call sums every element in
+    the same order as one launch of the whole call: the results agree bit for
+    bit."""
+    M, N, K, dtype = shape
+    b = _band_or_skip(M, N, K, dtype)
+    cu = torch.cuda.get_device_properties(0).multi_processor_count
+    whole = xg.xgemm_select_config(M, N, K, CODE[dtype], cu)
+    if b.band.split_k != 1 or whole.split_k != 1:
+        pytest.skip("a K split regroups the sums")
+    A, B = wl.make_inputs(M, N, K, dtype, "uniform", seed=M + 2 * N)
+    C1 = run_gpu(A, B, dtype)
+    C2 = run_gpu(A, B, dtype, config=whole)
+    assert np.array_equal(C1, C2)
+
+
+# ---------------------------------------------------------------------------
 # strided batched products
 # ---------------------------------------------------------------------------
 

@@ -472,6 +472,24 @@ def test_load_outside_a_and_b_is_caught(monkeypatch):
     assert "global_bounds" in {v.kind for v in rep.violations}
 
 
+@pytest.mark.parametrize("shape", [(2560, 6656, 1000), (9472, 2048, 1000), (2047, 10239, 1000)],
+                         ids=["columns", "rows", "columns_packed"])
+def test_band_plan_parts_are_race_free(shape):
+    """xgemm_run's body and band launches, each checked on its sub-matrix of
+    the full operands (the first workgroups of each launch)."""
+    M, N, K = shape
+    reps = sc.check_call(M, N, K, max_blocks=2)
+    assert len(reps) == 2
+    for rep in reps:
+        assert rep.ok, [str(v) for v in rep.violations]
+
+
+def test_band_plan_cli(capsys):
+    assert sc.main(["2560", "6656", "1000", "--max-blocks", "1"]) == 0
+    out = capsys.readouterr().out
+    assert out.count("OK") == 2
+
+
 def test_cli_reports_ok(capsys):
     assert sc.main(["256", "512", "448", "--tile", "0", "--split", "1"]) == 0
     assert "OK" in capsys.readouterr().out
