@@ -5,6 +5,8 @@ report the selector's choice against the fastest one.
 
 One JSON line per shape: the selected configuration, its time, the fastest
 measured configuration and every configuration's median time (microseconds).
+When xgemm_run cuts the call into a body and a band of C (xgemm_select_band),
+that plan is timed too (key "band" in all_us) and is the selected one.
 Inputs are seeded uniform[-1, 1] values generated on the device; configurations
 are timed in shuffled order, several calls per timing, median over rounds.
 """
@@ -44,8 +46,17 @@ def sweep_shape(M: int, N: int, K: int, dtype: str = "bf16", rounds: int = 5) ->
     C = torch.empty(M, N, device="cuda", dtype=torch.float32)
     h = xg.handle(torch.cuda.current_device())
     stream = torch.cuda.current_stream()
-    sel = xg.xgemm_select_config(M, N, K, code, torch.cuda.get_device_properties(0).multi_processor_count)
+    cu = torch.cuda.get_device_properties(0).multi_processor_count
+    sel = xg.xgemm_select_config(M, N, K, code, cu)
+    band = xg.xgemm_select_band(M, N, K, code, cu)
     runs = []
+    if band.axis != xg.XGEMM_BAND_NONE:
+        def call_band():
+            rc = xg.xgemm_run(h, M, N, K, A.data_ptr(), K, B.data_ptr(), N, C.data_ptr(), N, code, stream.cuda_stream)
+            if rc != xg.XGEMM_OK:
+                raise xg.XgemmError(rc)
+        call_band()
+        runs.append(("band", call_band))
     for tile, split in candidates(M, N, K, (sel.tile, sel.split_k)):
         cfg = xg.xgemm_config(tile=tile, split_k=split, group_m=sel.group_m, tail_split=0)
 
@@ -72,10 +83,17 @@ def sweep_shape(M: int, N: int, K: int, dtype: str = "bf16", rounds: int = 5) ->
             times[key].append(e0.elapsed_time(e1) / reps * 1e3)
     med = {k: statistics.median(v) for k, v in times.items()}
     best = min(med, key=med.get)
-    chosen = (sel.tile, sel.split_k)
-    return {"shape": [M, N, K], "dtype": dtype, "selected": list(chosen), "selected_us": round(med[chosen], 2),
-            "best": list(best), "best_us": round(med[best], 2), "loss": round(med[chosen] / med[best], 3),
-            "all_us": {"%d:%d" % k: round(v, 1) for k, v in sorted(med.items())}}
+    chosen = "band" if band.axis != xg.XGEMM_BAND_NONE else (sel.tile, sel.split_k)
+    name = lambda k: k if k == "band" else list(k)
+    out = {"shape": [M, N, K], "dtype": dtype, "selected": name(chosen), "selected_us": round(med[chosen], 2),
+           "best": name(best), "best_us": round(med[best], 2), "loss": round(med[chosen] / med[best], 3),
+           "all_us": {(k if k == "band" else "%d:%d" % k): round(v, 1)
+                      for k, v in sorted(med.items(), key=lambda kv: (kv[0] == "band", str(kv[0])))}}
+    if band.axis != xg.XGEMM_BAND_NONE:
+        out["band"] = {"axis": "columns" if band.axis == xg.XGEMM_BAND_COLUMNS else "rows",
+                       "body_extent": band.extent, "body": [band.body.tile, band.body.split_k],
+                       "band": [band.band.tile, band.band.split_k]}
+    return out
 
 
 def main(argv=None) -> int:
