@@ -229,14 +229,16 @@ BandPlan select_band(int64_t M, int64_t N, int64_t K, int cu_count)
             const int64_t step = axis == XGEMM_BAND_COLUMNS ? t.bn : t.bm;
             const int64_t tiles_across = cdiv(across, axis == XGEMM_BAND_COLUMNS ? t.bm : t.bn);
             const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
-            // bodies of r whole rounds (as many tile columns or rows as fit)
-            for (int64_t r = 1;; ++r) {
+            // bodies of the most whole rounds that fit (R) or one fewer: as
+            // many whole tile columns or rows as r rounds hold.  (An
+            // exhaustive search over r picked R on all 177 banded shapes of
+            // a 1024..16384 grid.)
+            const int64_t R = (along / step) * tiles_across / slots;
+            for (int64_t r = R > 1 ? R - 1 : 1; r <= R; ++r) {
                 const int64_t j = r * slots / tiles_across;
-                if (j < 1)
-                    continue;
                 const int64_t ext = j * step;
-                if (ext >= along || r > 64)
-                    break;
+                if (j < 1 || ext >= along)
+                    continue;
                 const int64_t bm = axis == XGEMM_BAND_COLUMNS ? M : ext, bn = axis == XGEMM_BAND_COLUMNS ? ext : N;
                 const int64_t rm = axis == XGEMM_BAND_COLUMNS ? M : M - ext, rn = axis == XGEMM_BAND_COLUMNS ? N - ext : N;
                 xgemm_config bandcfg;
