@@ -536,6 +536,30 @@ def test_band_plan_integer_exact():
     check_exact(C[ri, ci].reshape(M, cols.size), c.reshape(M, cols.size), "int band cols")
 
 
+@pytest.mark.parametrize("shape", [BANDED[0], BANDED[2]], ids=lambda s: "%dx%dx%d_%s" % s)
+def test_band_plan_padded_leading_dimensions(shape):
+    """The band's sub-matrices start ext rows (A, C) or ext columns (B, C)
+    into the caller's arrays: with padded lda, ldb and ldc the cut must still
+    land on the right elements, and C's padding must stay untouched."""
+    M, N, K, dtype = shape
+    b = _band_or_skip(M, N, K, dtype)
+    A, B = wl.make_inputs(M, N, K, dtype, "uniform", seed=M + 3 * N)
+    lda, ldb, ldc = K + 24, N + 8, N + 12
+    out = empty_out(M, N, ldc=ldc, fill=-7.0)
+    C = run_gpu(A, B, dtype, out=out, lda=lda, ldb=ldb)
+    flat = out.as_strided((M * ldc,), (1,), out.storage_offset()).cpu().numpy().reshape(M, ldc)
+    assert np.all(flat[:, N:] == -7.0), "C padding written"
+    rng = np.random.default_rng(11)
+    rows, cols = _cut_samples(b, M, N, rng)
+    Cr, Sr = oracle.gemm_rows(A, B, dtype, rows)
+    check_close(C[rows], Cr, Sr, "padded band rows")
+    ri = np.repeat(np.arange(M), cols.size)
+    ci = np.tile(cols, M)
+    c, s = oracle.gemm_entries(A, B, dtype, ri, ci)
+    check_close(C[ri, ci].reshape(M, cols.size), c.reshape(M, cols.size), s.reshape(M, cols.size),
+                "padded band cols")
+
+
 @pytest.mark.parametrize("shape", [BANDED[0], BANDED[2], BANDED[3]], ids=lambda s: "%dx%dx%d_%s" % s)
 def test_band_plan_equals_one_launch(shape):
     """With no K split in either part, a banded call sums every element in
