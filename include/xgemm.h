@@ -18,8 +18,12 @@
  *     |C[i][j] - exact| <= 1e-4 * sum_k |A[i][k] * B[k][j]|
  * where "exact" is the real-number result on the stored input values.
  *
- * Error behaviour: every entry point returns an xgemm_status.  Nothing is
- * enqueued on a stream when a call fails; no entry point aborts or throws.
+ * Error behaviour: every entry point returns an xgemm_status; no entry point
+ * aborts or throws.  A call that fails validation or allocation
+ * (XGEMM_ERR_INVALID_ARG, XGEMM_ERR_UNSUPPORTED, XGEMM_ERR_ALLOC) enqueues
+ * nothing.  XGEMM_ERR_HIP from a kernel launch may come after launches the
+ * same call had already enqueued (operand copies, the body of a banded call);
+ * the stream's work is then incomplete and C undefined.
  * Memory ownership: A, B and C are device pointers owned by the caller; the
  * library never frees them nor keeps them past the call.  The library owns
  * only the handle and the workspace inside it (split-k partials and copies
@@ -372,7 +376,7 @@ typedef struct xgemv_config {
  * (split_k * M floats; calls that share a handle must be ordered on one
  * stream).  Errors: XGEMM_ERR_INVALID_ARG for a NULL handle, bad sizes or
  * pointers; XGEMM_ERR_ALLOC if the workspace cannot grow; XGEMM_ERR_HIP if a
- * launch fails.  Nothing is enqueued on error.
+ * launch fails.  Nothing is enqueued on a validation or allocation error.
  */
 int xgemv_run(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
               void *stream);
