@@ -73,7 +73,7 @@ int64_t split_chunk(int64_t K, int split, int bk)
 // once).  A 128 x 128 workgroup shares its CU with a second one in a round
 // that fills every CU twice, which makes each step slower; a last round
 // with at most one workgroup per CU runs at the unshared rate (this per-
-// round charge picks a configuration within 3.7% of the fastest measured,
+// round charge picks a configuration within 3.4% of the fastest measured,
 // geometric mean over 60 shapes, against 5.7% when every round of a launch
 // was charged as shared).  The constants
 // were fitted (least squares on log time) to 180 measured (tile, split)
@@ -99,12 +99,15 @@ double model_cost(int64_t M, int64_t N, int64_t K, int cu_count, int tile, int s
     const int64_t n = tiles * split;
     const double steps = (double)cdiv(std::min(kc, K), t.bk);
     // whole rounds fill every slot (two workgroups per CU share it where the
-    // tile allows); a last partial round shares CUs only past one
-    // workgroup per CU
+    // tile allows); a last partial round shares CUs only past one workgroup
+    // per CU, its step rate taken between the two in proportion to the CUs
+    // that hold two
     const int64_t full = n / slots, last = n % slots;
     double cost = (double)full * (c.fixed_us + steps * (t.wg_per_cu > 1 ? c.step_shared_us : c.step_us));
-    if (last > 0)
-        cost += c.fixed_us + steps * (last > cu_count ? c.step_shared_us : c.step_us);
+    if (last > 0) {
+        const double twice = last > cu_count ? (double)(last - cu_count) / cu_count : 0.0;
+        cost += c.fixed_us + steps * (c.step_us + (c.step_shared_us - c.step_us) * twice);
+    }
     if (split > 1)
         cost += 3.70 + 0.411 * split + (2.0 * split + 1.0) * 4.0 * (double)M * (double)N / 8.494e6;
     return cost;
