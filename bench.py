@@ -15,7 +15,12 @@ mean of the inter-quartile range; Section 6) is reported beside it.
 
 Usage: python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--workload NAME]
        [--no-cpu-baseline] [--no-comparator] [--copy-calibration BYTES]
+       python bench.py --sweep M,N,K [M,N,K ...] [--dtype bf16] [--rounds 5]
        python bench.py --summarize-counters DIR [--workload NAME]   (CPU only)
+
+--sweep times every (tile, split-k) configuration of each shape and reports
+the selector's plan against the fastest one (one JSON line per shape; the
+configuration selector's validation).
 
 Counters: run this script under ``rocprofv3 --pmc`` (one pass per counter
 group, with --copy-calibration 1073741824 on the FETCH_SIZE and WRITE_SIZE
@@ -81,11 +86,39 @@ def stored_traffic(workload: str):
     return None if d is None else d.get("hbm_bytes_per_launch")
 
 
+def _kernel_metrics(med: dict, dur_ns: float, fetch_scale, write_scale) -> dict:
+    """Derived figures of one kernel from its median counter values."""
+    out = {"median_duration_ns": dur_ns, "counters_median": med}
+    if fetch_scale and "FETCH_SIZE" in med:
+        out["hbm_read_bytes_per_launch"] = 1024.0 * med["FETCH_SIZE"] * fetch_scale
+    if write_scale and "WRITE_SIZE" in med:
+        out["hbm_write_bytes_per_launch"] = 1024.0 * med["WRITE_SIZE"] * write_scale
+    if "hbm_read_bytes_per_launch" in out and "hbm_write_bytes_per_launch" in out:
+        out["hbm_bytes_per_launch"] = out["hbm_read_bytes_per_launch"] + out["hbm_write_bytes_per_launch"]
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in med and "GRBM_GUI_ACTIVE" in med:
+        # GRBM_GUI_ACTIVE is summed over the 8 XCDs; 1024 SIMDs in all
+        per_xcd = med["GRBM_GUI_ACTIVE"] / 8.0
+        out["mfma_busy_pct"] = 100.0 * med["SQ_VALU_MFMA_BUSY_CYCLES"] / (per_xcd * 1024.0)
+        out["clock_ghz"] = per_xcd / dur_ns
+    if "SQ_LDS_BANK_CONFLICT" in med and "SQ_LDS_IDX_ACTIVE" in med:
+        out["lds_bank_conflict_pct"] = 100.0 * med["SQ_LDS_BANK_CONFLICT"] / max(1.0, med["SQ_LDS_IDX_ACTIVE"])
+    if "TCC_HIT_sum" in med and "TCC_MISS_sum" in med:
+        out["l2_hit_pct"] = 100.0 * med["TCC_HIT_sum"] / max(1.0, med["TCC_HIT_sum"] + med["TCC_MISS_sum"])
+    return out
+
+
 def summarize_counters(directory: str, workload: str) -> str:
-    """rocprofv3 --pmc CSV output -> profiles/counters_<workload>.json."""
+    """rocprofv3 --pmc CSV output -> profiles/counters_<workload>.json.
+
+    Every kernel of the call is summarised (the GEMM launches, a split-k
+    reduction, operand copies); ``kernel`` and the top-level figures are those
+    of the GEMM kernel with the largest total time, and ``per_call`` sums the
+    HBM bytes and durations of all the call's kernels.  The copy kernel of
+    --copy-calibration only provides the byte counters' scale."""
     import csv
+    import datetime
     import statistics
-    vals, names, durs = {}, {}, {}
+    vals, durs = {}, {}
     for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
         with open(path) as f:
             for r in csv.DictReader(f):
@@ -93,16 +126,17 @@ def summarize_counters(directory: str, workload: str) -> str:
                 vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
                 durs.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
     fam = family(workload)
-    gemm = [k for k in vals if ("%s_kernel" % fam) in k]
     copy = [k for k in vals if "copyBuffer" in k or "copy_kernel" in k]
-    if not gemm:
+    ours = [k for k in vals if k not in copy and "xgem" in k]
+    main_kernels = [k for k in ours if ("%s_kernel" % fam) in k]
+    if not main_kernels:
         raise SystemExit("no %s kernel in %s" % (fam.upper(), directory))
-    k = max(gemm, key=lambda n: len(durs[n]))
-    med = {c: statistics.median(v) for c, v in vals[k].items()}
-    out = {"kernel": k, "workload": workload, "kernel_source_sha256": kernel_source_hash(fam),
-           "dispatches": len(durs[k]) // max(1, len(vals[k])), "median_duration_ns": statistics.median(durs[k]),
-           "counters_median": med}
     fetch_scale = write_scale = None
+    out = {"workload": workload, "kernel_source_sha256": kernel_source_hash(fam),
+           "source": {"directory": os.path.basename(os.path.normpath(directory)),
+                      "summarized": datetime.date.today().isoformat(),
+                      "note": "rocprofv3 --pmc passes of bench.py on one MI355X box; counters perturb "
+                              "timing, so durations here run longer than in a kernel trace"}}
     if copy:
         cm = {c: statistics.median(v) for c, v in vals[copy[0]].items()}
         gib_kib = 1024.0 * 1024.0
@@ -112,17 +146,25 @@ def summarize_counters(directory: str, workload: str) -> str:
             write_scale = gib_kib / cm["WRITE_SIZE"]
         out["copy_calibration"] = {"kernel": copy[0], "bytes": 1 << 30, "counters_median": cm,
                                    "fetch_scale": fetch_scale, "write_scale": write_scale}
-    if fetch_scale and write_scale and "FETCH_SIZE" in med and "WRITE_SIZE" in med:
-        out["hbm_bytes_per_launch"] = 1024.0 * (med["FETCH_SIZE"] * fetch_scale + med["WRITE_SIZE"] * write_scale)
-        out["hbm_read_bytes_per_launch"] = 1024.0 * med["FETCH_SIZE"] * fetch_scale
-        out["hbm_write_bytes_per_launch"] = 1024.0 * med["WRITE_SIZE"] * write_scale
-    if "SQ_VALU_MFMA_BUSY_CYCLES" in med and "GRBM_GUI_ACTIVE" in med:
-        # GRBM_GUI_ACTIVE is summed over the 8 XCDs; 1024 SIMDs in all
-        per_xcd = med["GRBM_GUI_ACTIVE"] / 8.0
-        out["mfma_busy_pct"] = 100.0 * med["SQ_VALU_MFMA_BUSY_CYCLES"] / (per_xcd * 1024.0)
-        out["clock_ghz"] = per_xcd / out["median_duration_ns"]
-    if "SQ_LDS_BANK_CONFLICT" in med and "SQ_LDS_IDX_ACTIVE" in med:
-        out["lds_bank_conflict_pct"] = 100.0 * med["SQ_LDS_BANK_CONFLICT"] / max(1.0, med["SQ_LDS_IDX_ACTIVE"])
+    per = {}
+    for k in ours:
+        med = {c: statistics.median(v) for c, v in vals[k].items()}
+        per[k] = _kernel_metrics(med, statistics.median(durs[k]), fetch_scale, write_scale)
+        per[k]["dispatches"] = len(durs[k]) // max(1, len(vals[k]))
+    main = max(main_kernels, key=lambda n: per[n]["median_duration_ns"])
+    out["kernel"] = main
+    out["dispatches"] = per[main]["dispatches"]
+    out.update({k: v for k, v in per[main].items() if k != "dispatches"})
+    out["kernels"] = per
+    # kernels of one call: each dispatched once per call (the GEMM launches,
+    # the reduction, operand copies)
+    calls = min(p["dispatches"] for p in per.values())
+    out["per_call"] = {
+        "kernels": len(per),
+        "median_duration_ns": sum(p["median_duration_ns"] * p["dispatches"] / calls for p in per.values()),
+    }
+    if all("hbm_bytes_per_launch" in p for p in per.values()):
+        out["per_call"]["hbm_bytes"] = sum(p["hbm_bytes_per_launch"] * p["dispatches"] / calls for p in per.values())
     path = COUNTERS_FILE % workload
     with open(path, "w") as f:
         json.dump(out, f, indent=1, sort_keys=True)
@@ -182,7 +224,7 @@ def bench_gemv(args, w):
     x = torch.from_numpy(x_np).to(dev)
     y = torch.empty(w.M, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
-    h = xg.handle(0)
+    h = xg.handle(0, stream)
     cfg = xg.xgemv_select_config(w.M, w.K, torch.cuda.get_device_properties(dev).multi_processor_count)
 
     def step():
@@ -259,6 +301,92 @@ def bench_gemv(args, w):
     print(json.dumps(out), flush=True)
 
 
+SWEEP_MAX_WORKGROUPS = 4096  # configurations with more workgroups than this are not swept
+
+
+def sweep_candidates(M: int, N: int, K: int, selected: tuple, xg) -> list:
+    """(tile, split) pairs the sweep times for one shape: every tile with
+    split-k 1, 2, 4, 8 and 16 where each split keeps 3 K steps and the launch
+    has at most SWEEP_MAX_WORKGROUPS workgroups, plus the selected one."""
+    out = {tuple(selected)}
+    for tile in range(xg.XGEMM_TILE_COUNT):
+        bm, bn, bk, _ = xg.xgemm_tile_info(tile)
+        for split in (1, 2, 4, 8, 16):
+            if split > 1 and K // split < 3 * bk:
+                continue
+            if -(-M // bm) * -(-N // bn) * split > SWEEP_MAX_WORKGROUPS:
+                continue
+            out.add((tile, split))
+    return sorted(out)
+
+
+def sweep_shape(M: int, N: int, K: int, dtype: str = "bf16", rounds: int = 5) -> dict:
+    """Median time of every candidate configuration (and of xgemm_run's plan
+    when it cuts C into a body and a band) on seeded uniform[-1, 1] inputs
+    drawn on the device; configurations timed in shuffled order, several
+    calls per timing."""
+    import random
+    import statistics
+    import torch
+    from paper_2609_16389_amd import xgemm as xg
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float16
+    code = xg.XGEMM_BF16 if dtype == "bf16" else xg.XGEMM_FP16
+    g = torch.Generator(device="cuda").manual_seed(M + N + K)
+    A = (torch.rand(M, K, device="cuda", generator=g) * 2 - 1).to(tdt)
+    B = (torch.rand(K, N, device="cuda", generator=g) * 2 - 1).to(tdt)
+    C = torch.empty(M, N, device="cuda", dtype=torch.float32)
+    stream = torch.cuda.current_stream()
+    h = xg.handle(torch.cuda.current_device(), stream)
+    cu = torch.cuda.get_device_properties(0).multi_processor_count
+    sel = xg.xgemm_select_config(M, N, K, code, cu)
+    band = xg.xgemm_select_band(M, N, K, code, cu)
+    runs = []
+    if band.axis != xg.XGEMM_BAND_NONE:
+        def call_band():
+            rc = xg.xgemm_run(h, M, N, K, A.data_ptr(), K, B.data_ptr(), N, C.data_ptr(), N, code, stream.cuda_stream)
+            if rc != xg.XGEMM_OK:
+                raise xg.XgemmError(rc)
+        call_band()
+        runs.append(("band", call_band))
+    for tile, split in sweep_candidates(M, N, K, (sel.tile, sel.split_k), xg):
+        cfg = xg.xgemm_config(tile=tile, split_k=split, group_m=sel.group_m, tail_split=0)
+
+        def call(cfg=cfg):
+            rc = xg.xgemm_run_config(h, M, N, K, A.data_ptr(), K, B.data_ptr(), N, C.data_ptr(), N, code,
+                                     stream.cuda_stream, cfg)
+            if rc != xg.XGEMM_OK:
+                raise xg.XgemmError(rc)
+        call()
+        runs.append(((tile, split), call))
+    torch.cuda.synchronize()
+    reps = max(3, min(50, int(2e8 / max(1.0, 2.0 * M * N * K / 1e3))))
+    times: dict = {k: [] for k, _ in runs}
+    for _ in range(rounds):
+        random.shuffle(runs)
+        for key, call in runs:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            call()
+            e0.record(stream)
+            for _ in range(reps):
+                call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times[key].append(e0.elapsed_time(e1) / reps * 1e3)
+    med = {k: statistics.median(v) for k, v in times.items()}
+    best = min(med, key=med.get)
+    chosen = "band" if band.axis != xg.XGEMM_BAND_NONE else (sel.tile, sel.split_k)
+    name = lambda k: k if k == "band" else list(k)
+    out = {"shape": [M, N, K], "dtype": dtype, "selected": name(chosen), "selected_us": round(med[chosen], 2),
+           "best": name(best), "best_us": round(med[best], 2), "loss": round(med[chosen] / med[best], 3),
+           "all_us": {(k if k == "band" else "%d:%d" % k): round(v, 1)
+                      for k, v in sorted(med.items(), key=lambda kv: (kv[0] == "band", str(kv[0])))}}
+    if band.axis != xg.XGEMM_BAND_NONE:
+        out["band"] = {"axis": "columns" if band.axis == xg.XGEMM_BAND_COLUMNS else "rows",
+                       "body_extent": band.extent, "body": [band.body.tile, band.body.split_k],
+                       "band": [band.band.tile, band.band.split_k]}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -274,6 +402,10 @@ def main():
                          "workload's shape instead of one xgemm_run (one JSON line, no baselines)")
     ap.add_argument("--summarize-counters", metavar="DIR", default=None,
                     help="write profiles/counters_<workload>.json from rocprofv3 --pmc output and exit")
+    ap.add_argument("--sweep", nargs="+", metavar="M,N,K", default=None,
+                    help="time every (tile, split-k) configuration of these shapes against the selector's plan")
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "fp16"], help="--sweep: input type")
+    ap.add_argument("--rounds", type=int, default=5, help="--sweep: timing rounds per configuration")
     args = ap.parse_args()
 
     if args.summarize_counters:
@@ -289,6 +421,11 @@ def main():
     from paper_2609_16389_amd import workloads as wl
     from paper_2609_16389_amd import xgemm as xg
 
+    if args.sweep:
+        for shape in args.sweep:
+            M, N, K = (int(v) for v in shape.split(","))
+            print(json.dumps(sweep_shape(M, N, K, args.dtype, args.rounds)), flush=True)
+        return
     if args.workload in wl.GEMV_WORKLOADS:
         bench_gemv(args, wl.GEMV_WORKLOADS[args.workload])
         return
@@ -302,7 +439,7 @@ def main():
     B = torch.from_numpy(B_bits.view(np.int16)).to(dev).view(tdt)
     C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
-    h = xg.handle(0)
+    h = xg.handle(0, stream)
     code = xg.XGEMM_BF16 if w.dtype == "bf16" else xg.XGEMM_FP16
     plan = xg.xgemm_select_band(w.M, w.N, w.K, code, torch.cuda.get_device_properties(dev).multi_processor_count)
     cfg = plan.body  # the whole call's configuration, or the body's when C is cut in two

@@ -80,7 +80,8 @@ typedef struct xgemm_config {
 
 /*
  * Create a handle bound to the calling thread's current HIP device.  Caches
- * the device's compute-unit count and architecture; allocates no device
+ * the device's compute-unit count and architecture and creates one HIP event
+ * (for ordering workspace users across streams); allocates no device
  * memory.  Returns XGEMM_ERR_UNSUPPORTED if the device is not gfx950,
  * XGEMM_ERR_HIP if no device is usable, XGEMM_ERR_INVALID_ARG if out is NULL.
  * The caller owns *out and releases it with xgemm_destroy.
@@ -88,11 +89,20 @@ typedef struct xgemm_config {
 int xgemm_create(xgemm_handle_t *out);
 
 /*
- * Release a handle and its workspace.  NULL is accepted (no-op).  Work that
- * uses the handle's workspace must have completed (synchronize the stream
- * first).
+ * Release a handle, its workspace and its event.  NULL is accepted (no-op).
+ * Work that uses the handle's workspace must have completed (synchronize
+ * the streams it was enqueued on first).
  */
 int xgemm_destroy(xgemm_handle_t h);
+
+/*
+ * Cap the device memory the handle's workspace may hold at `bytes` (0, the
+ * default: no cap).  A later call that needs a larger workspace returns
+ * XGEMM_ERR_ALLOC and enqueues nothing, as when hipMalloc fails; a
+ * workspace already larger than the cap is kept.  For callers that budget
+ * device memory.  XGEMM_ERR_INVALID_ARG for a NULL handle.
+ */
+int xgemm_set_workspace_limit(xgemm_handle_t h, size_t bytes);
 
 /*
  * C = A * B, row-major, enqueued asynchronously on `stream` (a hipStream_t;
@@ -115,8 +125,14 @@ int xgemm_destroy(xgemm_handle_t h);
  * split), read in place by a slower element-wise kernel.  Sizes are limited
  * to M, N, K < 2^31 with every matrix addressable in 64-bit element offsets.  A handle holds one workspace
  * (split-k partials and operand copies), grown on demand with hipMalloc
- * (XGEMM_ERR_ALLOC if that fails): calls that share a handle must be ordered
- * on one stream.  The configuration comes from the problem shape and the
+ * (XGEMM_ERR_ALLOC if that fails).  Calls that share a handle may be
+ * enqueued on different streams: a call that uses the workspace first makes
+ * its stream wait for the last such call on another stream (an event the
+ * handle records), so calls sharing a handle never overlap on the
+ * workspace, and a buffer being grown is freed only after its last user has
+ * completed.  Calls on different streams run concurrently only with one
+ * handle per stream.  A handle must not be used by two host threads at
+ * once.  The configuration comes from the problem shape and the
  * device's CU count (xgemm_select_band: one plan, or a body and a band of C
  * launched one after the other).
  */
@@ -373,10 +389,12 @@ typedef struct xgemv_config {
  * need A and x 16-byte aligned and lda a multiple of 4; any other alignment
  * is still correct through 4-byte loads.  The handle supplies the device's
  * CU count, and its workspace holds the partial sums of a K split
- * (split_k * M floats; calls that share a handle must be ordered on one
- * stream).  Errors: XGEMM_ERR_INVALID_ARG for a NULL handle, bad sizes or
- * pointers; XGEMM_ERR_ALLOC if the workspace cannot grow; XGEMM_ERR_HIP if a
- * launch fails.  Nothing is enqueued on a validation or allocation error.
+ * (split_k * M floats; ordered across streams as for xgemm_run).  Errors:
+ * XGEMM_ERR_INVALID_ARG for a NULL handle, bad sizes or pointers, or a
+ * forced configuration whose launch would exceed 2^31 - 1 workgroups
+ * (ceil(M / rows) * split_k); XGEMM_ERR_ALLOC if the workspace cannot grow;
+ * XGEMM_ERR_HIP if a launch fails.  Nothing is enqueued on a validation or
+ * allocation error.
  */
 int xgemv_run(xgemm_handle_t h, int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
               void *stream);

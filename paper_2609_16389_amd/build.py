@@ -11,9 +11,6 @@ DEPS = [SRC, os.path.join(PKG, "csrc", "gemm_kernel.hpp"), os.path.join(PKG, "cs
         os.path.join(PKG, "csrc", "pack_kernel.hpp"),
         os.path.join(ROOT, "include", "xgemm.h")]
 LIB = os.path.join(PKG, "libxgemm.so")
-# stand-alone MFMA-only microbenchmark (bounds any GEMM on the same data)
-PROBE_SRC = os.path.join(PKG, "csrc", "mfma_ceiling.hip")
-PROBE = os.path.join(PKG, "mfma_ceiling")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # Packed fp32 vector ops are disabled for all device code.
@@ -23,28 +20,14 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++20", "-fPIC", "-shared",
 
 
 def build(verbose: bool = False) -> str:
-    """Compile the library and the microbenchmark; always rebuilds.  Returns
-    the path of the .so."""
+    """Compile the library; always rebuilds.  Returns the path of the .so."""
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [HIPCC] + FLAGS + [SRC, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
-    build_probe(verbose)
     return LIB
-
-
-def build_probe(verbose: bool = False) -> str:
-    """Compile the MFMA-only microbenchmark executable."""
-    tmp = PROBE + ".tmp%d" % os.getpid()
-    flags = [f for f in FLAGS if f not in ("-fPIC", "-shared")]
-    cmd = [HIPCC] + flags + [PROBE_SRC, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, PROBE)
-    return PROBE
 
 
 def is_stale() -> bool:

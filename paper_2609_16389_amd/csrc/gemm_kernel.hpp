@@ -56,7 +56,13 @@ struct GemmParams {
     int64_t stride_a;       //   C + b*stride_c (elements); batched launches have split == 1
     int64_t stride_b;
     int64_t stride_c;
+    int grid;               // workgroups of the launch; a 2-D grid may hold more, which exit
 };
+
+// Linear workgroup id of a launch whose grid may be 2-D (x fastest, as the
+// hardware dispatches them): launches with more than 2^32 threads need the
+// second dimension.
+__device__ __forceinline__ int linear_block() { return (int)(blockIdx.y * gridDim.x + blockIdx.x); }
 
 template <int DT>
 __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c);
@@ -576,8 +582,11 @@ __global__ void __launch_bounds__(WGM * WGN * 64)
 gemm_kernel(GemmParams p_in)
 {
     __shared__ __attribute__((aligned(16))) char smem[general_lds_bytes<BM, BN, BK>()];
+    const int w = linear_block();
+    if (w >= p_in.grid)
+        return;
     const DeviceOps ops{smem};
-    general_tile<BM, BN, BK, WGM, WGN, DT>(ops, p_in, blockIdx.x, gridDim.x, threadIdx.x);
+    general_tile<BM, BN, BK, WGM, WGN, DT>(ops, p_in, w, p_in.grid, threadIdx.x);
 }
 
 // LDS bytes the pipelined kernel allocates.
@@ -1040,8 +1049,11 @@ __global__ void __launch_bounds__(WGM * WGN * 64, 1)
 gemm_kernel_dma(GemmParams p_in)
 {
     __shared__ __attribute__((aligned(1024))) char smem[dma_lds_bytes<BM, BN, BK, STAGES>()];
+    const int w = linear_block();
+    if (w >= p_in.grid)
+        return;
     const DeviceOps ops{smem};
-    dma_tile<BM, BN, BK, STAGES, WGM, WGN, DT, MI>(ops, p_in, blockIdx.x, gridDim.x, threadIdx.x);
+    dma_tile<BM, BN, BK, STAGES, WGM, WGN, DT, MI>(ops, p_in, w, p_in.grid, threadIdx.x);
 }
 
 // C[i][j] = sum over p of W[p][i][j], p ascending (a fixed order, so the

@@ -39,6 +39,7 @@ struct GemvParams {
     int k_chunk;  // K values per split, a multiple of 4 (K when split == 1)
     int split;
     int vec;      // A and x 16-byte aligned and lda a multiple of 4: 16-byte loads
+    int blocks;   // workgroups of the launch, ceil(M / R) * split; a 2-D grid may hold more, which exit
 };
 
 // Operations of the GEMV kernel on the device (the body below is also run on
@@ -195,8 +196,11 @@ __global__ void __launch_bounds__(kThreads)
 gemv_kernel(GemvParams p)
 {
     __shared__ float red[kWaves * R];
+    const int block = (int)(blockIdx.y * gridDim.x + blockIdx.x);
+    if (block >= p.blocks)
+        return;
     const DeviceOps ops{red};
-    gemv_block<R, U>(ops, p, blockIdx.x, threadIdx.x);
+    gemv_block<R, U>(ops, p, block, threadIdx.x);
 }
 
 }  // namespace xgemv_dev

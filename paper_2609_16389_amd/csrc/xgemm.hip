@@ -24,6 +24,15 @@ struct xgemm_ctx {
     int cu_count;
     void *workspace;
     size_t ws_bytes;
+    // Every call that touches the workspace records ws_event on its stream
+    // after its last launch; a call on another stream first makes its stream
+    // wait for that event, so that calls sharing the workspace never overlap,
+    // whichever streams they are enqueued on.  The workspace is only freed
+    // (to grow it) once the event has completed.
+    hipEvent_t ws_event;
+    hipStream_t ws_stream;  // stream of the last recorded ws_event
+    bool ws_recorded;
+    size_t ws_limit;        // largest workspace the handle may allocate (0: no limit)
     char last_error[256];
 };
 
@@ -285,26 +294,40 @@ size_t workspace_bytes(int64_t M, int64_t N, int split)
     return (size_t)split * (size_t)M * (size_t)ldw * sizeof(float);
 }
 
-template <int BM, int BN, int BK, int WGM, int WGN>
-hipError_t launch_gemm(int dtype, const GemmParams &p, int grid, hipStream_t s)
+// Grid of `blocks` workgroups (blocks < 2^31): one dimension while the
+// launch has fewer than 2^32 threads at 1024 threads per workgroup, else
+// rows of 65536 workgroups (the kernels take the linear id and let the
+// workgroups past `blocks` exit).
+dim3 grid_of(int64_t blocks)
 {
+    constexpr int64_t kRow = 65536;
+    if (blocks < ((int64_t)1 << 22))
+        return dim3((unsigned)blocks);
+    return dim3((unsigned)kRow, (unsigned)cdiv(blocks, kRow));
+}
+
+template <int BM, int BN, int BK, int WGM, int WGN>
+hipError_t launch_gemm(int dtype, GemmParams p, int grid, hipStream_t s)
+{
+    p.grid = grid;
     if (dtype == XGEMM_BF16)
-        hipLaunchKernelGGL((xgemm_dev::gemm_kernel<BM, BN, BK, WGM, WGN, 0>), dim3(grid),
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel<BM, BN, BK, WGM, WGN, 0>), grid_of(grid),
                            dim3(WGM * WGN * 64), 0, s, p);
     else
-        hipLaunchKernelGGL((xgemm_dev::gemm_kernel<BM, BN, BK, WGM, WGN, 1>), dim3(grid),
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel<BM, BN, BK, WGM, WGN, 1>), grid_of(grid),
                            dim3(WGM * WGN * 64), 0, s, p);
     return hipGetLastError();
 }
 
 template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int MI>
-hipError_t launch_dma(int dtype, const GemmParams &p, int grid, hipStream_t s)
+hipError_t launch_dma(int dtype, GemmParams p, int grid, hipStream_t s)
 {
+    p.grid = grid;
     if (dtype == XGEMM_BF16)
-        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 0, MI>), dim3(grid),
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 0, MI>), grid_of(grid),
                            dim3(WGM * WGN * 64), 0, s, p);
     else
-        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 1, MI>), dim3(grid),
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 1, MI>), grid_of(grid),
                            dim3(WGM * WGN * 64), 0, s, p);
     return hipGetLastError();
 }
@@ -618,18 +641,33 @@ int make_plan_with(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, 
     return finish();
 }
 
-// Grow the handle's workspace to `bytes` (never shrinks).  The old one may
-// still be in use by work enqueued on this stream, so the stream is
-// synchronised before it is freed.
-int ensure_workspace(xgemm_ctx *h, size_t bytes, hipStream_t s)
+// Make the handle's workspace usable by work enqueued next on stream s and
+// at least `bytes` large (it never shrinks).  Work of earlier calls on other
+// streams that used the workspace is ordered before s's next work (a wait on
+// the handle's event); a buffer being replaced is freed only after that work
+// has completed.  Every caller enqueues its workspace users and then calls
+// release_workspace on the same stream.
+int acquire_workspace(xgemm_ctx *h, size_t bytes, hipStream_t s)
 {
+    hipError_t e;
+    if (h->ws_limit > 0 && bytes > h->ws_limit) {
+        snprintf(h->last_error, sizeof(h->last_error), "workspace of %zu bytes exceeds the handle's limit of %zu",
+                 bytes, h->ws_limit);
+        return XGEMM_ERR_ALLOC;
+    }
+    if (h->ws_recorded && h->ws_stream != s) {
+        e = hipStreamWaitEvent(s, h->ws_event, 0);
+        if (e != hipSuccess) {
+            set_error(h, "hipStreamWaitEvent", e);
+            return XGEMM_ERR_HIP;
+        }
+    }
     if (bytes <= h->ws_bytes)
         return XGEMM_OK;
-    hipError_t e;
     if (h->workspace) {
-        e = hipStreamSynchronize(s);
+        e = h->ws_recorded ? hipEventSynchronize(h->ws_event) : hipSuccess;
         if (e != hipSuccess) {
-            set_error(h, "hipStreamSynchronize", e);
+            set_error(h, "hipEventSynchronize", e);
             return XGEMM_ERR_HIP;
         }
         (void)hipFree(h->workspace);
@@ -644,6 +682,19 @@ int ensure_workspace(xgemm_ctx *h, size_t bytes, hipStream_t s)
         return XGEMM_ERR_ALLOC;
     }
     h->ws_bytes = bytes;
+    return XGEMM_OK;
+}
+
+// Mark the end of the workspace users just enqueued on stream s.
+int release_workspace(xgemm_ctx *h, hipStream_t s)
+{
+    const hipError_t e = hipEventRecord(h->ws_event, s);
+    if (e != hipSuccess) {
+        set_error(h, "hipEventRecord", e);
+        return XGEMM_ERR_HIP;
+    }
+    h->ws_stream = s;
+    h->ws_recorded = true;
     return XGEMM_OK;
 }
 
@@ -712,12 +763,18 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     rc = make_plan(M1, N1, K, A, lda, B, ldb, C, ldc, band.body, h->cu_count, &p1, true);
     if (rc == XGEMM_OK)
         rc = make_plan(M2, N2, K, A2, lda, B2, ldb, C2, ldc, band.band, h->cu_count, &p2, true);
-    if (rc == XGEMM_OK)
-        rc = ensure_workspace(h, p1.ws > p2.ws ? p1.ws : p2.ws, s);
-    if (rc == XGEMM_OK)
-        rc = launch_plan(h, p1, M1, N1, K, A, lda, B, ldb, C, ldc, dtype, s);
+    if (rc != XGEMM_OK)
+        return rc;
+    const size_t ws = p1.ws > p2.ws ? p1.ws : p2.ws;
+    if (ws > 0 && (rc = acquire_workspace(h, ws, s)) != XGEMM_OK)
+        return rc;
+    rc = launch_plan(h, p1, M1, N1, K, A, lda, B, ldb, C, ldc, dtype, s);
     if (rc == XGEMM_OK)
         rc = launch_plan(h, p2, M2, N2, K, A2, lda, B2, ldb, C2, ldc, dtype, s);
+    if (ws > 0) {
+        const int rc2 = release_workspace(h, s);
+        rc = rc == XGEMM_OK ? rc2 : rc;
+    }
     return rc;
 }
 
@@ -728,10 +785,15 @@ int run_one(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_
 {
     Plan plan;
     int rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan, true);
-    if (rc == XGEMM_OK)
-        rc = ensure_workspace(h, plan.ws, s);
-    if (rc == XGEMM_OK)
-        rc = launch_plan(h, plan, M, N, K, A, lda, B, ldb, C, ldc, dtype, s);
+    if (rc != XGEMM_OK)
+        return rc;
+    if (plan.ws > 0 && (rc = acquire_workspace(h, plan.ws, s)) != XGEMM_OK)
+        return rc;
+    rc = launch_plan(h, plan, M, N, K, A, lda, B, ldb, C, ldc, dtype, s);
+    if (plan.ws > 0) {
+        const int rc2 = release_workspace(h, s);
+        rc = rc == XGEMM_OK ? rc2 : rc;
+    }
     return rc;
 }
 
@@ -846,16 +908,21 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
         pk.a_off = 0;
         pk.b_off = (a_bytes + 255) / 256 * 256;
         const size_t ws = pk.b ? pk.b_off + (size_t)nb * (size_t)pk.k8 * (size_t)pk.n8 * 2 : a_bytes;
-        rc = ensure_workspace(h, ws, s);
+        if (packed.nseg != 1 || packed.seg[0].reduce != 0 || packed.seg[0].p.split != 1 ||
+            packed.seg[0].grid * batch > 0x7fffffff)
+            return XGEMM_ERR_INVALID_ARG;  // batched plans are single unsplit launches
+        rc = acquire_workspace(h, ws, s);
         if (rc != XGEMM_OK)
             return rc;
         char *const w = (char *)h->workspace;
-        if (pk.a && (e = launch_pack(A, lda, sa, M, K, w + pk.a_off, M, pk.k8, na, s)) != hipSuccess) {
+        e = hipSuccess;
+        if (pk.a && (e = launch_pack(A, lda, sa, M, K, w + pk.a_off, M, pk.k8, na, s)) != hipSuccess)
             set_error(h, "pack A launch", e);
-            return XGEMM_ERR_HIP;
-        }
-        if (pk.b && (e = launch_pack(B, ldb, sb, K, N, w + pk.b_off, pk.k8, pk.n8, nb, s)) != hipSuccess) {
+        if (e == hipSuccess && pk.b &&
+            (e = launch_pack(B, ldb, sb, K, N, w + pk.b_off, pk.k8, pk.n8, nb, s)) != hipSuccess)
             set_error(h, "pack B launch", e);
+        if (e != hipSuccess) {
+            (void)release_workspace(h, s);
             return XGEMM_ERR_HIP;
         }
         plan = packed;
@@ -884,11 +951,16 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
     g.p.vec_c = g.p.vec_c && (sc % 4 == 0);
     g.dma = dma_eligible(g.p, kTiles[plan.tile].bm, pk.b);
     e = launch_tile(plan.tile, g.dma, dtype, g.p, (int)(g.grid * batch), s);
+    rc = XGEMM_OK;
     if (e != hipSuccess) {
         set_error(h, "gemm launch", e);
-        return XGEMM_ERR_HIP;
+        rc = XGEMM_ERR_HIP;
     }
-    return XGEMM_OK;
+    if (pk.a || pk.b) {
+        const int rc2 = release_workspace(h, s);
+        rc = rc == XGEMM_OK ? rc2 : rc;
+    }
+    return rc;
 }
 
 // ---------------------------------------------------------------------------
@@ -969,7 +1041,10 @@ int check_gemv_args(int64_t M, int64_t K, const float *A, int64_t lda, const flo
     return XGEMM_OK;
 }
 
-GemvParams gemv_params(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y,
+// Launch parameters of a GEMV with `rows` rows per workgroup; blocks is 0
+// when the launch would exceed 2^31 - 1 workgroups (only possible with a
+// forced split of a very tall matrix), which callers reject.
+GemvParams gemv_params(int64_t M, int64_t K, const float *A, int64_t lda, const float *x, float *y, int rows,
                        int split_k, float *part)
 {
     GemvParams p;
@@ -984,6 +1059,8 @@ GemvParams gemv_params(int64_t M, int64_t K, const float *A, int64_t lda, const 
     p.split = gemv_split(K, split_k, &kc);
     p.k_chunk = (int)kc;
     p.vec = ((uintptr_t)A % 16 == 0) && ((uintptr_t)x % 16 == 0) && (lda % 4 == 0);
+    const int64_t blocks = cdiv(M, rows) * p.split;
+    p.blocks = blocks <= 0x7fffffff ? (int)blocks : 0;
     return p;
 }
 
@@ -1010,23 +1087,28 @@ int run_gemv(xgemm_ctx *h, int64_t M, int64_t K, const float *A, int64_t lda, co
             cfg = *forced;
         else
             select_gemv(M, K, h->cu_count, &cfg);
-        GemvParams p = gemv_params(M, K, A, lda, x, y, cfg.split_k, nullptr);
+        GemvParams p = gemv_params(M, K, A, lda, x, y, cfg.rows, cfg.split_k, nullptr);
+        if (p.blocks == 0)
+            return XGEMM_ERR_INVALID_ARG;
         if (p.split > 1) {
-            rc = ensure_workspace(h, (size_t)p.split * (size_t)M * sizeof(float), s);
+            rc = acquire_workspace(h, (size_t)p.split * (size_t)M * sizeof(float), s);
             if (rc != XGEMM_OK)
                 return rc;
             p.part = (float *)h->workspace;
         }
         with_gemv_config(cfg, [&](auto r, auto u) {
             constexpr int R = decltype(r)::value, U = decltype(u)::value;
-            hipLaunchKernelGGL((xgemv_dev::gemv_kernel<R, U>), dim3((unsigned)(cdiv(M, R) * p.split)),
-                               dim3(xgemv_dev::kThreads), 0, s, p);
+            hipLaunchKernelGGL((xgemv_dev::gemv_kernel<R, U>), grid_of(p.blocks), dim3(xgemv_dev::kThreads), 0, s,
+                               p);
             return 0;
         });
         if (p.split > 1) {
             const int grid = (int)(cdiv(M, 256) < 1024 ? cdiv(M, 256) : 1024);
             hipLaunchKernelGGL(xgemv_dev::gemv_reduce, dim3(grid), dim3(256), 0, s, (const float *)p.part,
                                p.split, (int)M, y);
+            const int rc2 = release_workspace(h, s);
+            if (rc2 != XGEMM_OK)
+                return rc2;
         }
     }
     const hipError_t e = hipGetLastError();
@@ -1203,7 +1285,15 @@ int xgemm_create(xgemm_handle_t *out)
     h->cu_count = prop.multiProcessorCount;
     h->workspace = nullptr;
     h->ws_bytes = 0;
+    h->ws_stream = nullptr;
+    h->ws_recorded = false;
+    h->ws_limit = 0;
     h->last_error[0] = '\0';
+    if (hipEventCreateWithFlags(&h->ws_event, hipEventDisableTiming) != hipSuccess) {
+        (void)hipGetLastError();
+        delete h;
+        return XGEMM_ERR_HIP;
+    }
     *out = h;
     return XGEMM_OK;
 }
@@ -1217,8 +1307,20 @@ int xgemm_destroy(xgemm_handle_t h)
         (void)hipGetLastError();
         rc = XGEMM_ERR_HIP;
     }
+    if (hipEventDestroy(h->ws_event) != hipSuccess) {
+        (void)hipGetLastError();
+        rc = XGEMM_ERR_HIP;
+    }
     delete h;
     return rc;
+}
+
+int xgemm_set_workspace_limit(xgemm_handle_t h, size_t bytes)
+{
+    if (!h)
+        return XGEMM_ERR_INVALID_ARG;
+    h->ws_limit = bytes;
+    return XGEMM_OK;
 }
 
 int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
@@ -1429,8 +1531,8 @@ int xgemv_trace_workgroup(int64_t M, int64_t K, const float *A, int64_t lda, con
     if (!counts || capacity < 0 || (capacity > 0 && !out) || !valid_gemv_config(cfg) || M <= 0 || K <= 0 ||
         check_gemv_args(M, K, A, lda, x, y) != XGEMM_OK)
         return XGEMM_ERR_INVALID_ARG;
-    const GemvParams p = gemv_params(M, K, A, lda, x, y, cfg->split_k, W);
-    if (block < 0 || block >= cdiv(M, cfg->rows) * p.split || (p.split > 1 && !W))
+    const GemvParams p = gemv_params(M, K, A, lda, x, y, cfg->rows, cfg->split_k, W);
+    if (p.blocks == 0 || block < 0 || block >= p.blocks || (p.split > 1 && !W))
         return XGEMM_ERR_INVALID_ARG;
     return with_gemv_config(*cfg, [&](auto r, auto u) {
         constexpr int R = decltype(r)::value, U = decltype(u)::value;

@@ -117,6 +117,8 @@ lib.xgemm_create.argtypes = [ctypes.POINTER(_handle_t)]
 lib.xgemm_create.restype = _i32
 lib.xgemm_destroy.argtypes = [_handle_t]
 lib.xgemm_destroy.restype = _i32
+lib.xgemm_set_workspace_limit.argtypes = [_handle_t, ctypes.c_size_t]
+lib.xgemm_set_workspace_limit.restype = _i32
 lib.xgemm_run.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p]
 lib.xgemm_run.restype = _i32
 lib.xgemm_run_config.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p,
@@ -178,6 +180,10 @@ def xgemm_create() -> int:
 
 def xgemm_destroy(h) -> int:
     return lib.xgemm_destroy(h)
+
+
+def xgemm_set_workspace_limit(h, nbytes) -> int:
+    return lib.xgemm_set_workspace_limit(h, nbytes)
 
 
 def xgemm_run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream) -> int:
@@ -300,16 +306,31 @@ def xgemm_last_error(h) -> str:
 _handles = {}
 
 
-def handle(device_index: int | None = None):
-    """A per-device handle owned by this module (created on first use)."""
+def _stream_ptr(stream) -> int:
+    """The hipStream_t address of a torch stream, a raw address or None (the
+    null stream)."""
+    if stream is None:
+        return 0
+    return int(getattr(stream, "cuda_stream", stream) or 0)
+
+
+def handle(device_index: int | None = None, stream=None):
+    """The handle this module owns for (device, stream), created on first use.
+
+    A handle's workspace (split-k partials, operand copies) belongs to one
+    stream at a time: the library orders calls that share it across streams
+    after each other, so one handle per stream is what lets calls on
+    different streams run concurrently.  ``stream`` is a torch stream, a raw
+    hipStream_t address or None (the null stream)."""
     import torch
     if device_index is None:
         device_index = torch.cuda.current_device()
-    h = _handles.get(device_index)
+    key = (device_index, _stream_ptr(stream))
+    h = _handles.get(key)
     if h is None:
         with torch.cuda.device(device_index):
             h = xgemm_create()
-        _handles[device_index] = h
+        _handles[key] = h
     return h
 
 
@@ -355,7 +376,7 @@ def bmm(A, B, out=None, stream=None):
         if t.shape[2] > 1 and t.stride(2) != 1:
             raise ValueError("rows must be contiguous")
     s = stream if stream is not None else torch.cuda.current_stream(A.device)
-    h = handle(A.device.index)
+    h = handle(A.device.index, s)
     lda = A.stride(1) if M > 1 else max(K, 1)
     ldb = B.stride(1) if K > 1 else max(N, 1)
     ldc = out.stride(1) if M > 1 else max(N, 1)
@@ -389,7 +410,7 @@ def gemm(A, B, out=None, config: xgemm_config | None = None, stream=None):
     if out.dtype != torch.float32 or tuple(out.shape) != (M, N) or out.device != A.device:
         raise ValueError("out must be a float32 (M, N) tensor on A's device")
     s = stream if stream is not None else torch.cuda.current_stream(A.device)
-    h = handle(A.device.index)
+    h = handle(A.device.index, s)
     args = (h, M, N, K, A.data_ptr() or None, _ld(A), B.data_ptr() or None, _ld(B),
             out.data_ptr() or None, _ld(out), dtype, s.cuda_stream)
     if config is None:
@@ -420,9 +441,10 @@ def gemv(A, x, out=None, config: xgemv_config | None = None, stream=None):
     elif out.dtype != torch.float32 or out.shape != (M,) or not out.is_contiguous():
         raise ValueError("out must be a contiguous float32 vector of %d values" % M)
     if stream is None:
-        stream = torch.cuda.current_stream(A.device).cuda_stream
-    h = handle(A.device.index)
-    args = (h, M, K, A.data_ptr() or None, lda, x.data_ptr() or None, out.data_ptr() or None, stream)
+        stream = torch.cuda.current_stream(A.device)
+    h = handle(A.device.index, stream)
+    args = (h, M, K, A.data_ptr() or None, lda, x.data_ptr() or None, out.data_ptr() or None,
+            _stream_ptr(stream) or None)
     rc = xgemv_run_config(*args, config) if config is not None else xgemv_run(*args)
     if rc != XGEMM_OK:
         raise XgemmError(rc, xgemm_last_error(h))

@@ -191,18 +191,18 @@ def test_gemv_null_handle_and_trace_arguments():
 
 
 def test_sweep_candidates_host_logic():
-    """The selector sweep (a GPU tool) enumerates configurations on the host:
-    the selector's choice is always timed, splits shorter than 3 K steps and
-    launches above the workgroup cap are left out."""
-    from paper_2609_16389_amd import sweep
-    c = sweep.candidates(1024, 1024, 65536, (1, 8))
+    """The selector sweep (bench.py --sweep, a GPU measurement) enumerates
+    configurations on the host: the selector's choice is always timed, splits
+    shorter than 3 K steps and launches above the workgroup cap are left out."""
+    import bench
+    c = bench.sweep_candidates(1024, 1024, 65536, (1, 8), xg)
     assert (1, 8) in c and (0, 1) in c and (2, 16) in c and len(c) == len(set(c))
-    small = sweep.candidates(256, 256, 256, (2, 1))
+    small = bench.sweep_candidates(256, 256, 256, (2, 1), xg)
     assert all(s == 1 for _, s in small)          # K = 256: every split would be under 3 steps
-    big = sweep.candidates(16384, 16384, 4096, (0, 1))
+    big = bench.sweep_candidates(16384, 16384, 4096, (0, 1), xg)
     for t, s in big:
         bm, bn, _, _ = xg.xgemm_tile_info(t)
-        assert (16384 // bm) * (16384 // bn) * s <= sweep.MAX_WORKGROUPS or (t, s) == (0, 1)
+        assert (16384 // bm) * (16384 // bn) * s <= bench.SWEEP_MAX_WORKGROUPS or (t, s) == (0, 1)
 
 
 def test_packed_plan_layout():

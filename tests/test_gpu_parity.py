@@ -364,31 +364,99 @@ def test_invalid_arguments_on_gpu():
 
 
 def test_workspace_allocation_failure():
-    """A call whose operand copies would need about 4 TiB of workspace fails
-    with XGEMM_ERR_ALLOC before anything is enqueued, and the handle stays
-    usable.  (The pointers are never dereferenced: no kernel is launched.)"""
+    """A call whose workspace would exceed the handle's limit fails with
+    XGEMM_ERR_ALLOC before anything is enqueued (C untouched), calls that
+    need no workspace still run, and the handle is usable once the limit is
+    lifted.  All buffers are sized for the calls made."""
     h = xg.xgemm_create()
     try:
-        A = torch.zeros((16, 16), dtype=torch.bfloat16, device="cuda")
-        C = torch.full((16, 16), 7.0, dtype=torch.float32, device="cuda")
+        M, N, K = 256, 256, 1024
+        Ab, Bb, C_ref, S = _case(M, N, K, "bf16", seed=90)
+        Ad, Bd = to_device(Ab, "bf16"), to_device(Bb, "bf16")
+        C = torch.full((M, N), 7.0, dtype=torch.float32, device="cuda")
         s = torch.cuda.current_stream().cuda_stream
-        big = (1 << 20) + 1           # K and N odd: both operands would be copied
-        need = xg.xgemm_workspace_bytes(1 << 20, big, big, 256, xg.xgemm_select_config(1 << 20, big, big, 0, 256))
-        assert need > 1 << 41
-        rc = xg.xgemm_run(h, 1 << 20, big, big, A.data_ptr(), big, A.data_ptr(), big, C.data_ptr(), big, 0, s)
+        split4 = config(xg.XGEMM_TILE_128x128, 4)
+        assert xg.xgemm_workspace_bytes(M, N, K, 256, split4) == 4 * M * N * 4
+        assert xg.xgemm_set_workspace_limit(h, 4096) == xg.XGEMM_OK
+        assert xg.xgemm_set_workspace_limit(None, 4096) == xg.XGEMM_ERR_INVALID_ARG
+        rc = xg.xgemm_run_config(h, M, N, K, Ad.data_ptr(), K, Bd.data_ptr(), N, C.data_ptr(), N, 0, s, split4)
         assert rc == xg.XGEMM_ERR_ALLOC
         assert "workspace" in xg.xgemm_last_error(h)
         torch.cuda.synchronize()
         assert torch.all(C == 7.0)
-        # still usable
-        Ab, Bb, C_ref, S = _case(100, 101, 103, "bf16", seed=90)
-        Ad, Bd = to_device(Ab, "bf16"), to_device(Bb, "bf16")
-        out = torch.empty((100, 101), dtype=torch.float32, device="cuda")
-        assert xg.xgemm_run(h, 100, 101, 103, Ad.data_ptr(), 103, Bd.data_ptr(), 101, out.data_ptr(), 101, 0,
-                            s) == xg.XGEMM_OK
+        # an unsplit aligned call needs no workspace
+        assert xg.xgemm_run_config(h, M, N, K, Ad.data_ptr(), K, Bd.data_ptr(), N, C.data_ptr(), N, 0, s,
+                                   config(xg.XGEMM_TILE_128x128, 1)) == xg.XGEMM_OK
         torch.cuda.synchronize()
-        check_close(out.cpu().numpy(), C_ref, S, "after an allocation failure")
+        check_close(C.cpu().numpy(), C_ref, S, "unsplit under a workspace limit")
+        # lifted: the split call runs
+        C.fill_(7.0)
+        assert xg.xgemm_set_workspace_limit(h, 0) == xg.XGEMM_OK
+        assert xg.xgemm_run_config(h, M, N, K, Ad.data_ptr(), K, Bd.data_ptr(), N, C.data_ptr(), N, 0, s,
+                                   split4) == xg.XGEMM_OK
+        torch.cuda.synchronize()
+        check_close(C.cpu().numpy(), C_ref, S, "after an allocation failure")
     finally:
+        xg.xgemm_destroy(h)
+
+
+def _two_stream_cases():
+    """Two calls that both use a workspace: a forced 4-way K split (partials
+    in the workspace) and a packed B (N odd: B copied into the workspace)."""
+    split = (512, 512, 4096, config(xg.XGEMM_TILE_128x128, 4), 71)
+    packed = (1000, 1001, 1024, None, 72)
+    out = []
+    for M, N, K, cfg, seed in (split, packed):
+        A, B, C_ref, S = _case(M, N, K, "bf16", seed=seed)
+        out.append((M, N, K, cfg, to_device(A, "bf16"), to_device(B, "bf16"), C_ref, S))
+    return out
+
+
+def test_two_streams_own_handles_concurrent():
+    """Split-k and packed-operand calls through gemm() on two torch streams
+    at once, several rounds without synchronisation in between: the binding
+    keys its handles on (device, stream), so each stream writes its own
+    workspace.  Every result matches the oracle elementwise."""
+    cases = _two_stream_cases()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[torch.full((M, N), float("nan"), device="cuda") for (M, N, *_ ) in cases] for _ in streams]
+    torch.cuda.synchronize()
+    assert xg.handle(0, streams[0]) != xg.handle(0, streams[1])
+    for _ in range(4):
+        for si, st in enumerate(streams):
+            with torch.cuda.stream(st):
+                for ci, (M, N, K, cfg, dA, dB, _, _) in enumerate(cases):
+                    xg.gemm(dA, dB, out=outs[si][ci], config=cfg, stream=st)
+    torch.cuda.synchronize()
+    for si in range(2):
+        for ci, (M, N, K, cfg, dA, dB, C_ref, S) in enumerate(cases):
+            check_close(outs[si][ci].cpu().numpy(), C_ref, S, "stream %d case %d" % (si, ci))
+
+
+def test_two_streams_share_one_handle():
+    """The same calls through one C handle on two streams, enqueued without
+    synchronisation: the handle makes each workspace user wait for the last
+    one on the other stream, so the shared workspace is never written by two
+    calls at once.  Every result matches the oracle elementwise."""
+    cases = _two_stream_cases()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    h = xg.xgemm_create()
+    try:
+        outs = [[torch.full((M, N), float("nan"), device="cuda") for (M, N, *_ ) in cases] for _ in streams]
+        torch.cuda.synchronize()
+        for _ in range(4):
+            for ci, (M, N, K, cfg, dA, dB, _, _) in enumerate(cases):
+                for si, st in enumerate(streams):
+                    args = (h, M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, outs[si][ci].data_ptr(), N,
+                            xg.XGEMM_BF16, st.cuda_stream)
+                    rc = xg.xgemm_run(*args) if cfg is None else xg.xgemm_run_config(*args, cfg)
+                    assert rc == xg.XGEMM_OK, xg.xgemm_last_error(h)
+        torch.cuda.synchronize()
+        for si in range(2):
+            for ci, (M, N, K, cfg, dA, dB, C_ref, S) in enumerate(cases):
+                check_close(outs[si][ci].cpu().numpy(), C_ref, S, "shared handle, stream %d case %d" % (si, ci))
+    finally:
+        torch.cuda.synchronize()
         xg.xgemm_destroy(h)
 
 
