@@ -712,13 +712,88 @@ hipError_t launch_pack(const void *src, int64_t ld, int64_t src_stride, int64_t 
     return hipGetLastError();
 }
 
-int run_one(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
-            int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s, const xgemm_config &cfg);
-int launch_plan(xgemm_ctx *h, Plan plan, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+int launch_plan(xgemm_ctx *h, Plan plan, char *ws, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
                 const void *B, int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s);
 
+// The launches of one call: one plan over all of C, or (xgemm_run's body +
+// band plans) two plans on sub-matrices, run one after the other.  ws is
+// the workspace the larger of them needs.
+struct CallPlan {
+    int parts = 0;
+    Plan plan[2];
+    int64_t M[2], N[2];
+    const void *A[2];
+    const void *B[2];
+    float *C[2];
+    size_t ws = 0;
+};
+
+// Plan a call with K > 0 and M, N > 0 (arguments already checked): the
+// forced configuration, or the selected plan, banded or not.  Touches no
+// GPU.
+int plan_call(int cu_count, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
+              float *C, int64_t ldc, const xgemm_config *forced, CallPlan *cp)
+{
+    BandPlan band;
+    if (forced) {
+        band.body = *forced;
+    } else {
+        band = select_band(M, N, K, cu_count);
+    }
+    if (band.axis == XGEMM_BAND_NONE) {
+        cp->parts = 1;
+        cp->M[0] = M, cp->N[0] = N, cp->A[0] = A, cp->B[0] = B, cp->C[0] = C;
+    } else {
+        // body, then band: ordinary calls on sub-matrices of A, B and C
+        const int64_t ext = band.extent;
+        const bool cols = band.axis == XGEMM_BAND_COLUMNS;
+        cp->parts = 2;
+        cp->M[0] = cols ? M : ext, cp->N[0] = cols ? ext : N;
+        cp->M[1] = cols ? M : M - ext, cp->N[1] = cols ? N - ext : N;
+        cp->A[0] = A, cp->B[0] = B, cp->C[0] = C;
+        cp->A[1] = cols ? A : (const void *)((const char *)A + 2 * ext * lda);
+        cp->B[1] = cols ? (const void *)((const char *)B + 2 * ext) : B;
+        cp->C[1] = cols ? C + ext : C + ext * ldc;
+    }
+    cp->ws = 0;
+    for (int i = 0; i < cp->parts; ++i) {
+        const int rc = make_plan(cp->M[i], cp->N[i], K, cp->A[i], lda, cp->B[i], ldb, cp->C[i], ldc,
+                                 i == 0 ? band.body : band.band, cu_count, &cp->plan[i], true);
+        if (rc != XGEMM_OK)
+            return rc;
+        cp->ws = cp->plan[i].ws > cp->ws ? cp->plan[i].ws : cp->ws;
+    }
+    return XGEMM_OK;
+}
+
+// Enqueue every launch of a planned call, the workspace (cp.ws bytes, or
+// unused when 0) at ws.
+int launch_call(xgemm_ctx *h, const CallPlan &cp, char *ws, int64_t K, int64_t lda, int64_t ldb, int64_t ldc,
+                int dtype, hipStream_t s)
+{
+    int rc = XGEMM_OK;
+    for (int i = 0; i < cp.parts && rc == XGEMM_OK; ++i)
+        rc = launch_plan(h, cp.plan[i], ws, cp.M[i], cp.N[i], K, cp.A[i], lda, cp.B[i], ldb, cp.C[i], ldc, dtype, s);
+    return rc;
+}
+
+// The K == 0 product: C[0:M, 0:N] = 0.
+int launch_zero(xgemm_ctx *h, int64_t M, int64_t N, float *C, int64_t ldc, hipStream_t s)
+{
+    const int64_t n = M * N;
+    const int grid = (int)(cdiv(n, 256) < 4096 ? cdiv(n, 256) : 4096);
+    hipLaunchKernelGGL(xgemm_dev::fill_zero, dim3(grid), dim3(256), 0, s, C, ldc, (int)M, (int)N);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+        set_error(h, "fill_zero launch", e);
+        return XGEMM_ERR_HIP;
+    }
+    return XGEMM_OK;
+}
+
 // A call of xgemm_run (forced == nullptr: the selected plan, banded or not)
-// or xgemm_run_config (one launch plan with the forced configuration).
+// or xgemm_run_config (one launch plan with the forced configuration).  All
+// parts are planned and the workspace grown before anything is enqueued.
 int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
         int64_t ldb, float *C, int64_t ldc, int dtype, void *stream, const xgemm_config *forced)
 {
@@ -731,66 +806,16 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     hipStream_t s = (hipStream_t)stream;
     if (M == 0 || N == 0)
         return XGEMM_OK;
-    hipError_t e;
-    if (K == 0) {
-        const int64_t n = M * N;
-        const int grid = (int)(cdiv(n, 256) < 4096 ? cdiv(n, 256) : 4096);
-        hipLaunchKernelGGL(xgemm_dev::fill_zero, dim3(grid), dim3(256), 0, s, C, ldc, (int)M, (int)N);
-        e = hipGetLastError();
-        if (e != hipSuccess) {
-            set_error(h, "fill_zero launch", e);
-            return XGEMM_ERR_HIP;
-        }
-        return XGEMM_OK;
-    }
-
-    if (forced)
-        return run_one(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, s, *forced);
-    const BandPlan band = select_band(M, N, K, h->cu_count);
-    if (band.axis == XGEMM_BAND_NONE)
-        return run_one(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, s, band.body);
-    // body, then band: two ordinary calls on sub-matrices of A, B and C,
-    // ordered on the stream (they share the workspace).  Both are planned
-    // and the workspace grown before anything is enqueued.
-    const int64_t ext = band.extent;
-    const bool cols = band.axis == XGEMM_BAND_COLUMNS;
-    const int64_t M1 = cols ? M : ext, N1 = cols ? ext : N;
-    const int64_t M2 = cols ? M : M - ext, N2 = cols ? N - ext : N;
-    const void *A2 = cols ? A : (const void *)((const char *)A + 2 * ext * lda);
-    const void *B2 = cols ? (const void *)((const char *)B + 2 * ext) : B;
-    float *C2 = cols ? C + ext : C + ext * ldc;
-    Plan p1, p2;
-    rc = make_plan(M1, N1, K, A, lda, B, ldb, C, ldc, band.body, h->cu_count, &p1, true);
-    if (rc == XGEMM_OK)
-        rc = make_plan(M2, N2, K, A2, lda, B2, ldb, C2, ldc, band.band, h->cu_count, &p2, true);
+    if (K == 0)
+        return launch_zero(h, M, N, C, ldc, s);
+    CallPlan cp;
+    rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, forced, &cp);
     if (rc != XGEMM_OK)
         return rc;
-    const size_t ws = p1.ws > p2.ws ? p1.ws : p2.ws;
-    if (ws > 0 && (rc = acquire_workspace(h, ws, s)) != XGEMM_OK)
+    if (cp.ws > 0 && (rc = acquire_workspace(h, cp.ws, s)) != XGEMM_OK)
         return rc;
-    rc = launch_plan(h, p1, M1, N1, K, A, lda, B, ldb, C, ldc, dtype, s);
-    if (rc == XGEMM_OK)
-        rc = launch_plan(h, p2, M2, N2, K, A2, lda, B2, ldb, C2, ldc, dtype, s);
-    if (ws > 0) {
-        const int rc2 = release_workspace(h, s);
-        rc = rc == XGEMM_OK ? rc2 : rc;
-    }
-    return rc;
-}
-
-// One planned call (K > 0, M, N > 0, arguments already checked) with
-// configuration cfg.
-int run_one(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B,
-            int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s, const xgemm_config &cfg)
-{
-    Plan plan;
-    int rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, h->cu_count, &plan, true);
-    if (rc != XGEMM_OK)
-        return rc;
-    if (plan.ws > 0 && (rc = acquire_workspace(h, plan.ws, s)) != XGEMM_OK)
-        return rc;
-    rc = launch_plan(h, plan, M, N, K, A, lda, B, ldb, C, ldc, dtype, s);
-    if (plan.ws > 0) {
+    rc = launch_call(h, cp, (char *)h->workspace, K, lda, ldb, ldc, dtype, s);
+    if (cp.ws > 0) {
         const int rc2 = release_workspace(h, s);
         rc = rc == XGEMM_OK ? rc2 : rc;
     }
@@ -799,12 +824,11 @@ int run_one(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_
 
 // Enqueue a plan whose workspace is in place: operand copies, the GEMM
 // launches and their split-k reductions.
-int launch_plan(xgemm_ctx *h, Plan plan, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+int launch_plan(xgemm_ctx *h, Plan plan, char *ws, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
                 const void *B, int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s)
 {
     hipError_t e;
     // operand copies for the pipelined kernels
-    char *const ws = (char *)h->workspace;
     const Pack &pk = plan.pack;
     if (pk.a && (e = launch_pack(A, lda, 0, M, K, ws + pk.a_off, M, pk.k8, 1, s)) != hipSuccess) {
         set_error(h, "pack A launch", e);
@@ -823,7 +847,7 @@ int launch_plan(xgemm_ctx *h, Plan plan, int64_t M, int64_t N, int64_t K, const 
         if (pk.b)
             g.p.B = (const uint16_t *)(ws + pk.b_off);
         if (g.reduce)
-            g.p.C = (float *)h->workspace;
+            g.p.C = (float *)ws;
         e = launch_tile(plan.tile, g.dma, dtype, g.p, (int)g.grid, s);
         if (e != hipSuccess) {
             set_error(h, "gemm launch", e);
@@ -833,7 +857,7 @@ int launch_plan(xgemm_ctx *h, Plan plan, int64_t M, int64_t N, int64_t K, const 
             const int64_t nvec = M * cdiv(N, 4);
             const int grid = (int)(cdiv(nvec, 256) < 8192 ? cdiv(nvec, 256) : 8192);
             hipLaunchKernelGGL(xgemm_dev::splitk_reduce, dim3(grid), dim3(256), 0, s,
-                               (const float *)h->workspace, (int64_t)(M * plan.ldw), plan.ldw, g.p.split, C,
+                               (const float *)ws, (int64_t)(M * plan.ldw), plan.ldw, g.p.split, C,
                                ldc, (int)M, (int)N, vec_c);
         } else if (g.reduce == 2) {
             e = launch_tile_reduce(plan.tile, g.p, C, ldc, vec_c, s);
