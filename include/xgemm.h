@@ -141,6 +141,27 @@ int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
               float *C, int64_t ldc, int dtype, void *stream);
 
 /*
+ * For callers that cannot allocate device memory: code being captured into
+ * a HIP graph, tight serving loops, harnesses that forbid hipMalloc.  The
+ * same product as xgemm_run, with the same plan, kernels and arguments, and
+ * the same result bit for bit, but the split-k partials and operand copies
+ * live in a static array of the library (XGEMM_NOALLOC_SCRATCH_BYTES per
+ * GPU, held from the first xgemm_create on that GPU until the process ends)
+ * instead of the handle's workspace.  The call allocates nothing and frees
+ * nothing; nothing in the array needs to start at zero.  Every call of this
+ * entry point on one GPU shares that GPU's array, so calls that overlap in
+ * time on one GPU (on different streams, or through different handles) race
+ * and must be ordered by the caller.  Returns XGEMM_ERR_INVALID_ARG, with
+ * nothing enqueued and the reason in xgemm_last_error, when the call needs
+ * more than XGEMM_NOALLOC_SCRATCH_BYTES of scratch (a split-k plan or
+ * operand copies too large for it); other errors as xgemm_run.
+ */
+#define XGEMM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int xgemm_run_noalloc(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
+                      const void *A, int64_t lda, const void *B, int64_t ldb,
+                      float *C, int64_t ldc, int dtype, void *stream);
+
+/*
  * As xgemm_run, with the launch configuration forced to *cfg (validated:
  * XGEMM_ERR_INVALID_ARG for an unknown tile, split_k, group_m or tail_split
  * out of range, or tail_split > 1 together with split_k > 1).  Results agree

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <type_traits>
 #include <vector>
@@ -18,6 +19,20 @@
 #include "pack_kernel.hpp"
 
 using xgemm_dev::GemmParams;
+
+// Scratch of xgemm_run_noalloc: split-k partials and operand copies of the
+// calls that may not allocate.  One array per GPU, held by the code object
+// until the process ends; every such call on a GPU uses the same one.  Host
+// code never passes this name to a kernel or a copy: the device address of
+// each GPU's array comes from hipGetSymbolAddress (see xgemm_create).
+constexpr size_t kScratchBytes = XGEMM_NOALLOC_SCRATCH_BYTES;
+static __device__ __attribute__((aligned(256))) char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];  // device address of `scratch` on each device (null until looked up)
+}  // namespace
 
 struct xgemm_ctx {
     int device;
@@ -33,6 +48,7 @@ struct xgemm_ctx {
     hipStream_t ws_stream;  // stream of the last recorded ws_event
     bool ws_recorded;
     size_t ws_limit;        // largest workspace the handle may allocate (0: no limit)
+    void *scratch;          // this device's `scratch` array (xgemm_run_noalloc)
     char last_error[256];
 };
 
@@ -1313,6 +1329,22 @@ int xgemm_create(xgemm_handle_t *out)
     h->ws_recorded = false;
     h->ws_limit = 0;
     h->last_error[0] = '\0';
+    h->scratch = nullptr;
+    if (dev >= 0 && dev < kMaxDevices) {
+        // once per device, with the device current: the address of this
+        // device's copy of the scratch array
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        if (!g_scratch_ptr[dev]) {
+            void *ptr = nullptr;
+            if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+                (void)hipGetLastError();
+                delete h;
+                return XGEMM_ERR_HIP;
+            }
+            g_scratch_ptr[dev] = ptr;
+        }
+        h->scratch = g_scratch_ptr[dev];
+    }
     if (hipEventCreateWithFlags(&h->ws_event, hipEventDisableTiming) != hipSuccess) {
         (void)hipGetLastError();
         delete h;
@@ -1351,6 +1383,34 @@ int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K, const void *A, 
               const void *B, int64_t ldb, float *C, int64_t ldc, int dtype, void *stream)
 {
     return run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream, nullptr);
+}
+
+int xgemm_run_noalloc(xgemm_handle_t h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
+                      const void *B, int64_t ldb, float *C, int64_t ldc, int dtype, void *stream)
+{
+    int rc = check_args(h, M, N, K, A, lda, B, ldb, C, ldc, dtype);
+    if (rc != XGEMM_OK)
+        return rc;
+    h->last_error[0] = '\0';
+    if (!h->scratch) {
+        snprintf(h->last_error, sizeof(h->last_error), "no scratch array on device %d", h->device);
+        return XGEMM_ERR_UNSUPPORTED;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    if (M == 0 || N == 0)
+        return XGEMM_OK;
+    if (K == 0)
+        return launch_zero(h, M, N, C, ldc, s);
+    CallPlan cp;
+    rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, nullptr, &cp);
+    if (rc != XGEMM_OK)
+        return rc;
+    if (cp.ws > kScratchBytes) {
+        snprintf(h->last_error, sizeof(h->last_error),
+                 "the call needs %zu bytes of scratch, above the static maximum of %zu", cp.ws, kScratchBytes);
+        return XGEMM_ERR_INVALID_ARG;
+    }
+    return launch_call(h, cp, (char *)h->scratch, K, lda, ldb, ldc, dtype, s);
 }
 
 int xgemm_run_config(xgemm_handle_t h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,

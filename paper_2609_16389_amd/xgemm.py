@@ -121,6 +121,8 @@ lib.xgemm_set_workspace_limit.argtypes = [_handle_t, ctypes.c_size_t]
 lib.xgemm_set_workspace_limit.restype = _i32
 lib.xgemm_run.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p]
 lib.xgemm_run.restype = _i32
+lib.xgemm_run_noalloc.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p]
+lib.xgemm_run_noalloc.restype = _i32
 lib.xgemm_run_config.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p,
                                  ctypes.POINTER(xgemm_config)]
 lib.xgemm_run_config.restype = _i32
@@ -188,6 +190,13 @@ def xgemm_set_workspace_limit(h, nbytes) -> int:
 
 def xgemm_run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream) -> int:
     return lib.xgemm_run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream)
+
+
+def xgemm_run_noalloc(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream) -> int:
+    return lib.xgemm_run_noalloc(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream)
+
+
+XGEMM_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 def xgemm_run_config(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream, cfg) -> int:
