@@ -348,8 +348,12 @@ def sweep_shape(M: int, N: int, K: int, dtype: str = "bf16", rounds: int = 5) ->
                 raise xg.XgemmError(rc)
         call_band()
         runs.append(("band", call_band))
-    for tile, split in sweep_candidates(M, N, K, (sel.tile, sel.split_k), xg):
-        cfg = xg.xgemm_config(tile=tile, split_k=split, group_m=sel.group_m, tail_split=0)
+    cands = [(t, sp, 0) for t, sp in sweep_candidates(M, N, K, (sel.tile, sel.split_k), xg)]
+    sk = xg.xgemm_config(tile=xg.XGEMM_TILE_256x256, split_k=1, group_m=sel.group_m, stream_k=1)
+    if xg.xgemm_kernel_family(M, N, K, A.data_ptr(), K, B.data_ptr(), N, sk) == xg.XGEMM_KERNEL_PERSISTENT:
+        cands.append((xg.XGEMM_TILE_256x256, 1, 1))
+    for tile, split, stream_k in cands:
+        cfg = xg.xgemm_config(tile=tile, split_k=split, group_m=sel.group_m, stream_k=stream_k)
 
         def call(cfg=cfg):
             rc = xg.xgemm_run_config(h, M, N, K, A.data_ptr(), K, B.data_ptr(), N, C.data_ptr(), N, code,
@@ -357,7 +361,7 @@ def sweep_shape(M: int, N: int, K: int, dtype: str = "bf16", rounds: int = 5) ->
             if rc != xg.XGEMM_OK:
                 raise xg.XgemmError(rc)
         call()
-        runs.append(((tile, split), call))
+        runs.append(("sk" if stream_k else (tile, split), call))
     torch.cuda.synchronize()
     reps = max(3, min(50, int(2e8 / max(1.0, 2.0 * M * N * K / 1e3))))
     times: dict = {k: [] for k, _ in runs}
@@ -374,12 +378,12 @@ def sweep_shape(M: int, N: int, K: int, dtype: str = "bf16", rounds: int = 5) ->
             times[key].append(e0.elapsed_time(e1) / reps * 1e3)
     med = {k: statistics.median(v) for k, v in times.items()}
     best = min(med, key=med.get)
-    chosen = "band" if band.axis != xg.XGEMM_BAND_NONE else (sel.tile, sel.split_k)
-    name = lambda k: k if k == "band" else list(k)
+    chosen = "band" if band.axis != xg.XGEMM_BAND_NONE else ("sk" if sel.stream_k else (sel.tile, sel.split_k))
+    name = lambda k: k if isinstance(k, str) else list(k)
     out = {"shape": [M, N, K], "dtype": dtype, "selected": name(chosen), "selected_us": round(med[chosen], 2),
            "best": name(best), "best_us": round(med[best], 2), "loss": round(med[chosen] / med[best], 3),
-           "all_us": {(k if k == "band" else "%d:%d" % k): round(v, 1)
-                      for k, v in sorted(med.items(), key=lambda kv: (kv[0] == "band", str(kv[0])))}}
+           "all_us": {(k if isinstance(k, str) else "%d:%d" % k): round(v, 1)
+                      for k, v in sorted(med.items(), key=lambda kv: (isinstance(kv[0], str), str(kv[0])))}}
     if band.axis != xg.XGEMM_BAND_NONE:
         out["band"] = {"axis": "columns" if band.axis == xg.XGEMM_BAND_COLUMNS else "rows",
                        "body_extent": band.extent, "body": [band.body.tile, band.body.split_k],

@@ -73,9 +73,14 @@ typedef struct xgemm_config {
     int32_t tile;       /* an xgemm_tile value */
     int32_t split_k;    /* number of K partitions, 1 .. 64; > 1 uses the workspace */
     int32_t group_m;    /* tile rows per group in the launch order, 1 .. 64 (L2 locality) */
-    int32_t tail_split; /* 0 or 1: off; 2 .. 64 (only with split_k == 1): the output tiles past
-                           the last full wave of workgroups run as a second launch with this
-                           split-k factor, their partials going through the workspace */
+    int32_t stream_k;   /* 0: one workgroup per output tile (and K partition).  1: the
+                           persistent stream-K kernel with one workgroup per CU; n in
+                           2 .. 1023: the same kernel with n workgroups.  Only with split_k == 1
+                           and the 256 x 256 tile, for M and N multiples of 256, K a multiple of
+                           64, at least as many tiles as workgroups, A and B read in place by the
+                           pipelined kernel, C 16-byte aligned with ldc a multiple of 4 and
+                           256 * ldc * 4 < 2^32 bytes; otherwise the tile's ordinary kernel runs.
+                           See XGEMM_KERNEL_PERSISTENT. */
 } xgemm_config;
 
 /*
@@ -163,8 +168,8 @@ int xgemm_run_noalloc(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
 
 /*
  * As xgemm_run, with the launch configuration forced to *cfg (validated:
- * XGEMM_ERR_INVALID_ARG for an unknown tile, split_k, group_m or tail_split
- * out of range, or tail_split > 1 together with split_k > 1).  Results agree
+ * XGEMM_ERR_INVALID_ARG for an unknown tile, split_k, group_m or stream_k
+ * out of range, or stream_k > 0 together with split_k > 1).  Results agree
  * with xgemm_run within the accuracy contract; only the summation grouping
  * differs.
  */
@@ -246,8 +251,22 @@ int xgemm_tile_info(int tile, int *bm, int *bn, int *bk, int *threads);
 
 /* Kernel families (see xgemm_kernel_family). */
 enum xgemm_kernel_family_id {
-    XGEMM_KERNEL_GENERAL = 0,   /* any shape and alignment; element-wise edge handling */
-    XGEMM_KERNEL_PIPELINED = 1  /* direct global-to-LDS loads, multi-stage LDS pipeline */
+    XGEMM_KERNEL_GENERAL = 0,    /* any shape and alignment; element-wise edge handling */
+    XGEMM_KERNEL_PIPELINED = 1,  /* direct global-to-LDS loads, multi-stage LDS pipeline */
+    XGEMM_KERNEL_PERSISTENT = 2  /* the pipelined 256 x 256 schedule as a persistent stream-K
+                                    kernel.  The paper's kernels are persistent, handing out
+                                    output tiles from a task generator (Section 4.2), and it
+                                    blames the variation on small and long-K problems on wave
+                                    quantisation (Section 6).  Each workgroup takes whole tiles in
+                                    rounds, then an equal share of the remaining tiles' K steps, so
+                                    no CU idles in a partial last round; a tile split between two
+                                    workgroups is finished by whichever completes second, which
+                                    adds the other's partial sum in a fixed order (the tile's first
+                                    K steps plus its last), without waiting on it.  The LDS
+                                    pipeline runs across a workgroup's tiles and a finished tile's
+                                    stores overlap the next tile's first MFMAs.  The workspace
+                                    holds two partial sums per workgroup (2 x 256 x 256 floats)
+                                    when tiles are split. */
 };
 
 /*
@@ -265,11 +284,13 @@ int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t 
                         const void *B, int64_t ldb, const xgemm_config *cfg);
 
 /*
- * Bytes of workspace xgemm_run_config needs for this problem and cfg on a
- * device with cu_count compute units, for 16-byte aligned A and B with
- * lda = K and ldb = N: split_k * M * ceil(N/4)*4 floats when split_k > 1, the
- * tail tiles' partials when tail_split > 1 applies, plus the operand copies
- * when K or N is not a multiple of 8 (each 256-byte aligned, after the
+ * Bytes of workspace xgemm_run_config allocates for this problem and cfg on
+ * a device with cu_count compute units, for 16-byte aligned A and B with
+ * lda = K and ldb = N: a 4096-byte prefix of counters (for the persistent
+ * kernel's split tiles, zeroed when the workspace is allocated and left zero
+ * by every call), then split_k * M * ceil(N/4)*4 floats when split_k > 1, the
+ * persistent kernel's partial sums when it splits tiles, plus the operand
+ * copies when K or N is not a multiple of 8 (each 256-byte aligned, after the
  * partials); 0 when nothing is needed.  Host-only.  Returns 0 for invalid
  * arguments.
  */
@@ -316,12 +337,13 @@ typedef struct xgemm_trace_event {
     int64_t addr; /* global byte address (LDS_LOAD source, STORE destination) */
 } xgemm_trace_event;
 
-/* One kernel launch of a planned call. */
+/* One kernel launch of a planned call.  Offsets count bytes from W, the
+   start of the workspace (its counter prefix comes first). */
 typedef struct xgemm_trace_info {
-    int32_t segments;        /* GEMM launches in the plan: 1, or 2 with a tail split */
+    int32_t segments;        /* GEMM launches in the plan (1) */
     int32_t family;          /* xgemm_kernel_family_id of this launch */
-    int32_t reduce;          /* 0: writes C; 1: full-matrix split partials in W, summed by a later
-                                launch; 2: tile-major split partials in W, likewise */
+    int32_t reduce;          /* 0: writes C (the persistent kernel: also partial sums in W);
+                                1: full-matrix split partials in W, summed by a later launch */
     int32_t threads;         /* threads per workgroup */
     int32_t lds_bytes;       /* LDS bytes per workgroup of the pipelined kernel (else 0) */
     int32_t split;           /* split-k factor of this launch */
@@ -334,6 +356,13 @@ typedef struct xgemm_trace_info {
     int64_t lda, ldb;        /* leading dimensions the kernel reads A and B with */
     int64_t a_offset;        /* byte offset of the packed A (M x k, leading dimension lda) in W, or -1 */
     int64_t b_offset;        /* byte offset of the packed B (k x ldb) in W, or -1 */
+    int64_t data_offset;     /* byte offset of the workspace's data after the counter prefix: the
+                                split partials, or the persistent kernel's partial sums (two of
+                                256 x 256 floats per workgroup, in the accumulators' layout) */
+    int32_t dp_rounds;       /* persistent kernel: rounds of whole tiles per workgroup */
+    int32_t sk_tiles;        /* persistent kernel: tiles shared out as K-step ranges */
+    int32_t kt;              /* persistent kernel: K steps per tile */
+    int32_t reserved;
 } xgemm_trace_info;
 
 /*
@@ -353,15 +382,21 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
  * counts[t] (counts has `threads` entries, the caller owns both arrays).  A
  * count above capacity means the trace was cut; call again with a larger
  * capacity (capacity 0 with out == NULL only counts).  W is the workspace
- * address for launches that write partials (reduce != 0) or read packed
- * operands (packed != 0), else unused.
- * Both kernel families are traced.  XGEMM_ERR_INVALID_ARG as
- * xgemm_trace_plan, or for a block out of range, counts == NULL, or W ==
- * NULL where it is needed.
+ * address (its start) for launches that write partials (reduce != 0, or the
+ * persistent kernel with sk_tiles > 0) or read packed operands
+ * (packed != 0), else unused.  `schedule` (0 or 1) matters only to the
+ * persistent kernel, whose path through a split tile depends on which
+ * workgroup counts in first: 0 traces every split tile's last K steps
+ * counting in first (the usual order: they start a workgroup's range while
+ * the first steps end the previous one's), 1 its first steps.  Counter reads
+ * and atomic adds appear as 4-byte LOAD events, counter resets as STORE.
+ * Every kernel family is traced.  XGEMM_ERR_INVALID_ARG as
+ * xgemm_trace_plan, or for a block out of range, a schedule other than 0 or
+ * 1, counts == NULL, or W == NULL where it is needed.
  */
 int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
                           float *C, int64_t ldc, float *W, const xgemm_config *cfg, int cu_count, int segment,
-                          int64_t block, xgemm_trace_event *out, int64_t capacity, int64_t *counts);
+                          int64_t block, int schedule, xgemm_trace_event *out, int64_t capacity, int64_t *counts);
 
 /*
  * Matrix-vector product (GEMV): y = A * x in fp32.

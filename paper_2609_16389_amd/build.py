@@ -8,7 +8,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "xgemm.hip")
 DEPS = [SRC, os.path.join(PKG, "csrc", "gemm_kernel.hpp"), os.path.join(PKG, "csrc", "gemv_kernel.hpp"),
-        os.path.join(PKG, "csrc", "pack_kernel.hpp"),
+        os.path.join(PKG, "csrc", "pack_kernel.hpp"), os.path.join(PKG, "csrc", "sk_kernel.hpp"),
         os.path.join(ROOT, "include", "xgemm.h")]
 LIB = os.path.join(PKG, "libxgemm.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -51,7 +51,6 @@ struct GemmParams {
     int vec_c;              // output 16-byte aligned, ldc a multiple of 4
     int tile_base;          // this launch covers logical tiles [tile_base, tile_base + tile_count)
     int tile_count;
-    int tile_major;         // 1: write each (split, tile) partial as a dense BM x BN block of C
     int batch;              // independent problems; problem b uses A + b*stride_a, B + b*stride_b,
     int64_t stride_a;       //   C + b*stride_c (elements); batched launches have split == 1
     int64_t stride_b;
@@ -149,10 +148,8 @@ __host__ __device__ __forceinline__ GemmParams map_tile(const GemmParams &p_in, 
     return p;
 }
 
-// Output placement: row-major C (or a full-matrix split partial) at
-// out + row * ldc + col, or, for tile-major partials, the dense BM x BN
-// block of (split, local tile) with row and column taken relative to the
-// tile origin.
+// Output placement: row-major C, or split ks's full-matrix partial, at
+// base + row * ld + col.
 struct OutView {
     float *base;
     int64_t ld;
@@ -160,20 +157,13 @@ struct OutView {
 };
 
 template <int BM, int BN>
-__host__ __device__ __forceinline__ OutView out_view(const GemmParams &p, int ks, int local, int m0, int n0)
+__host__ __device__ __forceinline__ OutView out_view(const GemmParams &p, int ks, int, int, int)
 {
     OutView o;
-    if (p.tile_major) {
-        o.base = p.C + ((int64_t)ks * p.tile_count + local) * (int64_t)(BM * BN);
-        o.ld = BN;
-        o.r0 = m0;
-        o.c0 = n0;
-    } else {
-        o.base = p.C + (int64_t)ks * p.split_stride;
-        o.ld = p.ldc;
-        o.r0 = 0;
-        o.c0 = 0;
-    }
+    o.base = p.C + (int64_t)ks * p.split_stride;
+    o.ld = p.ldc;
+    o.r0 = 0;
+    o.c0 = 0;
     return o;
 }
 
@@ -400,7 +390,7 @@ __host__ __device__ __forceinline__ void general_tile(const Ops &ops, const Gemm
     const OutView ov = out_view<BM, BN>(p, ks, local, m0, n0);
     float *Cb = ov.base;
     const int64_t ldc = ov.ld;
-    const bool vec_store = p.tile_major || (p.vec_c && interior);
+    const bool vec_store = p.vec_c && interior;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int row = m0 + wm * TM + i * 32 + l32;
@@ -575,6 +565,53 @@ struct DeviceOps {
             *(u32x4 *)q = v;
     }
     __device__ __forceinline__ void sync() const { __syncthreads(); }
+    // persistent kernel: buffer accesses (a descriptor of a base address in
+    // SGPRs, a 32-bit per-lane byte offset, a uniform byte offset), flags and
+    // the LDS words of the split-tile hand-over
+    typedef __amdgpu_buffer_rsrc_t Rsrc;
+    // raw buffer over `base` (no stride, no range limit; gfx9 descriptor
+    // word 3: 32-bit data format)
+    __device__ __forceinline__ Rsrc rsrc(const void *base) const
+    {
+        return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)0xffffffff, 0x00020000);
+    }
+    __device__ __forceinline__ void buf_store4(Rsrc r, uint32_t voff, uint32_t soff, f32x4 v) const
+    {
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, 0);
+    }
+    __device__ __forceinline__ void buf_store1(Rsrc r, uint32_t voff, uint32_t soff, float v) const
+    {
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, voff, soff, 0);
+    }
+    __device__ __forceinline__ f32x4 buf_load4(Rsrc r, uint32_t voff, uint32_t soff) const
+    {
+        return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+    }
+    // every global store of this wave written back past the XCD's L2 and
+    // complete (buffer_wbl2, s_waitcnt vmcnt(0)); agent scope
+    __device__ __forceinline__ void fence_release() const { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
+    // later loads miss this CU's L1 and the XCD's L2 lines that other
+    // agents' writes may have made stale (buffer_inv); agent scope
+    __device__ __forceinline__ void fence_acquire() const { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+    __device__ __forceinline__ int flag_load(int *f) const
+    {
+        return __hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __device__ __forceinline__ void flag_store(int *f, int v) const
+    {
+        __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // atomic add; returns the value before it
+    __device__ __forceinline__ int flag_add(int *f, int v) const
+    {
+        return __hip_atomic_fetch_add(f, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __device__ __forceinline__ void lds_write4(char *q, int v, bool on) const
+    {
+        if (on)
+            *(int *)q = v;
+    }
+    __device__ __forceinline__ int lds_read4(const char *q) const { return *(const int *)q; }
 };
 
 template <int BM, int BN, int BK, int WGM, int WGN, int DT>
@@ -1017,7 +1054,7 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     const OutView ov = out_view<BM, BN>(p, ks, local, m0, n0);
     float *Cb = ov.base;
     const int64_t ldc = ov.ld;
-    const bool vec_store = p.tile_major || (p.vec_c && (m0 + BM <= p.M) && (n0 + BN <= p.N));
+    const bool vec_store = p.vec_c && (m0 + BM <= p.M) && (n0 + BN <= p.N);
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
         const int row = m0 + wm * TM + i * MI + lr;
@@ -1082,44 +1119,6 @@ splitk_reduce(const float *W, int64_t split_stride, int64_t ldw, int split,
             for (int e = 0; e < 4; ++e)
                 if (j + e < N)
                     c[e] = s[e];
-        }
-    }
-}
-
-// Tile-major split partials -> C: for each tile of the range [tile_base,
-// tile_base + tile_count), C[tile] = sum over p of W[p][tile], p ascending.
-// W holds split x tile_count dense BM x BN blocks.
-template <int BM, int BN>
-__global__ void __launch_bounds__(256)
-splitk_reduce_tiles(const float *W, int split, int tile_base, int tile_count, int tiles_m, int tiles_n,
-                    int group_m, float *C, int64_t ldc, int M, int N, int vec_c)
-{
-    constexpr int V = BM * BN / 4;  // float4 vectors per tile
-    const int64_t nvec = (int64_t)tile_count * V;
-    const int64_t pstride = (int64_t)tile_count * BM * BN;
-    for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < nvec;
-         t += (int64_t)gridDim.x * blockDim.x) {
-        const int local = (int)(t / V);
-        const int v = (int)(t - (int64_t)local * V);
-        const int r = v / (BN / 4), c = (v % (BN / 4)) * 4;
-        int tm, tn;
-        logical_tile(tile_base + local, tiles_m, tiles_n, group_m, tm, tn);
-        const int row = tm * BM + r, col = tn * BN + c;
-        if (row >= M || col >= N)
-            continue;
-        const float *w = W + (int64_t)local * BM * BN + (int64_t)r * BN + c;
-        f32x4 sum = *(const f32x4 *)w;
-        for (int q = 1; q < split; ++q) {
-            const f32x4 x = *(const f32x4 *)(w + q * pstride);
-            sum += x;
-        }
-        float *dst = C + (int64_t)row * ldc + col;
-        if (vec_c && col + 4 <= N) {
-            *(f32x4 *)dst = sum;
-        } else {
-            for (int e = 0; e < 4; ++e)
-                if (col + e < N)
-                    dst[e] = sum[e];
         }
     }
 }

@@ -17,6 +17,7 @@
 #include "gemm_kernel.hpp"
 #include "gemv_kernel.hpp"
 #include "pack_kernel.hpp"
+#include "sk_kernel.hpp"
 
 using xgemm_dev::GemmParams;
 
@@ -77,11 +78,17 @@ void set_error(xgemm_ctx *h, const char *what, hipError_t e)
         snprintf(h->last_error, sizeof(h->last_error), "%s: %s", what, hipGetErrorString(e));
 }
 
+// Counter words of the persistent kernel's split tiles: the first bytes of
+// every workspace, zero when the workspace is allocated and zero again after
+// every call that uses them; the other workspace users start after them.
+constexpr size_t kWsPrefix = 4096;
+constexpr int kMaxSkGrid = (int)(kWsPrefix / sizeof(int));
+
 bool valid_config(const xgemm_config *c)
 {
     return c && c->tile >= 0 && c->tile < XGEMM_TILE_COUNT && c->split_k >= 1 && c->split_k <= 64 &&
-           c->group_m >= 1 && c->group_m <= 64 && c->tail_split >= 0 && c->tail_split <= 64 &&
-           (c->tail_split <= 1 || c->split_k == 1);
+           c->group_m >= 1 && c->group_m <= 64 && c->stream_k >= 0 && c->stream_k < kMaxSkGrid &&
+           (c->stream_k == 0 || c->split_k == 1);
 }
 
 // K elements each split covers: K / split rounded up to the K step, so that
@@ -148,37 +155,6 @@ int choose_group_m(int64_t tiles_m, int64_t tiles_n, int split)
     return (tiles_n * 8 <= share && tiles_m >= 8) ? 8 : 4;
 }
 
-// Split-k factor for the tiles past the last full wave of workgroups (0:
-// run them unsplit).  A partial last wave leaves CUs idle for a whole tile
-// time; splitting those tiles' K ranges spreads them over the idle CUs at
-// the price of writing, reading and summing their partials.
-int choose_tail_split(int64_t M, int64_t N, int64_t K, int cu_count, int tile)
-{
-    const TileShape &t = kTiles[tile];
-    const int64_t tiles = cdiv(M, t.bm) * cdiv(N, t.bn);
-    const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
-    const int64_t tail = tiles % slots;
-    if (tiles <= slots || tail == 0)
-        return 0;
-    // Peak-rate cycles of one tile, at the kernel's sustained fraction of
-    // the peak (about 0.55 on MI355X with random data), against the
-    // partials' traffic at about 70% of HBM bandwidth (2.3 KB per cycle).
-    const double wg = 2.0 * t.bm * t.bn * (double)K * t.wg_per_cu / 4096.0 / 0.55;
-    double best = wg;  // the tail run unsplit: one more full tile time
-    int best_s = 0;
-    for (int s2 = 2; s2 <= 8; s2 *= 2) {
-        if (tail * s2 > slots || split_chunk(K, s2, t.bk) * (s2 - 1) >= K || K / s2 < 3 * t.bk)
-            break;
-        const double bytes = (2.0 * s2 + 1.0) * 4.0 * (double)tail * t.bm * t.bn;
-        const double c = wg / s2 + bytes / 2333.0 + 4000.0;
-        if (c < best * 0.95) {
-            best = c;
-            best_s = s2;
-        }
-    }
-    return best_s;
-}
-
 void select_config_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int cu_count, xgemm_config *out);
 
 void select_config(int64_t M, int64_t N, int64_t K, int cu_count, xgemm_config *out)
@@ -213,12 +189,7 @@ void select_config_batched(int64_t batch, int64_t M, int64_t N, int64_t K, int c
     out->tile = best_tile;
     out->split_k = best_split;
     out->group_m = choose_group_m(cdiv(M, t.bm), cdiv(N, t.bn), best_split * (int)(batch < 64 ? batch : 64));
-    // The tail split is not chosen automatically: on MI355X a partial last
-    // wave runs at a higher clock (fewer busy CUs, less power), and the
-    // measured 4096 x 14336 x 4096 problem (3.5 waves) took 447 us with a
-    // 2-way tail split against 445 us without.  choose_tail_split's model is
-    // kept for callers that force the split through xgemm_run_config.
-    out->tail_split = 0;
+    out->stream_k = 0;
 }
 
 // Body + band plans.  When the output tiles of the chosen configuration end
@@ -293,7 +264,7 @@ BandPlan select_band(int64_t M, int64_t N, int64_t K, int cu_count)
                     out.body.tile = tb;
                     out.body.split_k = 1;
                     out.body.group_m = choose_group_m(cdiv(bm, t.bm), cdiv(bn, t.bn), 1);
-                    out.body.tail_split = 0;
+                    out.body.stream_k = 0;
                     out.band = bandcfg;
                 }
             }
@@ -445,27 +416,6 @@ hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int g
     });
 }
 
-template <int BM, int BN>
-hipError_t launch_tile_reduce_t(const GemmParams &p, float *C, int64_t ldc, int vec_c, hipStream_t s)
-{
-    const int64_t nvec = (int64_t)p.tile_count * BM * BN / 4;
-    const int grid = (int)(cdiv(nvec, 256) < 8192 ? cdiv(nvec, 256) : 8192);
-    hipLaunchKernelGGL((xgemm_dev::splitk_reduce_tiles<BM, BN>), dim3(grid), dim3(256), 0, s, (const float *)p.C,
-                       p.split, p.tile_base, p.tile_count, p.tiles_m, p.tiles_n, p.group_m, C, ldc, p.M, p.N,
-                       vec_c);
-    return hipGetLastError();
-}
-
-hipError_t launch_tile_reduce(int tile, const GemmParams &p, float *C, int64_t ldc, int vec_c, hipStream_t s)
-{
-    switch (tile) {
-    case XGEMM_TILE_256x256: return launch_tile_reduce_t<256, 256>(p, C, ldc, vec_c, s);
-    case XGEMM_TILE_256x128: return launch_tile_reduce_t<256, 128>(p, C, ldc, vec_c, s);
-    case XGEMM_TILE_128x128: return launch_tile_reduce_t<128, 128>(p, C, ldc, vec_c, s);
-    default: return hipErrorInvalidValue;
-    }
-}
-
 int check_args(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
                const void *B, int64_t ldb, const float *C, int64_t ldc, int dtype)
 {
@@ -493,7 +443,9 @@ struct Segment {
     GemmParams p;
     int64_t grid;
     bool dma;    // pipelined direct-to-LDS kernel (else the general one)
-    int reduce;  // 0: writes C; 1: full-matrix partials + splitk_reduce; 2: tile partials + tile reduce
+    bool sk;     // the persistent stream-K kernel (the 256 x 256 tile; dma is set too)
+    int reduce;  // 0: writes C; 1: full-matrix partials + splitk_reduce
+    int dp_rounds, sk_tiles, kt;  // persistent kernel: rounds of whole tiles, shared tiles, K steps per tile
 };
 
 // Operands copied into the workspace (pack16) so that the pipelined kernels
@@ -588,7 +540,6 @@ int make_plan_with(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, 
     base.vec_ab = ((uintptr_t)base.A % 16 == 0) && ((uintptr_t)base.B % 16 == 0) && (base.lda % 8 == 0) &&
                   (base.ldb % 8 == 0);
     base.tile_base = 0;
-    base.tile_major = 0;
     base.batch = 1;
     base.stride_a = base.stride_b = base.stride_c = 0;
     out->tile = cfg.tile;
@@ -612,13 +563,14 @@ int make_plan_with(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, 
             g.p.vec_c = ((uintptr_t)C % 16 == 0) && (ldc % 4 == 0);
         } else {
             g.p.C = nullptr;  // the workspace, filled in at launch
-            g.p.ldc = reduce == 1 ? out->ldw : t.bn;
-            g.p.split_stride = reduce == 1 ? M * out->ldw : 0;
+            g.p.ldc = out->ldw;
+            g.p.split_stride = M * out->ldw;
             g.p.vec_c = 1;
-            g.p.tile_major = reduce == 2;
         }
         g.grid = count * sp;
         g.dma = dma_eligible(g.p, t.bm, pk.b);
+        g.sk = false;
+        g.dp_rounds = g.sk_tiles = g.kt = 0;
     };
 
     // packed operands follow the split partials in the workspace
@@ -643,29 +595,42 @@ int make_plan_with(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, 
         out->ws = workspace_bytes(M, N, split);
         return finish();
     }
-    const int64_t slots = (int64_t)cu_count * t.wg_per_cu;
-    int64_t kct = 0;
-    const int tail_split = cfg.tail_split >= 2 ? trim_split(K, cfg.tail_split, t.bk, &kct) : 1;
-    const int64_t tail = (tail_split >= 2 && tiles > slots) ? tiles % slots : 0;
-    if (tail > 0) {
-        add(0, tiles - tail, 1, kc, 0);
-        add(tiles - tail, tail, tail_split, kct, 2);
-        out->ws = (size_t)tail * tail_split * t.bm * t.bn * sizeof(float);
-    } else {
-        add(0, tiles, 1, kc, 0);
+    add(0, tiles, 1, kc, 0);
+    // the persistent stream-K kernel: the 256 x 256 tile on whole tiles of C
+    // and whole K steps, at least as many tiles as workgroups (so that each
+    // workgroup's range holds a tile's worth of steps), C 16-byte aligned
+    // with 256 of its rows within 4 GiB
+    if (cfg.stream_k > 0 && cfg.tile == XGEMM_TILE_256x256 && !pk.a && !pk.b) {
+        Segment &g = out->seg[0];
+        const int grid = cfg.stream_k == 1 ? cu_count : cfg.stream_k;
+        const int64_t kt = K / t.bk;
+        if (g.dma && M % t.bm == 0 && N % t.bn == 0 && K % t.bk == 0 && kt >= 1 && grid >= 1 &&
+            grid < kMaxSkGrid && tiles >= grid && tiles * kt < 0x7fffffff && g.p.vec_c &&
+            (int64_t)t.bm * ldc * 4 < ((int64_t)1 << 32)) {
+            const int64_t rounds = tiles / grid, rem = tiles % grid;
+            g.sk = true;
+            g.grid = grid;
+            g.kt = (int)kt;
+            g.dp_rounds = (int)(rem == 0 ? rounds : rounds - 1);
+            g.sk_tiles = (int)(rem == 0 ? 0 : rem + grid);
+            // two partial sums per slot (a slot per workgroup)
+            out->ws = g.sk_tiles > 0 ? (size_t)2 * grid * t.bm * t.bn * sizeof(float) : 0;
+        }
     }
     return finish();
 }
 
-// Make the handle's workspace usable by work enqueued next on stream s and
-// at least `bytes` large (it never shrinks).  Work of earlier calls on other
-// streams that used the workspace is ordered before s's next work (a wait on
-// the handle's event); a buffer being replaced is freed only after that work
-// has completed.  Every caller enqueues its workspace users and then calls
-// release_workspace on the same stream.
+// Make the handle's workspace usable by work enqueued next on stream s with
+// at least `bytes` after its counter prefix (it never shrinks).  Work of
+// earlier calls on other streams that used the workspace is ordered before
+// s's next work (a wait on the handle's event); a buffer being replaced is
+// freed only after that work has completed, and a new one gets its counter
+// prefix zeroed on s.  Every caller enqueues its workspace users and then
+// calls release_workspace on the same stream.
 int acquire_workspace(xgemm_ctx *h, size_t bytes, hipStream_t s)
 {
     hipError_t e;
+    bytes += kWsPrefix;
     if (h->ws_limit > 0 && bytes > h->ws_limit) {
         snprintf(h->last_error, sizeof(h->last_error), "workspace of %zu bytes exceeds the handle's limit of %zu",
                  bytes, h->ws_limit);
@@ -698,8 +663,18 @@ int acquire_workspace(xgemm_ctx *h, size_t bytes, hipStream_t s)
         return XGEMM_ERR_ALLOC;
     }
     h->ws_bytes = bytes;
+    hipLaunchKernelGGL(xgemm_dev::fill_zero, dim3(1), dim3(256), 0, s, (float *)h->workspace, (int64_t)0, 1,
+                       (int)(kWsPrefix / sizeof(float)));
+    e = hipGetLastError();
+    if (e != hipSuccess) {
+        set_error(h, "workspace prefix clear", e);
+        return XGEMM_ERR_HIP;
+    }
     return XGEMM_OK;
 }
+
+// The workspace's data after its counter prefix.
+char *ws_data(void *ws) { return (char *)ws + kWsPrefix; }
 
 // Mark the end of the workspace users just enqueued on stream s.
 int release_workspace(xgemm_ctx *h, hipStream_t s)
@@ -748,7 +723,7 @@ struct CallPlan {
 // forced configuration, or the selected plan, banded or not.  Touches no
 // GPU.
 int plan_call(int cu_count, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
-              float *C, int64_t ldc, const xgemm_config *forced, CallPlan *cp)
+              float *C, int64_t ldc, const xgemm_config *forced, CallPlan *cp, bool allow_sk = true)
 {
     BandPlan band;
     if (forced) {
@@ -756,6 +731,8 @@ int plan_call(int cu_count, int64_t M, int64_t N, int64_t K, const void *A, int6
     } else {
         band = select_band(M, N, K, cu_count);
     }
+    if (!allow_sk)
+        band.body.stream_k = band.band.stream_k = 0;
     if (band.axis == XGEMM_BAND_NONE) {
         cp->parts = 1;
         cp->M[0] = M, cp->N[0] = N, cp->A[0] = A, cp->B[0] = B, cp->C[0] = C;
@@ -840,10 +817,55 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
 
 // Enqueue a plan whose workspace is in place: operand copies, the GEMM
 // launches and their split-k reductions.
+// The persistent kernel's parameters for a planned segment; flags and part
+// are the workspace's counter prefix and its data.
+xgemm_dev::SkParams sk_params(const Segment &g, int *flags, float *part)
+{
+    xgemm_dev::SkParams q;
+    q.A = g.p.A;
+    q.B = g.p.B;
+    q.C = g.p.C;
+    q.part = part;
+    q.flags = flags;
+    q.lda = g.p.lda;
+    q.ldb = g.p.ldb;
+    q.ldc = g.p.ldc;
+    q.M = g.p.M;
+    q.N = g.p.N;
+    q.K = g.p.K;
+    q.tiles_m = g.p.tiles_m;
+    q.tiles_n = g.p.tiles_n;
+    q.group_m = g.p.group_m;
+    q.kt = g.kt;
+    q.grid = (int)g.grid;
+    q.dp_rounds = g.dp_rounds;
+    q.sk_tiles = g.sk_tiles;
+    return q;
+}
+
+constexpr int kSkBM = 256, kSkBN = 256, kSkWGM = 2, kSkWGN = 4;
+
+hipError_t launch_sk(int dtype, const xgemm_dev::SkParams &q, hipStream_t s)
+{
+    constexpr int T = kSkWGM * kSkWGN * 64;
+    if (dtype == XGEMM_BF16)
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_sk<kSkBM, kSkBN, kDmaBK, kSkWGM, kSkWGN, 0>), dim3(q.grid), dim3(T),
+                           0, s, q);
+    else
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_sk<kSkBM, kSkBN, kDmaBK, kSkWGM, kSkWGN, 1>), dim3(q.grid), dim3(T),
+                           0, s, q);
+    return hipGetLastError();
+}
+
+// Enqueue a plan whose workspace is in place (ws: its start, the counter
+// prefix; the plan's data follows it): operand copies, the GEMM launches
+// and their split-k reductions.
 int launch_plan(xgemm_ctx *h, Plan plan, char *ws, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
                 const void *B, int64_t ldb, float *C, int64_t ldc, int dtype, hipStream_t s)
 {
     hipError_t e;
+    int *const flags = (int *)ws;
+    ws = ws_data(ws);
     // operand copies for the pipelined kernels
     const Pack &pk = plan.pack;
     if (pk.a && (e = launch_pack(A, lda, 0, M, K, ws + pk.a_off, M, pk.k8, 1, s)) != hipSuccess) {
@@ -864,7 +886,8 @@ int launch_plan(xgemm_ctx *h, Plan plan, char *ws, int64_t M, int64_t N, int64_t
             g.p.B = (const uint16_t *)(ws + pk.b_off);
         if (g.reduce)
             g.p.C = (float *)ws;
-        e = launch_tile(plan.tile, g.dma, dtype, g.p, (int)g.grid, s);
+        e = g.sk ? launch_sk(dtype, sk_params(g, flags, (float *)ws), s)
+                 : launch_tile(plan.tile, g.dma, dtype, g.p, (int)g.grid, s);
         if (e != hipSuccess) {
             set_error(h, "gemm launch", e);
             return XGEMM_ERR_HIP;
@@ -875,8 +898,6 @@ int launch_plan(xgemm_ctx *h, Plan plan, char *ws, int64_t M, int64_t N, int64_t
             hipLaunchKernelGGL(xgemm_dev::splitk_reduce, dim3(grid), dim3(256), 0, s,
                                (const float *)ws, (int64_t)(M * plan.ldw), plan.ldw, g.p.split, C,
                                ldc, (int)M, (int)N, vec_c);
-        } else if (g.reduce == 2) {
-            e = launch_tile_reduce(plan.tile, g.p, C, ldc, vec_c, s);
         }
         if (g.reduce) {
             e = hipGetLastError();
@@ -954,7 +975,7 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
         rc = acquire_workspace(h, ws, s);
         if (rc != XGEMM_OK)
             return rc;
-        char *const w = (char *)h->workspace;
+        char *const w = ws_data(h->workspace);
         e = hipSuccess;
         if (pk.a && (e = launch_pack(A, lda, sa, M, K, w + pk.a_off, M, pk.k8, na, s)) != hipSuccess)
             set_error(h, "pack A launch", e);
@@ -1134,7 +1155,7 @@ int run_gemv(xgemm_ctx *h, int64_t M, int64_t K, const float *A, int64_t lda, co
             rc = acquire_workspace(h, (size_t)p.split * (size_t)M * sizeof(float), s);
             if (rc != XGEMM_OK)
                 return rc;
-            p.part = (float *)h->workspace;
+            p.part = (float *)ws_data(h->workspace);
         }
         with_gemv_config(cfg, [&](auto r, auto u) {
             constexpr int R = decltype(r)::value, U = decltype(u)::value;
@@ -1163,9 +1184,23 @@ int run_gemv(xgemm_ctx *h, int64_t M, int64_t K, const float *A, int64_t lda, co
 // call appends one event to the calling thread's trace instead of touching
 // memory.  LDS pointers point into a host buffer of the kernel's LDS size,
 // so LDS addresses are byte offsets from its start.
+// Where the persistent kernel's trace takes the values of its split-tile
+// counters from: `schedule` 0 has every split tile's last steps count in
+// first, 1 its first steps; tail and head are this workgroup's two counter
+// addresses (slots lw and lw + 1).  Thread 0's hand-over words are recorded
+// in order and every thread reads them back in the same order (the threads
+// of a workgroup are traced one after another, thread 0 first).
+struct TraceSplit {
+    int schedule = 0;
+    const int *tail = nullptr, *head = nullptr;
+    std::vector<int> words;
+};
+
 struct TraceOps {
     char *base;
     std::vector<xgemm_trace_event> *ev;
+    TraceSplit *split = nullptr;
+    mutable size_t word_pos = 0;
     char *lds() const { return base; }
     uint32_t lds_addr(const char *q) const { return (uint32_t)(q - base); }
     int uniform(int x) const { return x; }
@@ -1236,6 +1271,51 @@ struct TraceOps {
     {
         push(XGEMM_TRACE_WAIT_LGKM, 0, 0, 0);
         push(XGEMM_TRACE_BARRIER, 0, 0, 0);
+    }
+    // persistent kernel: buffer accesses at base + per-lane + uniform offset
+    typedef const char *Rsrc;
+    Rsrc rsrc(const void *b) const { return (const char *)b; }
+    void buf_store4(Rsrc r, uint32_t voff, uint32_t soff, xgemm_dev::f32x4) const
+    {
+        push(XGEMM_TRACE_STORE, 16, 0, (int64_t)(uintptr_t)(r + voff + soff));
+    }
+    void buf_store1(Rsrc r, uint32_t voff, uint32_t soff, float) const
+    {
+        push(XGEMM_TRACE_STORE, 4, 0, (int64_t)(uintptr_t)(r + voff + soff));
+    }
+    xgemm_dev::f32x4 buf_load4(Rsrc r, uint32_t voff, uint32_t soff) const
+    {
+        push(XGEMM_TRACE_LOAD, 16, 0, (int64_t)(uintptr_t)(r + voff + soff));
+        return xgemm_dev::f32x4{0, 0, 0, 0};
+    }
+    // the release fence ends with s_waitcnt vmcnt(0); the acquire fence
+    // (a cache invalidation) waits for nothing
+    void fence_release() const { push(XGEMM_TRACE_WAIT_VM, 0, 0, 0); }
+    void fence_acquire() const {}
+    // counter reads and atomic adds are vector-memory loads with a result
+    int flag_load(int *f) const
+    {
+        push(XGEMM_TRACE_LOAD, 4, 0, (int64_t)(uintptr_t)f);
+        // the head finds the last steps counted in (schedule 0) or not
+        return (split && f == split->head && split->schedule == 0) ? 1 : 0;
+    }
+    int flag_add(int *f, int) const
+    {
+        push(XGEMM_TRACE_LOAD, 4, 0, (int64_t)(uintptr_t)f);
+        // the piece counting in second finds 1: the tail under schedule 1
+        return (split && f == split->tail && split->schedule == 1) ? 1 : 0;
+    }
+    void flag_store(int *f, int) const { push(XGEMM_TRACE_STORE, 4, 0, (int64_t)(uintptr_t)f); }
+    void lds_write4(char *q, int v, bool on) const
+    {
+        push(XGEMM_TRACE_LDS_WRITE, 4, on ? (int64_t)(q - base) : -1, 0);
+        if (on && split)
+            split->words.push_back(v);
+    }
+    int lds_read4(const char *q) const
+    {
+        push(XGEMM_TRACE_LDS_READ, 4, q - base, 0);
+        return split && word_pos < split->words.size() ? split->words[word_pos++] : 0;
     }
 };
 
@@ -1341,6 +1421,13 @@ int xgemm_create(xgemm_handle_t *out)
                 delete h;
                 return XGEMM_ERR_HIP;
             }
+            // its counter prefix starts zero (the persistent kernel leaves it so)
+            if (hipMemsetAsync(ptr, 0, kWsPrefix, nullptr) != hipSuccess ||
+                hipStreamSynchronize(nullptr) != hipSuccess) {
+                (void)hipGetLastError();
+                delete h;
+                return XGEMM_ERR_HIP;
+            }
             g_scratch_ptr[dev] = ptr;
         }
         h->scratch = g_scratch_ptr[dev];
@@ -1403,11 +1490,14 @@ int xgemm_run_noalloc(xgemm_handle_t h, int64_t M, int64_t N, int64_t K, const v
         return launch_zero(h, M, N, C, ldc, s);
     CallPlan cp;
     rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, nullptr, &cp);
+    if (rc == XGEMM_OK && cp.ws + kWsPrefix > kScratchBytes)   // a persistent plan's partials may not fit
+        rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, nullptr, &cp, false);
     if (rc != XGEMM_OK)
         return rc;
-    if (cp.ws > kScratchBytes) {
+    if (cp.ws + kWsPrefix > kScratchBytes) {
         snprintf(h->last_error, sizeof(h->last_error),
-                 "the call needs %zu bytes of scratch, above the static maximum of %zu", cp.ws, kScratchBytes);
+                 "the call needs %zu bytes of scratch, above the static maximum of %zu", cp.ws + kWsPrefix,
+                 kScratchBytes);
         return XGEMM_ERR_INVALID_ARG;
     }
     return launch_call(h, cp, (char *)h->scratch, K, lda, ldb, ldc, dtype, s);
@@ -1473,10 +1563,10 @@ int xgemm_kernel_family(int64_t M, int64_t N, int64_t K, const void *A, int64_t 
         lda < K || ldb < N)
         return -1;
     Plan plan;
-    // C's alignment does not affect the choice; the tail split needs a CU count
+    // C taken as aligned; the persistent kernel's grid is 256 CUs here
     if (make_plan(M, N, K, A, lda, B, ldb, nullptr, N, *cfg, 256, &plan, true) != XGEMM_OK)
         return -1;
-    return plan.seg[0].dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
+    return plan.seg[0].sk ? XGEMM_KERNEL_PERSISTENT : plan.seg[0].dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
 }
 
 size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, const xgemm_config *cfg)
@@ -1489,7 +1579,7 @@ size_t xgemm_workspace_bytes(int64_t M, int64_t N, int64_t K, int cu_count, cons
     Plan plan;
     if (make_plan(M, N, K, nullptr, K, nullptr, N, nullptr, N, *cfg, cu_count, &plan, true) != XGEMM_OK)
         return 0;
-    return plan.ws;
+    return plan.ws > 0 ? plan.ws + kWsPrefix : 0;
 }
 
 int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
@@ -1504,10 +1594,11 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
         return rc;
     const Segment &g = plan.seg[segment];
     info->segments = plan.nseg;
-    info->family = g.dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
+    info->family = g.sk ? XGEMM_KERNEL_PERSISTENT : g.dma ? XGEMM_KERNEL_PIPELINED : XGEMM_KERNEL_GENERAL;
     info->reduce = g.reduce;
     info->threads = tile_threads(plan.tile, g.dma);
-    info->lds_bytes = g.dma ? with_dma_tile(plan.tile, [](auto t) {
+    info->lds_bytes = g.sk ? xgemm_dev::sk_lds_bytes<kSkBM, kSkBN, kDmaBK>()
+                    : g.dma ? with_dma_tile(plan.tile, [](auto t) {
         using T = decltype(t);
         return xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>();
     }) : with_general_tile(plan.tile, [](auto t) {
@@ -1516,7 +1607,7 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
     });
     info->split = g.p.split;
     info->grid = g.grid;
-    info->workspace_bytes = (int64_t)plan.ws;
+    info->workspace_bytes = plan.ws > 0 ? (int64_t)(plan.ws + kWsPrefix) : 0;
     info->tile_base = g.p.tile_base;
     info->tile_count = g.p.tile_count;
     const Pack &pk = plan.pack;
@@ -1524,16 +1615,21 @@ int xgemm_trace_plan(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda
     info->k = g.p.K;
     info->lda = g.p.lda;
     info->ldb = g.p.ldb;
-    info->a_offset = pk.a ? (int64_t)pk.a_off : -1;
-    info->b_offset = pk.b ? (int64_t)pk.b_off : -1;
+    info->a_offset = pk.a ? (int64_t)(kWsPrefix + pk.a_off) : -1;
+    info->b_offset = pk.b ? (int64_t)(kWsPrefix + pk.b_off) : -1;
+    info->data_offset = (int64_t)kWsPrefix;
+    info->dp_rounds = g.dp_rounds;
+    info->sk_tiles = g.sk_tiles;
+    info->kt = g.kt;
+    info->reserved = 0;
     return XGEMM_OK;
 }
 
 int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
                           float *C, int64_t ldc, float *W, const xgemm_config *cfg, int cu_count, int segment,
-                          int64_t block, xgemm_trace_event *out, int64_t capacity, int64_t *counts)
+                          int64_t block, int schedule, xgemm_trace_event *out, int64_t capacity, int64_t *counts)
 {
-    if (!counts || capacity < 0 || (capacity > 0 && !out))
+    if (!counts || capacity < 0 || (capacity > 0 && !out) || schedule < 0 || schedule > 1)
         return XGEMM_ERR_INVALID_ARG;
     Plan plan;
     int rc = trace_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, cu_count, segment, &plan);
@@ -1543,24 +1639,27 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
     if (block < 0 || block >= g.grid)
         return XGEMM_ERR_INVALID_ARG;
     const Pack &pk = plan.pack;
-    if (g.reduce || pk.a || pk.b) {
+    char *const wdata = W ? ws_data(W) : nullptr;
+    if (g.reduce || pk.a || pk.b || (g.sk && g.sk_tiles > 0)) {
         if (!W)
             return XGEMM_ERR_INVALID_ARG;
         if (g.reduce)
-            g.p.C = W;
+            g.p.C = (float *)wdata;
         if (pk.a)
-            g.p.A = (const uint16_t *)((char *)W + pk.a_off);
+            g.p.A = (const uint16_t *)(wdata + pk.a_off);
         if (pk.b)
-            g.p.B = (const uint16_t *)((char *)W + pk.b_off);
+            g.p.B = (const uint16_t *)(wdata + pk.b_off);
     }
     const int threads = tile_threads(plan.tile, g.dma);
+    TraceSplit split;
+    split.schedule = schedule;
     // run `body(ops, tid)` for every thread, collecting each one's events
     auto trace_threads = [&](size_t lds_bytes, auto &&body) {
         std::vector<char> lds(lds_bytes);
         std::vector<xgemm_trace_event> ev;
         for (int tid = 0; tid < threads; ++tid) {
             ev.clear();
-            const TraceOps ops{lds.data(), &ev};
+            const TraceOps ops{lds.data(), &ev, &split};
             body(ops, tid);
             counts[tid] = (int64_t)ev.size();
             const int64_t n = counts[tid] < capacity ? counts[tid] : capacity;
@@ -1569,6 +1668,15 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
         }
         return (int)XGEMM_OK;
     };
+    if (g.sk) {
+        const xgemm_dev::SkParams q = sk_params(g, (int *)W, (float *)wdata);
+        const int lw = xgemm_dev::sk_logical((int)block, q.grid);
+        split.tail = q.flags ? q.flags + lw : nullptr;
+        split.head = q.flags ? q.flags + lw + 1 : nullptr;
+        return trace_threads(xgemm_dev::sk_lds_bytes<kSkBM, kSkBN, kDmaBK>(), [&](const TraceOps &ops, int tid) {
+            xgemm_dev::sk_tile<kSkBM, kSkBN, kDmaBK, kSkWGM, kSkWGN, 0>(ops, q, (int)block, tid);
+        });
+    }
     if (g.dma)
         return with_dma_tile(plan.tile, [&](auto t) {
             using T = decltype(t);

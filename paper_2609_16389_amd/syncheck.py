@@ -388,17 +388,20 @@ class LaunchReport:
         return not self.violations
 
 
-def trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, threads, capacity=None):
+def trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, threads, capacity=None, schedule=0):
     """(events [threads, capacity], counts [threads]) of one workgroup.
     `threads` must be the launch's thread count (xgemm_trace_plan's
-    info.threads): the library writes that many counts."""
+    info.threads): the library writes that many counts.  `schedule` is the
+    order in which the two pieces of a persistent kernel's split tile count
+    in (0: its last K steps first)."""
     import ctypes
     info = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, seg)
     if threads != info.threads:
         raise ValueError("trace_workgroup: the launch has %d threads per workgroup, not %d" % (info.threads, threads))
     counts = np.zeros(threads, dtype=np.int64)
     cptr = counts.ctypes.data_as(ctypes.c_void_p)
-    args = (M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, BASE_W, ctypes.byref(cfg), cu_count, seg, block)
+    args = (M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, BASE_W, ctypes.byref(cfg), cu_count, seg, block,
+            schedule)
     if capacity is None:
         rc = xg.lib.xgemm_trace_workgroup(*args, None, 0, cptr)
         if rc != xg.XGEMM_OK:
@@ -409,67 +412,107 @@ def trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, threads, 
     if rc != xg.XGEMM_OK:
         raise xg.XgemmError(rc)
     if int(counts.max()) > capacity:
-        return trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, threads, int(counts.max()))
+        return trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, threads, int(counts.max()),
+                               schedule)
     return ev, counts
 
 
 class _Coverage:
-    """Counts how often each element of a launch's output is stored."""
+    """Counts how often each element of a launch's outputs is stored: C, the
+    full-matrix split partials, or (the persistent kernel) C and its
+    partial sums, two per slot of BM x BN floats; the persistent kernel's
+    4-byte counter stores are only checked to hit the counter prefix."""
 
     def __init__(self, info, M, N, ldc, bm, bn):
         self.reduce = info.reduce
+        self.sk = info.family == xg.XGEMM_KERNEL_PERSISTENT
         self.M, self.N, self.ldc, self.bm, self.bn = M, N, ldc, bm, bn
         self.split = info.split
-        if info.reduce == 0:
-            self.base, self.shape = BASE_C, (M, N)
-        elif info.reduce == 1:
-            self.ldw = (N + 3) // 4 * 4
-            self.base, self.shape = BASE_W, (info.split, M, N)
+        self.count = np.zeros((M, N), dtype=np.uint8) if info.reduce == 0 else None
+        self.ldw = (N + 3) // 4 * 4
+        if info.reduce == 1:
+            self.pbase = BASE_W + info.data_offset
+            self.part = np.zeros((info.split, M, N), dtype=np.uint8)
+        elif self.sk:
+            self.pbase = BASE_W + info.data_offset
+            self.part = np.zeros(2 * info.grid * bm * bn, dtype=np.uint8)
         else:
-            self.base, self.shape = BASE_W, (info.split, info.tile_count, bm * bn)
-        self.count = np.zeros(self.shape, dtype=np.uint8)
+            self.part = None
+
+    def _c(self, off):
+        e = off // 4
+        i, j = e // self.ldc, e % self.ldc
+        ok = (e >= 0) & (i < self.M) & (j < self.N)
+        return ok, (i[ok], j[ok])
+
+    def _p(self, off):
+        e = off // 4
+        if self.reduce == 1:
+            per = self.M * self.ldw
+            p, r = e // per, e % per
+            i, j = r // self.ldw, r % self.ldw
+            ok = (e >= 0) & (p < self.split) & (j < self.N)
+            return ok, (p[ok], i[ok], j[ok])
+        ok = (e >= 0) & (e < len(self.part))
+        return ok, (e[ok],)
 
     def add(self, addr, nbytes):
         """Record stores of nbytes at each address; returns a list of problems."""
         bad = []
-        off = addr - self.base
-        if (off % 4).any():
-            bad.append("store not aligned to a float")
-        elem = off // 4
-        for k in range(nbytes // 4):
-            e = elem + k
-            if self.reduce == 0:
-                i, j = e // self.ldc, e % self.ldc
-                ok = (e >= 0) & (i < self.M) & (j < self.N)
-                idx = (i[ok], j[ok])
-            elif self.reduce == 1:
-                per = self.M * self.ldw
-                p, r = e // per, e % per
-                i, j = r // self.ldw, r % self.ldw
-                ok = (e >= 0) & (p < self.split) & (j < self.N)
-                idx = (p[ok], i[ok], j[ok])
-            else:
-                per = self.bm * self.bn
-                blk, r = e // per, e % per
-                p, t = blk // self.shape[1], blk % self.shape[1]
-                ok = (e >= 0) & (p < self.split)
-                idx = (p[ok], t[ok], r[ok])
-            if not ok.all():
-                bad.append("store outside the output at byte offset %d" % int(off[~ok][0] + 4 * k))
-            np.add.at(self.count, idx, 1)
+        if self.sk and nbytes == 4:
+            # counter resets
+            off = addr - BASE_W
+            if ((off < 0) | (off >= PREFIX_BYTES) | (off % 4 != 0)).any():
+                bad.append("4-byte store outside the counter prefix")
+            return bad
+        in_c = (addr >= BASE_C) & (addr < BASE_W) if self.count is not None else np.zeros(len(addr), bool)
+        for sel, base, region in ((in_c, BASE_C, "C"), (~in_c, getattr(self, "pbase", BASE_W), "partials")):
+            a = addr[sel]
+            if not len(a):
+                continue
+            off = a - base
+            if (off % 4).any():
+                bad.append("store not aligned to a float")
+            for k in range(nbytes // 4):
+                ok, idx = self._c(off + 4 * k) if region == "C" else (self._p(off + 4 * k) if self.part is not None
+                                                                       else (np.zeros(len(off), bool), None))
+                if not ok.all():
+                    bad.append("store outside the output at byte offset %d" % int(off[~ok][0] + 4 * k))
+                if idx is not None:
+                    np.add.at(self.count if region == "C" else self.part, idx, 1)
         return bad
 
+    def written(self, addr, nbytes):
+        """Whether the partial elements that loads of nbytes at addr read were
+        all stored by some workgroup of the launch."""
+        off = addr - self.pbase
+        ok = np.ones(len(addr), bool)
+        for k in range(nbytes // 4):
+            inside, idx = self._p(off + 4 * k)
+            ok &= inside
+            ok[inside] &= self.part[idx] == 1
+        return ok
+
     def result(self):
-        zero = int((self.count == 0).sum())
-        many = int((self.count > 1).sum())
+        arr = self.count if self.reduce == 0 else self.part
+        zero = int((arr == 0).sum())
+        many = int((arr > 1).sum())
         return zero, many
 
+    def partial_many(self):
+        return int((self.part > 1).sum()) if self.part is not None else 0
 
-def check_launch(M, N, K, cfg, cu_count=256, lda=None, ldb=None, ldc=None, max_blocks=None):
+
+PREFIX_BYTES = 4096   # the workspace's counter prefix
+
+
+def check_launch(M, N, K, cfg, cu_count=256, lda=None, ldb=None, ldc=None, max_blocks=None, schedules=None):
     """Trace every workgroup of every launch of the plan for this call and
     run the checks; returns a LaunchReport.  max_blocks limits the
     workgroups traced per launch (for quick checks of large shapes; the
-    coverage check is then skipped)."""
+    coverage check is then skipped).  A persistent launch that splits tiles
+    is checked under both orders of its split tiles' pieces (schedules 0
+    and 1) unless `schedules` names them."""
     lda = K if lda is None else lda
     ldb = N if ldb is None else ldb
     ldc = N if ldc is None else ldc
@@ -492,88 +535,79 @@ def check_launch(M, N, K, cfg, cu_count=256, lda=None, ldb=None, ldc=None, max_b
         b_hi = b_lo + 2 * info0.k * info0.ldb
     else:
         b_lo, b_hi = BASE_B, BASE_B + 2 * ((K - 1) * ldb + N)
-    c_cov = None
     for seg in range(info0.segments):
         info = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, seg)
-        cov = _Coverage(info, M, N, ldc, bm, bn)
-        if info.reduce == 0:
-            c_cov = cov
+        sk = info.family == xg.XGEMM_KERNEL_PERSISTENT
+        scheds = schedules if schedules is not None else ((0, 1) if sk and info.sk_tiles > 0 else (0,))
         nblk = info.grid if max_blocks is None else min(info.grid, max_blocks)
-        for block in range(nblk):
-            ev, counts = trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, info.threads)
-            n_blocks += 1
-            n_events += int(counts.sum())
-            valid = np.arange(ev.shape[1])[None, :] < counts[:, None]
-            # global reads: direct (to LDS) and register loads
-            ld = valid & ((ev["op"] == LDS_LOAD) | (ev["op"] == LOAD))
-            ga = ev["addr"][ld]
-            nb = ev["arg"][ld]
-            inside = ((ga >= a_lo) & (ga + nb <= a_hi)) | ((ga >= b_lo) & (ga + nb <= b_hi))
-            if not inside.all():
-                violations.append(Violation("global_bounds", -1, -1, "launch %d workgroup %d: load "
-                                            "reads outside A and B at address %#x" %
-                                            (seg, block, int(ga[~inside][0]))))
-            # global stores
-            st = valid & (ev["op"] == STORE)
-            for nbytes in np.unique(ev["arg"][st]):
-                sel = st & (ev["arg"] == nbytes)
-                for msg in cov.add(ev["addr"][sel], int(nbytes)):
-                    violations.append(Violation("global_bounds", -1, -1, "launch %d workgroup %d: %s" %
-                                                (seg, block, msg)))
-            # LDS: one interpretation per distinct operation stream
-            key = hashlib.sha1()
-            for f in ("op", "arg", "lds"):
-                key.update(np.where(valid, ev[f], 0).tobytes())
-            key.update(counts.tobytes())
-            key = key.digest()
-            if key not in lds_seen:
-                lds_seen.add(key)
-                pre = []
-                waves = wave_streams(ev, counts, pre)
-                violations.extend(pre)
-                for v in check_workgroup_lds(waves, info.lds_bytes):
-                    v.detail = "launch %d workgroup %d: %s" % (seg, block, v.detail)
-                    violations.append(v)
-        if max_blocks is None:
+        for schedule in scheds:
+            cov = _Coverage(info, M, N, ldc, bm, bn)
+            part_loads = []
+            for block in range(nblk):
+                ev, counts = trace_workgroup(M, N, K, lda, ldb, ldc, cfg, cu_count, seg, block, info.threads,
+                                             schedule=schedule)
+                n_blocks += 1
+                n_events += int(counts.sum())
+                valid = np.arange(ev.shape[1])[None, :] < counts[:, None]
+                # global reads: direct (to LDS) and register loads; the
+                # persistent kernel also reads its counters and partial sums
+                ld = valid & ((ev["op"] == LDS_LOAD) | (ev["op"] == LOAD))
+                ga = ev["addr"][ld]
+                nb = ev["arg"][ld]
+                inside = ((ga >= a_lo) & (ga + nb <= a_hi)) | ((ga >= b_lo) & (ga + nb <= b_hi))
+                if sk:
+                    ctr = (ga >= BASE_W) & (ga + nb <= BASE_W + PREFIX_BYTES) & (nb == 4)
+                    part = (ga >= BASE_W + info.data_offset) & (ga + nb <= BASE_W + info.workspace_bytes) & (nb == 16)
+                    inside |= ctr | part
+                    part_loads.append(ga[part])
+                if not inside.all():
+                    violations.append(Violation("global_bounds", -1, -1, "launch %d workgroup %d: load "
+                                                "reads outside A and B at address %#x" %
+                                                (seg, block, int(ga[~inside][0]))))
+                # global stores
+                st = valid & (ev["op"] == STORE)
+                for nbytes in np.unique(ev["arg"][st]):
+                    sel = st & (ev["arg"] == nbytes)
+                    for msg in cov.add(ev["addr"][sel], int(nbytes)):
+                        violations.append(Violation("global_bounds", -1, -1, "launch %d workgroup %d: %s" %
+                                                    (seg, block, msg)))
+                # LDS: one interpretation per distinct operation stream
+                key = hashlib.sha1()
+                for f in ("op", "arg", "lds"):
+                    key.update(np.where(valid, ev[f], 0).tobytes())
+                key.update(counts.tobytes())
+                key = key.digest()
+                if key not in lds_seen:
+                    lds_seen.add(key)
+                    pre = []
+                    waves = wave_streams(ev, counts, pre)
+                    violations.extend(pre)
+                    for v in check_workgroup_lds(waves, info.lds_bytes):
+                        v.detail = "launch %d workgroup %d: %s" % (seg, block, v.detail)
+                        violations.append(v)
+            if max_blocks is not None:
+                continue
             zero, many = cov.result()
-            if info.reduce == 2 or info.reduce == 1 or info.reduce == 0:
-                if many:
-                    violations.append(Violation("coverage", -1, -1, "launch %d: %d output elements stored by "
-                                                "more than one store (unordered workgroups race)" % (seg, many)))
-                if zero and info.reduce != 0:
-                    violations.append(Violation("coverage", -1, -1, "launch %d: %d partial elements never "
-                                                "written" % (seg, zero)))
-    if max_blocks is None and c_cov is not None:
-        # C must be covered once by the direct launch plus the tiles whose
-        # partials a later launch sums (tail split): those are reported by
-        # the tile-partial coverage above, so only the direct launch's tiles
-        # are counted here.
-        zero, _ = c_cov.result()
-        expect_missing = 0
-        if info0.segments > 1:
-            info1 = xg.xgemm_trace_plan(M, N, K, BASE_A, lda, BASE_B, ldb, BASE_C, ldc, cfg, cu_count, 1)
-            expect_missing = _tile_elements(M, N, bm, bn, cfg.group_m, info1.tile_base, info1.tile_count)
-        if zero != expect_missing:
-            violations.append(Violation("coverage", -1, -1, "%d elements of C never written (expected %d left "
-                                        "to the partial sums)" % (zero, expect_missing)))
+            tag = "launch %d%s" % (seg, " (schedule %d)" % schedule if sk else "")
+            if many:
+                violations.append(Violation("coverage", -1, -1, "%s: %d output elements stored by more than one "
+                                            "store (unordered workgroups race)" % (tag, many)))
+            if zero and info.reduce == 1:
+                violations.append(Violation("coverage", -1, -1, "%s: %d partial elements never written" %
+                                            (tag, zero)))
+            if info.reduce == 0 and zero:
+                violations.append(Violation("coverage", -1, -1, "%s: %d elements of C never written" % (tag, zero)))
+            if sk:
+                if cov.partial_many():
+                    violations.append(Violation("coverage", -1, -1, "%s: %d partial-sum elements stored twice" %
+                                                (tag, cov.partial_many())))
+                pl = np.concatenate(part_loads) if part_loads else np.zeros(0, np.int64)
+                if len(pl) and not cov.written(pl, 16).all():
+                    violations.append(Violation("coverage", -1, -1, "%s: a partial sum read that no workgroup "
+                                                "stores" % tag))
     return LaunchReport(shape=(M, N, K), config=repr(cfg), segments=info0.segments, workgroups=n_blocks,
                         lds_classes=len(lds_seen), events=n_events, seconds=time.perf_counter() - t0,
                         violations=violations)
-
-
-def _tile_elements(M, N, bm, bn, group_m, first, count):
-    """Elements of C inside logical tiles [first, first + count)."""
-    tiles_m, tiles_n = -(-M // bm), -(-N // bn)
-    total = 0
-    for t in range(first, first + count):
-        group = group_m * tiles_n
-        g = t // group
-        first_m = g * group_m
-        gm = min(tiles_m - first_m, group_m)
-        r = t - g * group
-        tm, tn = first_m + r % gm, r // gm
-        total += (min(M, (tm + 1) * bm) - tm * bm) * (min(N, (tn + 1) * bn) - tn * bn)
-    return total
 
 
 def trace_gemv_workgroup(M, K, lda, cfg, block, capacity=None):
@@ -694,12 +728,13 @@ def main(argv=None):
     ap.add_argument("K", type=int)
     ap.add_argument("--tile", type=int, default=None)
     ap.add_argument("--split", type=int, default=None)
-    ap.add_argument("--tail-split", type=int, default=0)
+    ap.add_argument("--stream-k", type=int, default=0,
+                    help="the persistent stream-K kernel: 1 on every CU, n > 1 on n workgroups")
     ap.add_argument("--group-m", type=int, default=None)
     ap.add_argument("--cu-count", type=int, default=256)
     ap.add_argument("--max-blocks", type=int, default=None)
     args = ap.parse_args(argv)
-    if all(v is None for v in (args.tile, args.split, args.group_m)) and args.tail_split == 0:
+    if all(v is None for v in (args.tile, args.split, args.group_m)) and args.stream_k == 0:
         # the selector's plan, as xgemm_run makes it (possibly a body and a band)
         reps = check_call(args.M, args.N, args.K, xg.XGEMM_BF16, args.cu_count, args.max_blocks)
         for rep in reps:
@@ -716,7 +751,7 @@ def main(argv=None):
         cfg.split_k = args.split
     if args.group_m is not None:
         cfg.group_m = args.group_m
-    cfg.tail_split = args.tail_split
+    cfg.stream_k = args.stream_k
     try:
         rep = check_launch(args.M, args.N, args.K, cfg, args.cu_count, max_blocks=args.max_blocks)
     except xg.XgemmError as e:

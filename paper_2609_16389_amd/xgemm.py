@@ -32,15 +32,16 @@ XGEMM_TILE_COUNT = 3
 
 XGEMM_KERNEL_GENERAL = 0
 XGEMM_KERNEL_PIPELINED = 1
+XGEMM_KERNEL_PERSISTENT = 2
 
 
 class xgemm_config(ctypes.Structure):
     _fields_ = [("tile", ctypes.c_int32), ("split_k", ctypes.c_int32),
-                ("group_m", ctypes.c_int32), ("tail_split", ctypes.c_int32)]
+                ("group_m", ctypes.c_int32), ("stream_k", ctypes.c_int32)]
 
     def __repr__(self):
-        return "xgemm_config(tile=%d, split_k=%d, group_m=%d, tail_split=%d)" % (
-            self.tile, self.split_k, self.group_m, self.tail_split)
+        return "xgemm_config(tile=%d, split_k=%d, group_m=%d, stream_k=%d)" % (
+            self.tile, self.split_k, self.group_m, self.stream_k)
 
 
 XGEMM_BAND_NONE = 0
@@ -87,7 +88,9 @@ class xgemm_trace_info(ctypes.Structure):
                 ("grid", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
                 ("tile_base", ctypes.c_int32), ("tile_count", ctypes.c_int32),
                 ("packed", ctypes.c_int32), ("k", ctypes.c_int32), ("lda", ctypes.c_int64), ("ldb", ctypes.c_int64),
-                ("a_offset", ctypes.c_int64), ("b_offset", ctypes.c_int64)]
+                ("a_offset", ctypes.c_int64), ("b_offset", ctypes.c_int64), ("data_offset", ctypes.c_int64),
+                ("dp_rounds", ctypes.c_int32), ("sk_tiles", ctypes.c_int32), ("kt", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class XgemmError(RuntimeError):
@@ -143,7 +146,7 @@ lib.xgemm_trace_plan.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64,
                                  _i32, _i32, ctypes.POINTER(xgemm_trace_info)]
 lib.xgemm_trace_plan.restype = _i32
 lib.xgemm_trace_workgroup.argtypes = [_i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _p,
-                                      ctypes.POINTER(xgemm_config), _i32, _i32, _i64, _p, _i64, _p]
+                                      ctypes.POINTER(xgemm_config), _i32, _i32, _i64, _i32, _p, _i64, _p]
 lib.xgemm_trace_workgroup.restype = _i32
 lib.xgemv_run.argtypes = [_handle_t, _i64, _i64, _p, _i64, _p, _p, _p]
 lib.xgemv_run.restype = _i32
@@ -257,11 +260,13 @@ TRACE_EVENT_DTYPE = [("op", "<i4"), ("arg", "<i4"), ("lds", "<i8"), ("addr", "<i
 
 
 def xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, cfg, cu_count, segment, block, threads,
-                          capacity=None):
+                          capacity=None, schedule=0):
     """Events of every thread of one workgroup: a list of `threads` numpy
     record arrays (fields op, arg, lds, addr).  `threads` must be the
     launch's thread count (xgemm_trace_plan's info.threads), since the
-    library writes that many counts.  Raises XgemmError."""
+    library writes that many counts.  `schedule` picks which piece of a
+    persistent kernel's split tile counts in first (0: its last K steps).
+    Raises XgemmError."""
     import numpy as np
     if threads != xgemm_trace_plan(M, N, K, A, lda, B, ldb, C, ldc, cfg, cu_count, segment).threads:
         raise XgemmError(XGEMM_ERR_INVALID_ARG, "threads is not the launch's thread count")
@@ -269,18 +274,18 @@ def xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, cfg, cu_count, seg
     cptr = counts.ctypes.data_as(ctypes.c_void_p)
     if capacity is None:
         rc = lib.xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, ctypes.byref(cfg), cu_count,
-                                       segment, block, None, 0, cptr)
+                                       segment, block, schedule, None, 0, cptr)
         if rc != XGEMM_OK:
             raise XgemmError(rc)
         capacity = int(counts.max())
     out = np.zeros((threads, max(capacity, 1)), dtype=TRACE_EVENT_DTYPE)
     rc = lib.xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, ctypes.byref(cfg), cu_count, segment,
-                                   block, out.ctypes.data_as(ctypes.c_void_p), out.shape[1], cptr)
+                                   block, schedule, out.ctypes.data_as(ctypes.c_void_p), out.shape[1], cptr)
     if rc != XGEMM_OK:
         raise XgemmError(rc)
     if int(counts.max()) > out.shape[1]:
         return xgemm_trace_workgroup(M, N, K, A, lda, B, ldb, C, ldc, W, cfg, cu_count, segment, block,
-                                     threads, int(counts.max()))
+                                     threads, int(counts.max()), schedule)
     return [out[t, :counts[t]] for t in range(threads)]
 
 

@@ -65,5 +65,5 @@ def check_exact(C_gpu: np.ndarray, C_ref: np.ndarray, what: str = ""):
                              % (what, int(bad.sum()), i, j, C_gpu[i, j], C_ref[i, j]))
 
 
-def config(tile, split=1, group_m=4, tail_split=0):
-    return xg.xgemm_config(tile=tile, split_k=split, group_m=group_m, tail_split=tail_split)
+def config(tile, split=1, group_m=4, stream_k=0):
+    return xg.xgemm_config(tile=tile, split_k=split, group_m=group_m, stream_k=stream_k)

@@ -69,34 +69,88 @@ def test_selector_rejects_bad_arguments():
     assert xg.lib.xgemm_select_config(1, 1, 1, 0, 256, None) == xg.XGEMM_ERR_INVALID_ARG
 
 
+PREFIX = 4096   # the workspace's counter prefix
+
+
 def test_workspace_bytes():
-    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0)
+    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, stream_k=0)
     assert xg.xgemm_workspace_bytes(1024, 1024, 4096, 256, cfg) == 0
     cfg.split_k = 16
-    assert xg.xgemm_workspace_bytes(1024, 1024, 65536, 256, cfg) == 16 * 1024 * 1024 * 4
+    assert xg.xgemm_workspace_bytes(1024, 1024, 65536, 256, cfg) == PREFIX + 16 * 1024 * 1024 * 4
     # rows of partials padded to 4 floats; N = 5 also copies B (65536 x 8, after the partials)
-    assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 16 * 10 * 8 * 4 + 65536 * 8 * 2
-    cfg.tail_split = 2                      # tail split needs split_k == 1
+    assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == PREFIX + 16 * 10 * 8 * 4 + 65536 * 8 * 2
+    cfg.stream_k = 1                        # the persistent kernel needs split_k == 1
     assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 0
-    cfg.tail_split, cfg.tile = 0, 99
+    cfg.stream_k, cfg.tile = 0, 99
     assert xg.xgemm_workspace_bytes(10, 5, 65536, 256, cfg) == 0
+    cfg.tile, cfg.split_k, cfg.stream_k = 0, 1, 1024   # at most 1023 workgroups
+    assert xg.xgemm_workspace_bytes(4096, 4096, 4096, 256, cfg) == 0
 
 
-def test_tail_split_plan():
-    # 4096 x 14336 with 256 x 256 tiles: 896 tiles = 3 full waves of 256 + 128
+def _sk_info(M, N, K, stream_k=1, cu=256, tile=0, ldc=None, c=3 << 40):
+    cfg = xg.xgemm_config(tile=tile, split_k=1, group_m=4, stream_k=stream_k)
+    return xg.xgemm_trace_plan(M, N, K, 1 << 40, K, 2 << 40, N, c, N if ldc is None else ldc, cfg, cu, 0)
+
+
+def test_persistent_plan():
+    """The persistent stream-K plan: whole rounds of tiles, then the rest as
+    K-step ranges of at least one tile each; partial sums in the workspace
+    only when tiles are split."""
+    # 4096 x 14336 with 256 x 256 tiles: 896 tiles = 3 rounds of 256 + 128
     w = wl.WORKLOADS["proj4096x14336x4096_fp16"]
-    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=2)
-    assert xg.xgemm_workspace_bytes(w.M, w.N, w.K, 256, cfg) == 128 * 2 * 256 * 256 * 4
-    # not chosen automatically (measured neutral on MI355X)
-    assert xg.xgemm_select_config(w.M, w.N, w.K, xg.XGEMM_FP16, 256).tail_split == 0
-    # whole waves (8192^3: 1024 tiles) need no tail split
-    w8 = wl.WORKLOADS["gemm8192_bf16"]
-    cfg8 = xg.xgemm_select_config(w8.M, w8.N, w8.K, xg.XGEMM_BF16, 256)
-    assert cfg8.tail_split == 0
-    assert xg.xgemm_workspace_bytes(w8.M, w8.N, w8.K, 256, cfg8) == 0
-    # fewer tiles than one wave: nothing to split
-    forced = xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=4)
-    assert xg.xgemm_workspace_bytes(1024, 1024, 4096, 256, forced) == 0
+    info = _sk_info(w.M, w.N, w.K)
+    assert info.family == xg.XGEMM_KERNEL_PERSISTENT and info.grid == 256 and info.threads == 512
+    assert (info.dp_rounds, info.sk_tiles, info.kt) == (2, 384, 64)
+    assert info.workspace_bytes == PREFIX + 2 * 256 * 256 * 256 * 4 and info.data_offset == PREFIX
+    assert info.lds_bytes == 2 * 65536 + 256
+    # whole rounds (8192^3: 1024 tiles on 256 CUs): no split, no workspace
+    info = _sk_info(8192, 8192, 8192)
+    assert (info.dp_rounds, info.sk_tiles, info.kt) == (4, 0, 128)
+    assert info.workspace_bytes == 0
+    # an explicit grid: 20 tiles on 8 workgroups = 1 round, then 12 tiles shared
+    info = _sk_info(1024, 1280, 1024, stream_k=8)
+    assert (info.grid, info.dp_rounds, info.sk_tiles) == (8, 1, 12)
+    # the ordinary kernel where the persistent one does not apply
+    family = lambda *a, **k: _sk_info(*a, **k).family
+    assert family(1024, 1024, 65536) == xg.XGEMM_KERNEL_PIPELINED       # 16 tiles < 256 CUs
+    assert family(4096, 4096 + 8, 4096) == xg.XGEMM_KERNEL_PIPELINED    # N not whole tiles
+    assert family(4096, 4096, 4096 + 8) == xg.XGEMM_KERNEL_PIPELINED    # K not whole steps
+    assert family(4096, 4096, 4096, tile=1) == xg.XGEMM_KERNEL_PIPELINED
+    assert family(4096, 4096, 4096, c=(3 << 40) + 4) == xg.XGEMM_KERNEL_PIPELINED   # C misaligned
+    assert family(4096, 4096, 4096, ldc=(1 << 22)) == xg.XGEMM_KERNEL_PIPELINED     # 256 rows > 4 GiB
+    assert family(4096, 4096, 4096) == xg.XGEMM_KERNEL_PERSISTENT
+    # not chosen by the selector unless it wins (see the selector tests)
+    assert xg.xgemm_select_config(8192, 8192, 8192, xg.XGEMM_BF16, 256).stream_k in (0, 1)
+
+
+def test_persistent_ranges_cover_every_step_once():
+    """Host replica of the kernel's work split (one workgroup's logical id,
+    rounds of whole tiles, then equal K-step ranges of the rest): every
+    (tile, K step) is computed exactly once, every range holds at least one
+    tile's steps, and a tile is split between at most two neighbouring
+    ranges -- its first steps ending range lw, its last starting lw + 1."""
+    for T, P, kt in [(896, 256, 64), (300, 256, 7), (257, 256, 3), (20, 8, 16), (9, 8, 2), (1024, 256, 128),
+                     (511, 256, 64), (13, 13, 5)]:
+        rounds, rem = divmod(T, P)
+        dp = rounds if rem == 0 else rounds - 1
+        sk = 0 if rem == 0 else rem + P
+        seen = {}
+        owners = {}
+        for lw in range(P):
+            s0, s1 = sk * kt * lw // P, sk * kt * (lw + 1) // P
+            if sk:
+                assert s1 - s0 >= kt
+            steps = [(lw + r * P, k) for r in range(dp) for k in range(kt)]
+            steps += [(dp * P + i // kt, i % kt) for i in range(s0, s1)]
+            for t, k in steps:
+                seen[(t, k)] = seen.get((t, k), 0) + 1
+                owners.setdefault(t, {}).setdefault(lw, []).append(k)
+        assert len(seen) == T * kt and set(seen.values()) == {1}, (T, P, kt)
+        for t, by in owners.items():
+            assert len(by) <= 2, (T, P, kt, t)
+            if len(by) == 2:
+                a, b = sorted(by)
+                assert b == a + 1 and min(by[a]) == 0 and max(by[b]) == kt - 1 and max(by[a]) + 1 == min(by[b])
 
 
 def test_single_hip_runtime_in_process():
@@ -116,7 +170,7 @@ def test_single_hip_runtime_in_process():
 
 
 def test_kernel_family_rules():
-    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0)
+    cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, stream_k=0)
     al = 1 << 20  # a 16-byte aligned stand-in address (only alignment is inspected)
     fam = lambda M, N, K, a=al, lda=None, b=al, ldb=None, c=cfg: xg.xgemm_kernel_family(
         M, N, K, a, K if lda is None else lda, b, N if ldb is None else ldb, c)
@@ -137,11 +191,11 @@ def test_kernel_family_rules():
     assert fam(300, 304, 304, a=al + 2) == P and fam(300, 304, short, a=al + 2) == G  # misaligned A
     assert fam(300, 304, 304, lda=308) == P and fam(300, 304, short, lda=124) == G  # lda % 8 != 0
     assert fam(300, 304, 304, ldb=308) == P and fam(300, 304, short, ldb=308) == G  # ldb % 8 != 0
-    cfg16 = xg.xgemm_config(tile=0, split_k=16, group_m=4, tail_split=0)
+    cfg16 = xg.xgemm_config(tile=0, split_k=16, group_m=4, stream_k=0)
     assert fam(1024, 1024, 65536, c=cfg16) == P
     assert fam(1024, 1024, 1024, c=cfg16) == G   # 64-element splits are too short
     assert fam(0, 8, 32) == -1
-    bad = xg.xgemm_config(tile=7, split_k=1, group_m=4, tail_split=0)
+    bad = xg.xgemm_config(tile=7, split_k=1, group_m=4, stream_k=0)
     assert fam(8, 8, 32, c=bad) == -1
 
 
@@ -209,23 +263,23 @@ def test_packed_plan_layout():
     """Packed operands sit after the split partials in the workspace, 256-byte
     aligned, with K and N rounded up to 8 and the kernel reading them with
     those leading dimensions."""
-    cfg = xg.xgemm_config(tile=0, split_k=2, group_m=4, tail_split=0)
+    cfg = xg.xgemm_config(tile=0, split_k=2, group_m=4, stream_k=0)
     M, N, K = 1000, 1001, 2003
     info = xg.xgemm_trace_plan(M, N, K, 1 << 20, K, 1 << 21, N, 1 << 22, N, cfg, 256, 0)
     assert info.family == xg.XGEMM_KERNEL_PIPELINED and info.packed == 3   # K % 8 != 0: both
     assert info.k == 2008 and info.lda == 2008 and info.ldb == 1008
     split_bytes = 2 * M * 1004 * 4                     # two partials of M x ceil4(N) floats
-    assert info.a_offset == (split_bytes + 255) // 256 * 256
+    assert info.a_offset == PREFIX + (split_bytes + 255) // 256 * 256
     assert info.b_offset == (info.a_offset + M * 2008 * 2 + 255) // 256 * 256
     assert info.workspace_bytes == info.b_offset + 2008 * 1008 * 2
     assert xg.xgemm_workspace_bytes(M, N, K, 256, cfg) == info.workspace_bytes
     # only B misses the layout: A is read in place
     info = xg.xgemm_trace_plan(M, N, 2000, 1 << 20, 2000, 1 << 21, N, 1 << 22, N,
-                               xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0), 256, 0)
+                               xg.xgemm_config(tile=0, split_k=1, group_m=4, stream_k=0), 256, 0)
     assert info.packed == 2 and info.a_offset == -1 and info.lda == 2000 and info.ldb == 1008
     # aligned operands: nothing packed
     info = xg.xgemm_trace_plan(1024, 1024, 1024, 1 << 20, 1024, 1 << 21, 1024, 1 << 22, 1024,
-                               xg.xgemm_config(tile=0, split_k=1, group_m=4, tail_split=0), 256, 0)
+                               xg.xgemm_config(tile=0, split_k=1, group_m=4, stream_k=0), 256, 0)
     assert info.packed == 0 and info.a_offset == -1 and info.b_offset == -1 and info.workspace_bytes == 0
 
 
@@ -251,7 +305,7 @@ def test_band_selection_on_workloads():
         assert b.axis == xg.XGEMM_BAND_NONE and b.extent == 0, shape
         whole = xg.xgemm_select_config(*shape, xg.XGEMM_BF16, 256)
         assert (b.body.tile, b.body.split_k, b.body.group_m) == (whole.tile, whole.split_k, whole.group_m)
-        assert (b.band.tile, b.band.split_k, b.band.group_m, b.band.tail_split) == (0, 0, 0, 0)
+        assert (b.band.tile, b.band.split_k, b.band.group_m, b.band.stream_k) == (0, 0, 0, 0)
     # a band of rows
     b = _band(9472, 2048, 1000)
     assert (b.axis, b.extent) == (xg.XGEMM_BAND_ROWS, 8192)
@@ -274,9 +328,9 @@ def test_band_plan_invariants(cu):
                 bm, bn, _, _ = xg.xgemm_tile_info(b.body.tile)
                 along, step = (N, bn) if b.axis == xg.XGEMM_BAND_COLUMNS else (M, bm)
                 assert 0 < b.extent < along and b.extent % step == 0
-                assert b.body.split_k == 1 and b.body.tail_split == 0 and b.body.group_m >= 1
+                assert b.body.split_k == 1 and b.body.stream_k == 0 and b.body.group_m >= 1
                 assert 0 <= b.band.tile < xg.XGEMM_TILE_COUNT and 1 <= b.band.split_k <= 16
-                assert b.band.tail_split == 0 and b.band.group_m >= 1
+                assert b.band.stream_k == 0 and b.band.group_m >= 1
                 # the band's configuration is the selector's for the band's shape
                 rm, rn = (M, N - b.extent) if b.axis == xg.XGEMM_BAND_COLUMNS else (M - b.extent, N)
                 whole = xg.xgemm_select_config(rm, rn, K, xg.XGEMM_BF16, cu)

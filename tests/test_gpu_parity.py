@@ -221,26 +221,147 @@ def test_split_k_integer_exact(split):
     check_exact(run_gpu(A, B, "fp16", config=config(xg.XGEMM_TILE_128x128, split)), C_ref)
 
 
-@pytest.mark.parametrize("tail_split", [2, 4, 8])
-@pytest.mark.parametrize("shape", [(2304, 7936, 2048), (2300, 7930, 1000)], ids=lambda s: "x".join(map(str, s)))
-def test_tail_split(tail_split, shape):
-    """Tiles past the last full wave of 256 workgroups run as a second,
-    split-k launch whose tile partials are reduced into C."""
-    M, N, K = shape  # 9 x 31 = 279 tiles of 256 x 256: a tail of 23
-    A, B, C_ref, S = _case(M, N, K, "bf16", seed=tail_split)
-    cfg = config(xg.XGEMM_TILE_256x256, 1, 4, tail_split)
-    partials = 23 * tail_split * 256 * 256 * 4
-    # N % 8 != 0 (2300 x 7930): B is also copied, padded to 8 columns, after the partials
-    packed_b = 0 if N % 8 == 0 else (partials + 255) // 256 * 256 - partials + K * ((N + 7) // 8 * 8) * 2
-    assert xg.xgemm_workspace_bytes(M, N, K, 256, cfg) == partials + packed_b
-    check_close(run_gpu(A, B, "bf16", config=cfg), C_ref, S, "tail split %d %s" % (tail_split, shape))
+# ---------------------------------------------------------------------------
+# the persistent stream-K kernel (xgemm_config.stream_k)
+# ---------------------------------------------------------------------------
+
+def _sk_cfg(grid=1):
+    """The 256 x 256 tile as the persistent kernel: grid 1 = one workgroup
+    per CU, n > 1 = n workgroups."""
+    return config(xg.XGEMM_TILE_256x256, 1, 4, grid)
 
 
-def test_tail_split_integer_exact():
-    M, N, K = 2304, 7936, 1024
-    A, B = wl.make_int_inputs(M, N, K, "fp16", seed=12)
-    C_ref, _ = oracle.gemm(A, B, "fp16")
-    check_exact(run_gpu(A, B, "fp16", config=config(xg.XGEMM_TILE_256x256, 1, 4, 4)), C_ref, "tail split")
+def _cu():
+    return torch.cuda.get_device_properties(0).multi_processor_count
+
+
+def _sk_info(M, N, K, cfg):
+    return xg.xgemm_trace_plan(M, N, K, 1 << 40, K, 2 << 40, N, 3 << 40, N, cfg, _cu(), 0)
+
+
+def _logical_tile(t, tiles_m, tiles_n, group_m):
+    group = group_m * tiles_n
+    g = t // group
+    first_m = g * group_m
+    gm = min(tiles_m - first_m, group_m)
+    r = t - g * group
+    return first_m + r % gm, r // gm
+
+
+def _split_tiles(info, M, N, group_m=4):
+    """(tile row, tile column) of every tile the plan splits between two
+    workgroups' ranges."""
+    P, kt = info.grid, info.kt
+    isk = info.sk_tiles * kt
+    out = []
+    for lw in range(1, P):
+        s0 = isk * lw // P
+        if s0 % kt:
+            out.append(_logical_tile(info.dp_rounds * P + s0 // kt, M // 256, N // 256, group_m))
+    return out
+
+
+# (M, N, K, workgroups): rounds of whole tiles, then shared ranges of
+# various lengths (1 to 2 tiles, K steps per tile 3 to 16), split tiles in
+# every position
+SK_GRIDS = [(1024, 1280, 1024, 3), (1024, 1280, 1024, 7), (1024, 1280, 1024, 8), (1024, 1280, 1024, 13),
+            (768, 768, 320, 4), (512, 768, 384, 4), (2048, 2048, 768, 24), (2048, 2048, 768, 60),
+            (1536, 2560, 512, 16)]
+
+
+@pytest.mark.parametrize("shape", SK_GRIDS, ids=lambda s: "%dx%dx%d_g%d" % s)
+def test_persistent_kernel_small_grids(shape):
+    M, N, K, grid = shape
+    info = _sk_info(M, N, K, _sk_cfg(grid))
+    assert info.family == xg.XGEMM_KERNEL_PERSISTENT and info.grid == grid
+    for dtype in ("bf16", "fp16"):
+        A, B, C_ref, S = _case(M, N, K, dtype, seed=grid + K)
+        check_close(run_gpu(A, B, dtype, config=_sk_cfg(grid)), C_ref, S, "persistent %s %s" % (shape, dtype))
+
+
+@pytest.mark.parametrize("shape", [(1024, 1280, 1024, 7), (2048, 2048, 768, 60)], ids=lambda s: "%dx%dx%d_g%d" % s)
+def test_persistent_kernel_integer_exact_and_deterministic(shape):
+    """Small-integer inputs: exact whatever the grouping; and real-valued
+    inputs give the same bits on every run (a split tile is always its first
+    K steps plus its last, whichever workgroup finishes it)."""
+    M, N, K, grid = shape
+    A, B = wl.make_int_inputs(M, N, K, "bf16", seed=grid)
+    C_ref, _ = oracle.gemm(A, B, "bf16")
+    check_exact(run_gpu(A, B, "bf16", config=_sk_cfg(grid)), C_ref, "persistent integer %s" % (shape,))
+    A, B = wl.make_inputs(M, N, K, "fp16", "uniform", seed=grid + 1)
+    runs = [run_gpu(A, B, "fp16", config=_sk_cfg(grid)) for _ in range(4)]
+    for r in runs[1:]:
+        assert np.array_equal(r, runs[0])
+
+
+def test_persistent_kernel_counters_left_zero():
+    """A split tile's finisher resets its counter: calls that follow on the
+    same handle -- persistent ones, and split-k and copied-operand calls that
+    use the workspace after its counters -- all stay correct."""
+    h = xg.xgemm_create()
+    try:
+        s = torch.cuda.current_stream().cuda_stream
+        cases = [(1024, 1280, 1024, _sk_cfg(7), 61), (512, 520, 4096, config(xg.XGEMM_TILE_128x128, 4), 62),
+                 (1024, 1280, 1024, _sk_cfg(13), 63), (1000, 1001, 1024, None, 64), (2048, 2048, 768, _sk_cfg(60), 65)]
+        for rep in range(2):
+            for M, N, K, cfg, seed in cases:
+                A, B, C_ref, S = _case(M, N, K, "bf16", seed=seed)
+                dA, dB = to_device(A, "bf16"), to_device(B, "bf16")
+                C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+                args = (h, M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, C.data_ptr(), N, xg.XGEMM_BF16, s)
+                rc = xg.xgemm_run(*args) if cfg is None else xg.xgemm_run_config(*args, cfg)
+                assert rc == xg.XGEMM_OK, xg.xgemm_last_error(h)
+                torch.cuda.synchronize()
+                check_close(C.cpu().numpy(), C_ref, S, "sequence %d %dx%dx%d" % (rep, M, N, K))
+    finally:
+        xg.xgemm_destroy(h)
+
+
+@pytest.mark.parametrize("shape", [(1000, 1280, 1024), (1024, 1000, 1024), (1024, 1280, 1000), (1024, 1024, 65536 // 16)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_persistent_kernel_falls_back(shape):
+    """Where the persistent kernel does not apply (M or N not whole tiles, K
+    not whole steps, fewer tiles than CUs) the tile's ordinary kernel runs."""
+    M, N, K = shape
+    cfg = _sk_cfg(1)
+    assert xg.xgemm_kernel_family(M, N, K, 1 << 20, K, 1 << 20, N, cfg) != xg.XGEMM_KERNEL_PERSISTENT
+    A, B, C_ref, S = _case(M, N, K, "bf16", seed=K % 97)
+    check_close(run_gpu(A, B, "bf16", config=cfg), C_ref, S, "fallback %s" % (shape,))
+
+
+SK_BIG = ["gemm4096_bf16", "gemm8192_bf16", "proj16384x5120x4096_fp16", "proj4096x14336x4096_fp16"]
+
+
+@pytest.mark.parametrize("name", SK_BIG)
+def test_persistent_kernel_full_size_sampled(name):
+    """The full-size workloads through the persistent kernel on every CU:
+    sampled rows, columns and entries, plus every element of up to three
+    split tiles (their two pieces meet in the hand-over) and of the first
+    and last tile."""
+    w = wl.WORKLOADS[name]
+    cfg = _sk_cfg(1)
+    info = _sk_info(w.M, w.N, w.K, cfg)
+    assert info.family == xg.XGEMM_KERNEL_PERSISTENT
+    A, B = wl.workload_inputs(w)
+    C = run_gpu(A, B, w.dtype, config=cfg)
+    rng = np.random.default_rng(4321)
+    rows = np.unique(np.concatenate([[0, w.M - 1], rng.integers(0, w.M, 4)]))
+    Cr, Sr = oracle.gemm_rows(A, B, w.dtype, rows)
+    check_close(C[rows], Cr, Sr, "%s rows" % name)
+    ri, ci = rng.integers(0, w.M, 4096), rng.integers(0, w.N, 4096)
+    c, s = oracle.gemm_entries(A, B, w.dtype, ri, ci)
+    check_close(C[ri, ci][None], c[None], s[None], "%s entries" % name)
+    tiles = _split_tiles(info, w.M, w.N)
+    picks = [tiles[0], tiles[len(tiles) // 2], tiles[-1]] if tiles else []
+    picks += [(0, 0), (w.M // 256 - 1, w.N // 256 - 1)]
+    for tm, tn in picks:
+        ri = np.repeat(np.arange(tm * 256, tm * 256 + 256), 256)
+        ci = np.tile(np.arange(tn * 256, tn * 256 + 256), 256)
+        c, s = oracle.gemm_entries(A, B, w.dtype, ri, ci)
+        check_close(C[ri, ci].reshape(256, 256), c.reshape(256, 256), s.reshape(256, 256),
+                    "%s tile (%d, %d)" % (name, tm, tn))
+    if name == "proj4096x14336x4096_fp16":
+        assert len(tiles) == 128
 
 
 # ---------------------------------------------------------------------------
@@ -376,7 +497,7 @@ def test_workspace_allocation_failure():
         C = torch.full((M, N), 7.0, dtype=torch.float32, device="cuda")
         s = torch.cuda.current_stream().cuda_stream
         split4 = config(xg.XGEMM_TILE_128x128, 4)
-        assert xg.xgemm_workspace_bytes(M, N, K, 256, split4) == 4 * M * N * 4
+        assert xg.xgemm_workspace_bytes(M, N, K, 256, split4) == 4096 + 4 * M * N * 4
         assert xg.xgemm_set_workspace_limit(h, 4096) == xg.XGEMM_OK
         assert xg.xgemm_set_workspace_limit(None, 4096) == xg.XGEMM_ERR_INVALID_ARG
         rc = xg.xgemm_run_config(h, M, N, K, Ad.data_ptr(), K, Bd.data_ptr(), N, C.data_ptr(), N, 0, s, split4)
@@ -523,6 +644,27 @@ def test_full_size_workload_sampled(name):
     ci = rng.integers(0, w.N, 4096)
     c, s = oracle.gemm_entries(A, B, w.dtype, ri, ci)
     check_close(C[ri, ci][None], c[None], s[None], "%s entries" % name)
+
+
+def test_full_size_8192_every_element():
+    """The 8192^3 bf16 benchmark workload (uniform[-1,1], seed 2) in the
+    benchmark's plan: every one of the 67M outputs against the oracle's full
+    product (about 30 s of host time on 16 cores)."""
+    w = wl.WORKLOADS["gemm8192_bf16"]
+    A, B = wl.workload_inputs(w)
+    C = run_gpu(A, B, w.dtype)
+    C_ref, S = oracle.gemm(A, B, w.dtype)
+    check_close(C, C_ref, S, "8192^3 every element")
+
+
+def test_full_size_8192_integer_every_element():
+    """8192^3 with integer entries in [-8, 8], every output bit-exact against
+    the oracle's full product."""
+    M = N = K = 8192
+    A, B = wl.make_int_inputs(M, N, K, "bf16", seed=2)
+    C = run_gpu(A, B, "bf16")
+    C_ref, _ = oracle.gemm(A, B, "bf16")
+    check_exact(C, C_ref, "8192^3 integer every element")
 
 
 def test_full_size_8192_integer_exact_sampled():

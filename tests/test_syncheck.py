@@ -176,8 +176,8 @@ def test_per_lane_read_granules():
 # 2. the kernel's own traces
 # ---------------------------------------------------------------------------
 
-def cfg(tile, split=1, group_m=4, tail_split=0):
-    return xg.xgemm_config(tile, split, group_m, tail_split)
+def cfg(tile, split=1, group_m=4, stream_k=0):
+    return xg.xgemm_config(tile, split, group_m, stream_k)
 
 
 def stages(tile):
@@ -234,12 +234,82 @@ def test_kernel_split_k_partials(tile, split):
     assert rep.ok, [str(v) for v in rep.violations]
 
 
-def test_kernel_tail_split():
-    # 3 x 3 tiles of 128 x 128 on a 2-CU device (4 slots): one tail tile
-    # runs as a second launch with 4-way split partials
-    rep = sc.check_launch(384, 384, 64 * 16, cfg(2, 1, 4, 4), cu_count=2)
-    assert rep.segments == 2
+# the persistent stream-K kernel on small grids: (M, N, K, workgroups)
+SK_CASES = [
+    (512, 768, 64 * 6, 4),     # 6 tiles on 4: all shared (1.5 tiles each)
+    (768, 768, 64 * 5, 4),     # 9 tiles on 4: one round, then 5 shared, kt = 5
+    (1024, 1280, 64 * 4, 8),   # 20 tiles on 8: one round, then 12 shared (6 steps of 4 each)
+    (512, 512, 64 * 3, 3),     # 4 tiles on 3: 4 tiles shared, ranges of 4 steps over kt = 3
+    (1024, 512, 64 * 3, 8),    # 8 tiles on 8: one whole round, nothing split
+    (512, 256, 64 * 4, 2),     # 2 tiles on 2: one whole round
+]
+
+
+@pytest.mark.parametrize("M,N,K,grid", SK_CASES, ids=lambda v: str(v))
+def test_persistent_kernel_is_race_free(M, N, K, grid):
+    """Every workgroup of the persistent kernel, under both orders in which
+    the pieces of a split tile count in: LDS ordering across the tiles of a
+    range (the next tile's loads in flight during the last steps, the
+    previous tile's stores under the next one's first rows), loads inside A,
+    B and the workspace, C stored exactly once, partial sums written once and
+    read only where written."""
+    c = cfg(0, 1, 4, grid)
+    info = xg.xgemm_trace_plan(M, N, K, sc.BASE_A, K, sc.BASE_B, N, sc.BASE_C, N, c, 256, 0)
+    assert info.family == xg.XGEMM_KERNEL_PERSISTENT and info.grid == grid
+    rep = sc.check_launch(M, N, K, c)
     assert rep.ok, [str(v) for v in rep.violations]
+
+
+def test_persistent_kernel_trace_structure():
+    """Ranges of 1.5 tiles (6 tiles of 256 x 256 on 4 workgroups, K = 384, all
+    shared out):
+    one barrier after the prologue and one per K step, plus the hand-over's
+    barriers; direct loads in the prologue (two steps) and in every step
+    (the last two steps repeat the range's last step); the split tile's pieces
+    publish (schedule 0: the last steps, at the start of their range) or add
+    (the first steps, at the end of theirs) as expected."""
+    M, N, K, grid = 512, 768, 64 * 6, 4
+    c = cfg(0, 1, 4, grid)
+    info = xg.xgemm_trace_plan(M, N, K, sc.BASE_A, K, sc.BASE_B, N, sc.BASE_C, N, c, 256, 0)
+    assert (info.dp_rounds, info.sk_tiles, info.kt) == (0, 6, 6)
+    for block in range(grid):
+        lw = (block % 8) * (grid // 8) + block // 8 if block < (grid // 8) * 8 else block
+        s0, s1 = 6 * 6 * lw // grid, 6 * 6 * (lw + 1) // grid
+        G = s1 - s0
+        ev, counts = sc.trace_workgroup(M, N, K, K, N, N, c, 256, 0, block, info.threads)
+        waves = sc.wave_streams(ev, counts)
+        tail, head = s0 % 6 != 0, s1 % 6 != 0
+        # prologue + per step, publish (release + count) and hand-over words
+        extra = (2 if tail else 0) + (1 if head else 0)
+        for ws in waves:
+            assert (ws.op == sc.LDS_LOAD).sum() == (G + 2) * 8
+            assert (ws.op == sc.BARRIER).sum() == 1 + G + extra, (block, lw, G, tail, head)
+        # thread 0's partial-sum loads (16 bytes each): only the head adds them
+        t0 = ev[0][:counts[0]]
+        part_loads = ((t0["op"] == sc.LOAD) & (t0["arg"] == 16)).sum()
+        assert part_loads == (32 if head else 0)
+
+
+def test_persistent_kernel_planted_mistake_is_caught():
+    """The checker is not blind to the persistent kernel: the same traces with
+    the wait before one K step's barrier removed (a planted mistake, in the
+    trace only) fail with a read-after-write race."""
+    M, N, K, grid = 512, 768, 64 * 6, 4
+    c = cfg(0, 1, 4, grid)
+    info = xg.xgemm_trace_plan(M, N, K, sc.BASE_A, K, sc.BASE_B, N, sc.BASE_C, N, c, 256, 0)
+    ev, counts = sc.trace_workgroup(M, N, K, K, N, N, c, 256, 0, 1, info.threads)
+    waves = sc.wave_streams(ev, counts)
+    assert not sc.check_workgroup_lds(waves, info.lds_bytes)
+    # drop every wave's second vector-memory wait (the first K step's, for
+    # the second step's loads): that stage is then read right after the
+    # barrier before its direct loads are known to have landed
+    for ws in waves:
+        idx = np.nonzero(ws.op == sc.WAIT_VM)[0][1]
+        keep = np.ones(len(ws.op), bool)
+        keep[idx] = False
+        ws.op, ws.arg, ws.lds, ws.addr = ws.op[keep], ws.arg[keep], ws.lds[keep], ws.addr[keep]
+    kinds = {v.kind for v in sc.check_workgroup_lds(waves, info.lds_bytes)}
+    assert "raw" in kinds
 
 
 @pytest.mark.parametrize("shape,c,lds", [
@@ -453,9 +523,32 @@ def test_packed_operand_bounds_are_enforced(monkeypatch):
 def test_duplicate_workgroup_output_is_caught(monkeypatch):
     real = sc.trace_workgroup
     monkeypatch.setattr(sc, "trace_workgroup",
-                        lambda M, N, K, lda, ldb, ldc, c, cu, seg, block, threads, capacity=None:
-                        real(M, N, K, lda, ldb, ldc, c, cu, seg, 0, threads, capacity))
+                        lambda M, N, K, lda, ldb, ldc, c, cu, seg, block, threads, capacity=None, schedule=0:
+                        real(M, N, K, lda, ldb, ldc, c, cu, seg, 0, threads, capacity, schedule))
     rep = sc.check_launch(512, 512, 256, cfg(0))
+    assert "coverage" in {v.kind for v in rep.violations}
+    # the persistent kernel's workgroups: one range traced for all
+    rep = sc.check_launch(512, 768, 64 * 6, cfg(0, 1, 4, 4))
+    assert "coverage" in {v.kind for v in rep.violations}
+
+
+def test_persistent_partial_sum_races_are_caught(monkeypatch):
+    """Under a schedule where both pieces of every split tile find the other
+    already counted in (not a real order: one of them must count in first),
+    both would add the other's partial and store C: the coverage check
+    reports the double stores."""
+    real = sc.trace_workgroup
+
+    def both(*args, **kw):
+        ev0, c0 = real(*args, **dict(kw, schedule=0))
+        ev1, c1 = real(*args, **dict(kw, schedule=1))
+        # the head's events come from schedule 0 (it adds), the tail's from 1
+        # (it adds too): keep whichever trace stores more of C per thread
+        n0 = ((ev0["op"] == sc.STORE) & (ev0["arg"] == 16)).sum()
+        n1 = ((ev1["op"] == sc.STORE) & (ev1["arg"] == 16)).sum()
+        return (ev0, c0) if n0 >= n1 else (ev1, c1)
+    monkeypatch.setattr(sc, "trace_workgroup", both)
+    rep = sc.check_launch(512, 768, 64 * 6, cfg(0, 1, 4, 4), schedules=(0,))
     assert "coverage" in {v.kind for v in rep.violations}
 
 
