@@ -10,10 +10,17 @@ one JSON line.  ``value`` is the whole-job throughput over the K timed steps,
 bracketed by device synchronisation; ``roofline.achieved`` uses the average
 duration of the GEMM kernel from HIP events recorded on the stream the kernel
 is launched on (for a call the selector cuts into a body and a band of C,
-both launches: ``config.band`` then describes the band).  The paper's own protocol (5 warm-up + 100 timed iterations,
-mean of the inter-quartile range; Section 6) is reported beside it.
+both launches: ``config.band`` then describes the band).  The paper's own
+protocol (5 warm-up + 100 timed iterations, mean of the inter-quartile range;
+Section 6) is reported beside it.  Before the warm-up steps, untimed calls
+run for --settle seconds (at least 64 calls): from idle, the GPU's power
+controller takes tens of calls to settle, and the first ones run 10-35%
+slower than the sustained rate that the timed steps are meant to measure
+(``settle`` in the line says how many calls that took).  ``counters`` and
+``roofline.traffic`` are not measured by this run: they come from the
+committed rocprofv3 summary of the same kernel sources, taken on another box.
 
-Usage: python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--workload NAME]
+Usage: python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--settle 0.5] [--workload NAME]
        [--no-cpu-baseline] [--no-comparator] [--copy-calibration BYTES]
        python bench.py --sweep M,N,K [M,N,K ...] [--dtype bf16] [--rounds 5]
        python bench.py --summarize-counters DIR [--workload NAME]   (CPU only)
@@ -52,7 +59,7 @@ GEMV_METRIC = "GEMV TFLOP/s and %% of the MI355X HBM-bound GEMV peak (fp32, %d²
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "counters_%s.json")
 # device code whose change invalidates committed counters of each kernel
 # family (the kernel the counters describe is also named in them)
-KERNEL_SOURCES = {"gemm": ("gemm_kernel.hpp",), "gemv": ("gemv_kernel.hpp",)}
+KERNEL_SOURCES = {"gemm": ("gemm_kernel.hpp", "sk_kernel.hpp"), "gemv": ("gemv_kernel.hpp",)}
 
 
 def family(workload: str) -> str:
@@ -171,6 +178,37 @@ def summarize_counters(directory: str, workload: str) -> str:
     return path
 
 
+def settle(step, seconds: float, min_calls: int = 64) -> dict:
+    """Run `step` until the GPU has reached its sustained clock under the
+    power cap: at least min_calls calls and `seconds` of wall time (the host
+    waits for the GPU every 16 calls, so the time is the GPU's).  From idle,
+    the first tens of large GEMMs run 10-35% slower than the sustained rate
+    while the power controller settles (8192^3: 823, 773, 933, 1029, 1004,
+    946 ... us, then 734 us from about the 50th call on)."""
+    import torch
+    t0 = time.perf_counter()
+    n = 0
+    while n < min_calls or time.perf_counter() - t0 < seconds:
+        step()
+        n += 1
+        if n % 16 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+    return {"calls": n, "seconds": round(time.perf_counter() - t0, 3)}
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), for the baseline's record."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, A, B, budget_s: float = 12.0):
     """The oracle, untuned, on a bounded sample: the first R rows of C."""
     import oracle
@@ -189,6 +227,7 @@ def cpu_baseline(w, A, B, budget_s: float = 12.0):
     t = time.perf_counter() - t0
     flops = 2.0 * rows * w.N * w.K
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": "rows 0..%d of C (%d x %d outputs, K=%d) of the %s workload, fp64, including "
                       "decoding B; %.1f s" % (rows - 1, rows, w.N, w.K, w.name, t)}
 
@@ -208,6 +247,7 @@ def gemv_cpu_baseline(w, A, x, budget_s: float = 10.0):
         oracle.gemv(A, x)
     t = (time.perf_counter() - t0) / reps
     return {"value": round(w.flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "cpu": cpu_model(),
             "sample": "the whole %s workload (%d x %d), fp64, %d repetitions of %.3f s" % (w.name, w.M, w.K, reps, t)}
 
 
@@ -232,6 +272,7 @@ def bench_gemv(args, w):
         if rc != xg.XGEMM_OK:
             raise xg.XgemmError(rc, xg.xgemm_last_error(h))
 
+    settled = settle(step, args.settle)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -280,6 +321,7 @@ def bench_gemv(args, w):
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": settled,
         "ms_per_step": round(wall / args.steps * 1e3, 5),
         "higher_is_better": True,
         "scaling": "strong",
@@ -378,7 +420,7 @@ def sweep_shape(M: int, N: int, K: int, dtype: str = "bf16", rounds: int = 5) ->
             times[key].append(e0.elapsed_time(e1) / reps * 1e3)
     med = {k: statistics.median(v) for k, v in times.items()}
     best = min(med, key=med.get)
-    chosen = "band" if band.axis != xg.XGEMM_BAND_NONE else ("sk" if sel.stream_k else (sel.tile, sel.split_k))
+    chosen = "band" if band.axis != xg.XGEMM_BAND_NONE else ("sk" if band.body.stream_k else (sel.tile, sel.split_k))
     name = lambda k: k if isinstance(k, str) else list(k)
     out = {"shape": [M, N, K], "dtype": dtype, "selected": name(chosen), "selected_us": round(med[chosen], 2),
            "best": name(best), "best_us": round(med[best], 2), "loss": round(med[chosen] / med[best], 3),
@@ -396,6 +438,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle", type=float, default=0.5,
+                    help="seconds of untimed calls before the warmup steps, so that the timed steps run at "
+                         "the GPU's sustained clock (0: only the minimum of 64 calls)")
     ap.add_argument("--workload", default="gemm8192_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true")
@@ -447,6 +492,7 @@ def main():
     code = xg.XGEMM_BF16 if w.dtype == "bf16" else xg.XGEMM_FP16
     plan = xg.xgemm_select_band(w.M, w.N, w.K, code, torch.cuda.get_device_properties(dev).multi_processor_count)
     cfg = plan.body  # the whole call's configuration, or the body's when C is cut in two
+    kernel_family = xg.xgemm_kernel_family(w.M, w.N, w.K, A.data_ptr(), w.K, B.data_ptr(), w.N, cfg)
 
     def step():
         rc = xg.xgemm_run(h, w.M, w.N, w.K, A.data_ptr(), w.K, B.data_ptr(), w.N, C.data_ptr(), w.N,
@@ -468,6 +514,7 @@ def main():
                 Ab[b].copy_(torch.from_numpy(a_bits.view(np.int16)).to(dev).view(tdt))
                 Bb[b].copy_(torch.from_numpy(b_bits.view(np.int16)).to(dev).view(tdt))
         Cb = torch.empty((L, w.M, w.N), dtype=torch.float32, device=dev)
+        settled = settle(lambda: xg.bmm(Ab, Bb, out=Cb), args.settle)
         for _ in range(args.warmup):
             xg.bmm(Ab, Bb, out=Cb)
         torch.cuda.synchronize()
@@ -480,13 +527,16 @@ def main():
         t = e0.elapsed_time(e1) * 1e-3 / args.steps
         print(json.dumps({"metric": "strided batched GEMM TFLOP/s", "value": round(L * w.flops / t / 1e12, 2),
                           "unit": "TFLOP/s", "batch": L, "ms_per_step": round(t * 1e3, 4), "dtype": w.dtype,
+                          "settle": settled,
                           "config": {"workload": w.name, "M": w.M, "N": w.N, "K": w.K}}), flush=True)
         return
 
+    settled = settle(step, args.settle)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    print("bench: warmup done", file=sys.stderr, flush=True)
+    print("bench: settled (%d calls, %.2f s), warmup done" % (settled["calls"], settled["seconds"]),
+          file=sys.stderr, flush=True)
 
     # timed region: exactly K steps, bracketed by synchronisation; per-step
     # HIP events on the launch stream give the kernel durations
@@ -548,6 +598,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle": settled,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "strong",
@@ -556,7 +607,9 @@ def main():
         "data": "synthetic (seeded uniform[-1,1], seed %d)" % w.seed if w.dist == "uniform"
                 else "synthetic (seeded normal(0,%g), seed %d)" % (w.param, w.seed),
         "config": dict({"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "out": "fp32",
-                        "tile": cfg.tile, "split_k": cfg.split_k},
+                        "tile": cfg.tile, "split_k": cfg.split_k,
+                        "kernel": "persistent" if kernel_family == xg.XGEMM_KERNEL_PERSISTENT else
+                        "pipelined" if kernel_family == xg.XGEMM_KERNEL_PIPELINED else "general"},
                        **({} if plan.axis == xg.XGEMM_BAND_NONE else {"band": {
                            "axis": "columns" if plan.axis == xg.XGEMM_BAND_COLUMNS else "rows",
                            "body_extent": plan.extent, "tile": plan.band.tile,
@@ -567,9 +620,15 @@ def main():
                      "frac": round(achieved / peak, 4),
                      "traffic": traffic},
         "comparator": comparator,
-        "counters": None if counters is None else {
+        # counters and roofline.traffic are not measured by this run: they
+        # come from the committed rocprofv3 --pmc summary of the same kernel
+        # sources, taken on another MI355X
+        "counters": None if counters is None else dict({
             k: counters.get(k) for k in ("mfma_busy_pct", "clock_ghz", "lds_bank_conflict_pct",
                                          "hbm_read_bytes_per_launch", "hbm_write_bytes_per_launch")},
+            source="committed profile profiles/counters_%s.json (another box; kernel sources %s)"
+                   % (w.name, counters.get("kernel_source_sha256"))),
+        "traffic_source": None if traffic is None else "committed profile profiles/counters_%s.json" % w.name,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

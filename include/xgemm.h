@@ -149,11 +149,17 @@ int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K,
  * For callers that cannot allocate device memory: code being captured into
  * a HIP graph, tight serving loops, harnesses that forbid hipMalloc.  The
  * same product as xgemm_run, with the same plan, kernels and arguments, and
- * the same result bit for bit, but the split-k partials and operand copies
- * live in a static array of the library (XGEMM_NOALLOC_SCRATCH_BYTES per
- * GPU, held from the first xgemm_create on that GPU until the process ends)
- * instead of the handle's workspace.  The call allocates nothing and frees
- * nothing; nothing in the array needs to start at zero.  Every call of this
+ * the same result bit for bit, but the split-k partials, the persistent
+ * kernel's partial sums and counters, and operand copies live in a static
+ * array of the library (XGEMM_NOALLOC_SCRATCH_BYTES per GPU, held from the
+ * first xgemm_create on that GPU until the process ends) instead of the
+ * handle's workspace.  One exception: where xgemm_run's plan is the
+ * persistent kernel with shared tiles whose partial sums do not fit the
+ * array, the call takes the plan xgemm_run would take without that kernel
+ * (banded or not); its result agrees with xgemm_run's within the accuracy
+ * contract, not necessarily in the last bits.  The call allocates nothing
+ * and frees nothing; the library keeps the array's counters at zero between
+ * calls, and nothing else in it needs to start at zero.  Every call of this
  * entry point on one GPU shares that GPU's array, so calls that overlap in
  * time on one GPU (on different streams, or through different handles) race
  * and must be ordered by the caller.  Returns XGEMM_ERR_INVALID_ARG, with
@@ -229,13 +235,17 @@ typedef struct xgemm_band {
     int32_t reserved;   /* 0 */
     int64_t extent;     /* columns or rows of C in the body (0 with XGEMM_BAND_NONE) */
     xgemm_config body;  /* the body's configuration; with XGEMM_BAND_NONE, the whole call's
-                           (as xgemm_select_config) */
+                           (as xgemm_select_config, with stream_k = 1 where the call runs the
+                           persistent kernel: the 256 x 256 tile in four or more whole
+                           rounds of CUs, or three or more and a half) */
     xgemm_config band;  /* the band's configuration (zeros with XGEMM_BAND_NONE) */
 } xgemm_band;
 
 /*
  * The plan xgemm_run would use for this problem on a device with cu_count
- * compute units (host-only; touches no GPU).  XGEMM_ERR_INVALID_ARG for
+ * compute units (host-only; touches no GPU).  A persistent plan
+ * (body.stream_k = 1) becomes the plan without the persistent kernel when
+ * the operands' alignment or leading dimensions do not suit that kernel.  XGEMM_ERR_INVALID_ARG for
  * negative sizes, an unknown dtype, cu_count < 1 or out == NULL.
  */
 int xgemm_select_band(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, xgemm_band *out);

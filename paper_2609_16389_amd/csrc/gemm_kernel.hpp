@@ -499,6 +499,11 @@ __device__ __forceinline__ void barrier_only()
 // so the code order between fences is the issue order.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
+// Cache-policy bits of the buffer load/store builtins on gfx950: nt
+// (streaming) and sc1 (device scope).
+constexpr int kCpolNt = 2;
+constexpr int kCpolSc1 = 16;
+
 // Chunk swizzle of the A tile for rows of ROWB bytes (4 or 8 chunks): with
 // 64-byte rows, four rows share a 256-byte bank window and rows r, r+4,
 // r+8, r+12 get distinct slots; with 128-byte rows, two rows share a window
@@ -579,23 +584,33 @@ struct DeviceOps {
     {
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, 0);
     }
-    __device__ __forceinline__ void buf_store1(Rsrc r, uint32_t voff, uint32_t soff, float v) const
+    // streaming store (nt): the XCD's L2 does not keep the line for reuse
+    __device__ __forceinline__ void buf_store4_nt(Rsrc r, uint32_t voff, uint32_t soff, f32x4 v) const
     {
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, voff, soff, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, kCpolNt);
     }
-    __device__ __forceinline__ f32x4 buf_load4(Rsrc r, uint32_t voff, uint32_t soff) const
+    // partial sums: device-scope (sc1) stores and loads.  A device-scope
+    // store, once complete, is visible to loads of that scope from every
+    // XCD, and such loads do not return stale copies from a CU's L1 or an
+    // XCD's L2; so the hand-over needs neither a write-back of the whole L2
+    // (buffer_wbl2) nor an invalidation (buffer_inv).
+    __device__ __forceinline__ void buf_store4_dev(Rsrc r, uint32_t voff, uint32_t soff, f32x4 v) const
     {
-        return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, kCpolSc1);
     }
-    // every global store of this wave written back past the XCD's L2 and
-    // complete (buffer_wbl2, s_waitcnt vmcnt(0)); agent scope
-    __device__ __forceinline__ void fence_release() const { __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent"); }
-    // later loads miss this CU's L1 and the XCD's L2 lines that other
-    // agents' writes may have made stale (buffer_inv); agent scope
-    __device__ __forceinline__ void fence_acquire() const { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+    __device__ __forceinline__ f32x4 buf_load4_dev(Rsrc r, uint32_t voff, uint32_t soff) const
+    {
+        return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kCpolSc1));
+    }
+    // every store of this wave complete (s_waitcnt vmcnt(0)): for the
+    // device-scope partial sums, visible to every XCD
+    __device__ __forceinline__ void stores_done() const { wait_vmcnt<0>(); }
+    // the counters: device-scope atomics (relaxed: the partial sums they
+    // publish are device-scope accesses themselves, ordered by stores_done
+    // before the count and by the count's value before the loads)
     __device__ __forceinline__ int flag_load(int *f) const
     {
-        return __hip_atomic_load(f, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+        return __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __device__ __forceinline__ void flag_store(int *f, int v) const
     {
@@ -604,7 +619,7 @@ struct DeviceOps {
     // atomic add; returns the value before it
     __device__ __forceinline__ int flag_add(int *f, int v) const
     {
-        return __hip_atomic_fetch_add(f, v, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        return __hip_atomic_fetch_add(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __device__ __forceinline__ void lds_write4(char *q, int v, bool on) const
     {

@@ -16,24 +16,25 @@
 //     start of range lw + 1.
 // The LDS pipeline runs across tile boundaries: during a tile's last K
 // steps the loads of the next tile's first steps are already in flight, and
-// a finished tile's C stores are issued from each accumulator row just
-// before that row's first MFMA of the next tile (which starts from zero), so
-// the stores drain under the next tile's work.
+// a finished tile's C stores (streaming stores) are issued at the start of
+// the next tile's first step, whose MFMAs start from zero, so the stores
+// drain under the next tile's work.
 //
 // A tile split between ranges lw and lw + 1 (its slot is lw + 1) is
 // finished by whichever of its two pieces completes second, without any
-// wait: each piece first reads the slot's counter; if the other piece has
-// already counted in, it adds that piece's partial sum and stores C.
-// Otherwise it writes its own partial sum to its half of the slot, makes it
-// visible past its XCD's L2 (agent-scope release), and counts in with an
-// atomic add; the piece that finds the other already counted (the add
-// returns 1) adds the other's partial and stores C, and resets the counter,
-// so every call leaves all counters zero.  The sum is always the tile's
-// first steps plus its last steps (fp32 addition is commutative, so the bits
-// do not depend on which piece finishes it).  In the usual order the last
-// steps (at the start of range lw + 1) are done long before the first steps
-// (at the end of range lw), so one partial is written and read per split
-// tile.
+// wait.  The piece of the last steps (at the start of range lw + 1) writes
+// its partial sum to its half of the slot with device-scope stores, waits
+// for them to complete and counts in with an atomic add.  The piece of the
+// first steps (at the end of range lw) reads the counter: if the other
+// piece has counted in, it adds that partial (device-scope loads) and
+// stores C; otherwise it publishes its own partial the same way.  Whichever
+// piece's add returns 1 forms the sum and resets the counter, so every call
+// leaves all counters zero.  The sum is always the tile's first steps plus
+// its last steps (fp32 addition is commutative, so the bits do not depend on
+// which piece finishes it).  In the usual order the last steps are done long
+// before the first steps, so one partial is written and read per split
+// tile.  Device-scope accesses make the partials visible across XCDs
+// without writing back or invalidating whole L2 caches.
 #pragma once
 
 #include "gemm_kernel.hpp"
@@ -222,13 +223,15 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
     // within 4 GiB and C 16-byte aligned).  Lane l owns row lr, columns
     // 4 kg .. 4 kg + 3 of each 16 x 16 block.
     const uint32_t c_lane = (uint32_t)((lr * p.ldc + kg * 4) * 4);
-    // C of logical tile (tm, tn), block row i (FN 16-byte stores per lane)
+    // C of logical tile (tm, tn), block row i (FN 16-byte stores per lane):
+    // streaming stores, whose lines an XCD's L2 does not keep, so that they
+    // take no L2 space from the operands of the tiles that follow
     auto store_c_row = [&](int tm, int tn, int i) {
         const auto r = ops.rsrc(p.C + (int64_t)(tm * BM + wm * TM) * p.ldc + tn * BN + wn * TN);
         const uint32_t soff = (uint32_t)(i * MI * p.ldc * 4);
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-            ops.buf_store4(r, c_lane + j * MI * 4, soff, acc[i][j]);
+            ops.buf_store4_nt(r, c_lane + j * MI * 4, soff, acc[i][j]);
     };
     // partial sums of slot s, piece 0 (first steps) or 1 (last steps): block
     // (i, j) of wave w is 64 lanes x 16 bytes, contiguous, in the
@@ -355,9 +358,9 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
         for (int i = 0; i < FM; ++i)
 #pragma unroll
             for (int j = 0; j < FN; ++j)
-                ops.buf_store4(r, p_lane + j * 1024, i * FN * 1024, acc[i][j]);
-        // every wave's partial written back past its L2, then count in
-        ops.fence_release();
+                ops.buf_store4_dev(r, p_lane + j * 1024, i * FN * 1024, acc[i][j]);
+        // every wave's partial complete (visible to every XCD), then count in
+        ops.stores_done();
         ops.barrier();
         int old = 0;
         if (tid == 0)
@@ -373,35 +376,31 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
             v = ops.flag_load(p.flags + s);
         if (broadcast(bcast, v) != 1 && publish(s, 0) != 1)
             return;
-        ops.fence_acquire();
         const auto r = part_rsrc(s, 1);
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
 #pragma unroll
             for (int j = 0; j < FN; ++j)
-                acc[i][j] = acc[i][j] + ops.buf_load4(r, p_lane + j * 1024, i * FN * 1024);
+                acc[i][j] = acc[i][j] + ops.buf_load4_dev(r, p_lane + j * 1024, i * FN * 1024);
             store_c_row(tm, tn, i);
             ops.fence();
         }
         if (tid == 0)
             ops.flag_store(p.flags + s, 0);
     };
-    // The last steps of the tile (tm, tn) of slot s are in acc (mid-range):
-    // publish them; if the first steps were published already, C is the sum
-    // of the two partials, read back.
-    auto finish_tail = [&](int s, int tm, int tn) {
-        if (publish(s, 1) != 1)
-            return;
-        ops.fence_acquire();
+    // Both partials of slot s are published (this workgroup's last steps
+    // counted in second): C of the tile (tm, tn) is their sum, read back
+    // (the same sum as finish_head's: fp32 addition commutes).
+    auto combine = [&](int s, int tm, int tn) {
         const auto r0 = part_rsrc(s, 0), r1 = part_rsrc(s, 1);
         const auto rc = ops.rsrc(p.C + (int64_t)(tm * BM + wm * TM) * p.ldc + tn * BN + wn * TN);
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
 #pragma unroll
             for (int j = 0; j < FN; ++j) {
-                const accT x = ops.buf_load4(r0, p_lane + j * 1024, i * FN * 1024) +
-                               ops.buf_load4(r1, p_lane + j * 1024, i * FN * 1024);
-                ops.buf_store4(rc, c_lane + j * MI * 4, (uint32_t)(i * MI * p.ldc * 4), x);
+                const accT x = ops.buf_load4_dev(r0, p_lane + j * 1024, i * FN * 1024) +
+                               ops.buf_load4_dev(r1, p_lane + j * 1024, i * FN * 1024);
+                ops.buf_store4_nt(rc, c_lane + j * MI * 4, (uint32_t)(i * MI * p.ldc * 4), x);
             }
             ops.fence();
         }
@@ -436,14 +435,47 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
             gb[0][j] = frag_B(0, 0, j);
     }
 
-    // Steps cc.g .. g_end - 1 (lc: the step loaded two ahead).  A whole tile
-    // that ends on the way is stored under the next step's first rows, or
-    // right away after the last step.
+    // A range's stream-K part starting inside a tile begins with that
+    // tile's last steps (split with range lw - 1, slot lw): they end at
+    // step tail_end - 1.
+    const int k_sk = rg.s0 % p.kt;
+    const int tail_end = (rg.s1 > rg.s0 && k_sk > 0) ? rg.gdp + (p.kt - k_sk) : 0;
+
+    // Steps 0 .. G - 1, lc the step loaded two ahead.  Most steps are plain:
+    // the step computed and the one loaded lie in one tile and nothing ends;
+    // they run in an inner loop that only moves the load pointers along K.
+    // The steps around a tile boundary take the general path: the first
+    // step of a tile stores the previous whole tile under its MFMAs
+    // (flush), and the last step of a range stores its whole tile.  The
+    // range's tail (if any) and its head are handed over between passes and
+    // after the last.
     bool flush = false;   // the tile (ftm, ftn) is stored under the next step
     int ftm = 0, ftn = 0;
     int kfirst = cc.k;    // K step the current unit started at
-    auto run = [&](int g_end) {
-        for (; cc.g < g_end; advance(cc)) {
+    bool tail_combine = false;
+    int ttm = 0, ttn = 0;
+    // two passes: up to the end of the tail (if any), then the rest
+#pragma nounroll
+    for (int pass = tail_end > 0 ? 0 : 1; pass < 2; ++pass) {
+        const int g_end = pass == 0 ? tail_end : L.G;
+        while (cc.g < g_end) {
+            if (cc.k == 0 || cc.g == rg.gdp)
+                kfirst = cc.k;
+            // plain steps: lc advances within its tile, cc stays two behind it
+            int n = (!flush && cc.t == lc.t) ? min(p.kt - 1 - lc.k, L.G - 1 - lc.g) : 0;
+            if (n > 0) {
+                Src s = src_of(lc);
+                for (; n > 0; --n) {
+                    s.a += BK;
+                    s.b += (int64_t)BK * ldb;
+                    kstep(cc.g, false, 0, 0, s);
+                    ++cc.g;
+                    ++cc.k;
+                }
+                lc.g = cc.g + 1;
+                lc.k = cc.k + 1;
+            }
+            // one general step
             if (cc.k == 0 || cc.g == rg.gdp)
                 kfirst = cc.k;
             const bool fl = flush;
@@ -463,22 +495,18 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
                     clear_acc();
                 }
             }
+            advance(cc);
         }
-    };
-    // A range's stream-K part starting inside a tile begins with that
-    // tile's last steps (split with range lw - 1, slot lw): they end at
-    // step tail_end - 1.
-    const int k_sk = rg.s0 % p.kt;
-    const int tail_end = (rg.s1 > rg.s0 && k_sk > 0) ? rg.gdp + (p.kt - k_sk) : 0;
-    if (tail_end > 0) {
-        run(tail_end);
-        int t, k, tm, tn;
-        sk_locate(p, rg, lw, tail_end - 1, t, k);
-        logical_tile(t, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
-        finish_tail(lw, tm, tn);
-        clear_acc();
+        if (pass == 0) {
+            // the tail's last steps: publish them; if the first steps are
+            // already published, the sum is formed after the range
+            tail_combine = publish(lw, 1) == 1;
+            int t, k;
+            sk_locate(p, rg, lw, tail_end - 1, t, k);
+            logical_tile(t, p.tiles_m, p.tiles_n, p.group_m, ttm, ttn);
+            clear_acc();
+        }
     }
-    run(L.G);
     ops.template wait_vm<0>();   // the repeated last loads landed: no LDS write in flight at exit
     // A range ending inside a tile ends with that tile's first steps (split
     // with range lw + 1, slot lw + 1).
@@ -488,6 +516,8 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
         logical_tile(t, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
         finish_head(lw + 1, tm, tn);
     }
+    if (tail_combine)
+        combine(lw, ttm, ttn);
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN, int DT>

@@ -214,7 +214,27 @@ struct BandPlan {
     xgemm_config body{}, band{};
 };
 
-BandPlan select_band(int64_t M, int64_t N, int64_t K, int cu_count)
+// The persistent kernel (one workgroup per CU walking its tiles, each
+// tile's C stores draining under the next tile's MFMAs) in place of one
+// workgroup per 256 x 256 tile, where it measured faster: four or more whole
+// rounds (8192^3 742 against 762 us, 8192 x 14336 x 4096 679 against 701,
+// 12288 x 12288 x 4096 fp16 917 against 988; 8192 x 8192 x 2048 even), or
+// three or more and a half (4096 x 14336 x 4096 fp16 390 against 398 with
+// the band plan).  With two or three whole rounds it measured 3-6% slower.
+// Other partial rounds stay with the band plans: there the shared ranges
+// start at many different K offsets, so the tiles an XCD runs at one time
+// share no operand rows in its L2 (6144^3: 404 against 357 us).
+bool use_persistent(int64_t M, int64_t N, int64_t K, int cu_count, const xgemm_config &whole)
+{
+    const TileShape &t = kTiles[XGEMM_TILE_256x256];
+    if (whole.tile != XGEMM_TILE_256x256 || whole.split_k != 1 || M % t.bm || N % t.bn || K % t.bk ||
+        cu_count < 1 || cu_count >= kMaxSkGrid)
+        return false;
+    const int64_t tiles = (M / t.bm) * (N / t.bn), rounds = tiles / cu_count, rem = tiles % cu_count;
+    return rem == 0 ? rounds >= 4 : (2 * rem == cu_count && rounds >= 3);
+}
+
+BandPlan select_band(int64_t M, int64_t N, int64_t K, int cu_count, bool persistent = true)
 {
     BandPlan out;
     xgemm_config whole;
@@ -222,6 +242,10 @@ BandPlan select_band(int64_t M, int64_t N, int64_t K, int cu_count)
     out.body = whole;
     if (whole.split_k > 1)
         return out;  // a K split already spreads the problem over the GPU
+    if (persistent && use_persistent(M, N, K, cu_count, whole)) {
+        out.body.stream_k = 1;
+        return out;
+    }
     {
         // one round or less: the call already takes one tile time, and a
         // partial round runs at a higher clock than the model charges
@@ -729,10 +753,20 @@ int plan_call(int cu_count, int64_t M, int64_t N, int64_t K, const void *A, int6
     if (forced) {
         band.body = *forced;
     } else {
-        band = select_band(M, N, K, cu_count);
+        band = select_band(M, N, K, cu_count, allow_sk);
     }
     if (!allow_sk)
         band.body.stream_k = band.band.stream_k = 0;
+    if (!forced && band.body.stream_k > 0) {
+        // operands the persistent kernel cannot take as they are (alignment,
+        // leading dimensions): the plan without it, banded or not
+        Plan probe;
+        const int rc = make_plan(M, N, K, A, lda, B, ldb, C, ldc, band.body, cu_count, &probe, true);
+        if (rc != XGEMM_OK)
+            return rc;
+        if (!probe.seg[0].sk)
+            band = select_band(M, N, K, cu_count, false);
+    }
     if (band.axis == XGEMM_BAND_NONE) {
         cp->parts = 1;
         cp->M[0] = M, cp->N[0] = N, cp->A[0] = A, cp->B[0] = B, cp->C[0] = C;
@@ -1279,19 +1313,14 @@ struct TraceOps {
     {
         push(XGEMM_TRACE_STORE, 16, 0, (int64_t)(uintptr_t)(r + voff + soff));
     }
-    void buf_store1(Rsrc r, uint32_t voff, uint32_t soff, float) const
-    {
-        push(XGEMM_TRACE_STORE, 4, 0, (int64_t)(uintptr_t)(r + voff + soff));
-    }
-    xgemm_dev::f32x4 buf_load4(Rsrc r, uint32_t voff, uint32_t soff) const
+    void buf_store4_nt(Rsrc r, uint32_t voff, uint32_t soff, xgemm_dev::f32x4 v) const { buf_store4(r, voff, soff, v); }
+    void buf_store4_dev(Rsrc r, uint32_t voff, uint32_t soff, xgemm_dev::f32x4 v) const { buf_store4(r, voff, soff, v); }
+    xgemm_dev::f32x4 buf_load4_dev(Rsrc r, uint32_t voff, uint32_t soff) const
     {
         push(XGEMM_TRACE_LOAD, 16, 0, (int64_t)(uintptr_t)(r + voff + soff));
         return xgemm_dev::f32x4{0, 0, 0, 0};
     }
-    // the release fence ends with s_waitcnt vmcnt(0); the acquire fence
-    // (a cache invalidation) waits for nothing
-    void fence_release() const { push(XGEMM_TRACE_WAIT_VM, 0, 0, 0); }
-    void fence_acquire() const {}
+    void stores_done() const { push(XGEMM_TRACE_WAIT_VM, 0, 0, 0); }
     // counter reads and atomic adds are vector-memory loads with a result
     int flag_load(int *f) const
     {

@@ -292,20 +292,28 @@ def _band(M, N, K, dtype=xg.XGEMM_BF16, cu=256):
 
 
 def test_band_selection_on_workloads():
-    # 4096 x 14336 x 4096: 896 tiles of 256 x 256 are 3.5 rounds on 256 CUs;
-    # the body takes 3 whole rounds (12288 columns) and a 256 x 128 band
-    # the last 2048 columns in one round
-    b = _band(4096, 14336, 4096, xg.XGEMM_FP16)
-    assert (b.axis, b.extent, b.body.tile, b.body.split_k) == (xg.XGEMM_BAND_COLUMNS, 12288, 0, 1)
-    assert (b.band.tile, b.band.split_k) == (1, 1)
-    # whole rounds, one round or less, and split-k plans are not banded
-    for shape in [(8192, 8192, 8192), (16384, 5120, 4096), (4096, 4096, 4096), (1024, 1024, 65536),
-                  (256, 256, 256), (2048, 5120, 4096), (3072, 3072, 4096)]:
+    # 6144^3: 576 tiles of 256 x 256 are 2.25 rounds on 256 CUs; the body
+    # takes 21 tile columns (504 tiles) and a 128 x 128 band the last 768
+    # columns
+    b = _band(6144, 6144, 6144)
+    assert (b.axis, b.extent, b.body.tile, b.body.split_k, b.body.stream_k) == (xg.XGEMM_BAND_COLUMNS, 5376, 0, 1, 0)
+    assert (b.band.tile, b.band.split_k, b.band.stream_k) == (2, 1, 0)
+    # the persistent kernel: four or more whole rounds of 256 x 256 tiles
+    # (8192^3: 4, 16384 x 5120: 5), or three and a half (4096 x 14336: 896
+    # tiles); not banded
+    for shape, sk in [((8192, 8192, 8192), 1), ((16384, 5120, 4096), 1), ((4096, 14336, 4096), 1),
+                      ((6144, 8192, 4096), 0), ((4096, 8192, 4096), 0), ((4096, 4096, 4096), 0),
+                      ((5120, 5120, 5120), 0), ((1024, 1024, 65536), 0), ((256, 256, 256), 0),
+                      ((2048, 5120, 4096), 0), ((3072, 3072, 4096), 0)]:
         b = _band(*shape)
         assert b.axis == xg.XGEMM_BAND_NONE and b.extent == 0, shape
         whole = xg.xgemm_select_config(*shape, xg.XGEMM_BF16, 256)
         assert (b.body.tile, b.body.split_k, b.body.group_m) == (whole.tile, whole.split_k, whole.group_m)
+        assert b.body.stream_k == sk, shape
         assert (b.band.tile, b.band.split_k, b.band.group_m, b.band.stream_k) == (0, 0, 0, 0)
+    # the rule is in whole rounds of the device's CUs: 8192^3 on 304 CUs is
+    # 3.37 rounds
+    assert _band(8192, 8192, 8192, xg.XGEMM_BF16, 304).body.stream_k == 0
     # a band of rows
     b = _band(9472, 2048, 1000)
     assert (b.axis, b.extent) == (xg.XGEMM_BAND_ROWS, 8192)
