@@ -163,15 +163,19 @@ def summarize_counters(directory: str, workload: str) -> str:
     out["dispatches"] = per[main]["dispatches"]
     out.update({k: v for k, v in per[main].items() if k != "dispatches"})
     out["kernels"] = per
-    # kernels of one call: each dispatched once per call (the GEMM launches,
-    # the reduction, operand copies)
-    calls = min(p["dispatches"] for p in per.values())
+    # kernels of one call: dispatched once per call like the GEMM kernel (the
+    # GEMM launches, the reduction, operand copies); kernels dispatched less
+    # often are one-time set-up (zeroing a new workspace's counters)
+    calls = per[main]["dispatches"]
+    in_call = {k: p for k, p in per.items() if p["dispatches"] >= calls}
     out["per_call"] = {
-        "kernels": len(per),
-        "median_duration_ns": sum(p["median_duration_ns"] * p["dispatches"] / calls for p in per.values()),
+        "kernels": len(in_call),
+        "median_duration_ns": sum(p["median_duration_ns"] * p["dispatches"] / calls for p in in_call.values()),
+        "setup_kernels": sorted(k for k in per if k not in in_call),
     }
-    if all("hbm_bytes_per_launch" in p for p in per.values()):
-        out["per_call"]["hbm_bytes"] = sum(p["hbm_bytes_per_launch"] * p["dispatches"] / calls for p in per.values())
+    if all("hbm_bytes_per_launch" in p for p in in_call.values()):
+        out["per_call"]["hbm_bytes"] = sum(p["hbm_bytes_per_launch"] * p["dispatches"] / calls
+                                           for p in in_call.values())
     path = COUNTERS_FILE % workload
     with open(path, "w") as f:
         json.dump(out, f, indent=1, sort_keys=True)
