@@ -51,6 +51,10 @@ struct SkParams {
     int64_t lda, ldb, ldc;
     int M, N, K;      // M and N multiples of the tile, K of the K step
     int tiles_m, tiles_n, group_m;
+    int tiles_per;    // tiles of one problem (tiles_m * tiles_n); tile t is tile t % tiles_per of
+                      // problem t / tiles_per, whose A, B and C start stride_a, stride_b,
+                      // stride_c elements (times the problem index) after A, B and C
+    int64_t stride_a, stride_b, stride_c;
     int kt;           // K steps per tile (K is a multiple of the K step)
     int grid;         // workgroups of the launch (one per CU)
     int dp_rounds;    // rounds of whole tiles before the shared ones
@@ -72,6 +76,19 @@ __host__ __device__ __forceinline__ int sk_logical(int block, int grid)
 {
     const int per = grid / kNumXcd;
     return block < per * kNumXcd ? (block % kNumXcd) * per + block / kNumXcd : block;
+}
+
+// A tile of the launch: problem b, tile (m, n) of that problem's C.
+struct SkTile {
+    int b, m, n;
+};
+
+__host__ __device__ __forceinline__ SkTile sk_tile_of(const SkParams &p, int t)
+{
+    SkTile r;
+    r.b = t / p.tiles_per;
+    logical_tile(t - r.b * p.tiles_per, p.tiles_m, p.tiles_n, p.group_m, r.m, r.n);
+    return r;
 }
 
 // The K-step range of logical workgroup lw: steps [0, gdp) are its whole
@@ -223,11 +240,15 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
     // within 4 GiB and C 16-byte aligned).  Lane l owns row lr, columns
     // 4 kg .. 4 kg + 3 of each 16 x 16 block.
     const uint32_t c_lane = (uint32_t)((lr * p.ldc + kg * 4) * 4);
-    // C of logical tile (tm, tn), block row i (FN 16-byte stores per lane):
-    // streaming stores, whose lines an XCD's L2 does not keep, so that they
-    // take no L2 space from the operands of the tiles that follow
-    auto store_c_row = [&](int tm, int tn, int i) {
-        const auto r = ops.rsrc(p.C + (int64_t)(tm * BM + wm * TM) * p.ldc + tn * BN + wn * TN);
+    // this wave's block of C in tile u
+    auto c_base = [&](const SkTile &u) {
+        return p.C + u.b * p.stride_c + (int64_t)(u.m * BM + wm * TM) * p.ldc + u.n * BN + wn * TN;
+    };
+    // C of tile u, block row i (FN 16-byte stores per lane): streaming
+    // stores, whose lines an XCD's L2 does not keep, so that they take no L2
+    // space from the operands of the tiles that follow
+    auto store_c_row = [&](const SkTile &u, int i) {
+        const auto r = ops.rsrc(c_base(u));
         const uint32_t soff = (uint32_t)(i * MI * p.ldc * 4);
 #pragma unroll
         for (int j = 0; j < FN; ++j)
@@ -244,10 +265,11 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
     // A cursor walks the range step by step, without divisions except where
     // it enters a new tile.
     struct Cursor {
-        int g, t, k, tm, tn;
+        int g, t, k;
+        SkTile u;
     };
     const SkRange &L = rg;
-    auto set_tile = [&](Cursor &c) { logical_tile(c.t, p.tiles_m, p.tiles_n, p.group_m, c.tm, c.tn); };
+    auto set_tile = [&](Cursor &c) { c.u = sk_tile_of(p, c.t); };
     auto start = [&](Cursor &c, int g) {
         c.g = g;
         sk_locate(p, rg, lw, g, c.t, c.k);
@@ -270,15 +292,15 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
     };
     auto src_of = [&](const Cursor &c) {
         Src s;
-        const int m0 = c.tm * BM, n0 = c.tn * BN;
-        s.a = p.A + (int64_t)m0 * lda + c.k * BK;
-        s.b = p.B + (int64_t)c.k * BK * ldb + n0;
+        const int m0 = c.u.m * BM, n0 = c.u.n * BN;
+        s.a = p.A + c.u.b * p.stride_a + (int64_t)m0 * lda + c.k * BK;
+        s.b = p.B + c.u.b * p.stride_b + (int64_t)c.k * BK * ldb + n0;
         return s;
     };
 
     // --- one K step g of the range ---
     // With `flush` (once per tile) the step first stores the previous tile's
-    // accumulators (tile (ftm, ftn)) and clears them; the stores drain under
+    // accumulators (tile f) and clears them; the stores drain under
     // the step's MFMAs.  Sub-step 0 works from ga[0] / gb[0] and reads
     // sub-step 1 of the same stage.  Then R
     // rows of sub-step 1, the waits, the barrier, and the other rows of
@@ -288,12 +310,12 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
     // stage no later step reads) and the reads take what those loads
     // brought, so no branch interrupts the MFMAs; the range waits for its
     // last loads before it ends.
-    auto kstep = [&](int g, bool flush, int ftm, int ftn, const Src &s) {
+    auto kstep = [&](int g, bool flush, const SkTile &f, const Src &s) {
         const int stage = g & 1, next = stage ^ 1;
         if (__builtin_expect(flush, 0)) {
 #pragma unroll
             for (int i = 0; i < FM; ++i)
-                store_c_row(ftm, ftn, i);
+                store_c_row(f, i);
             clear_acc();
         }
 #pragma unroll
@@ -367,10 +389,10 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
             old = ops.flag_add(p.flags + s, 1);
         return broadcast(bcast + 64, old);
     };
-    // The first steps of the tile (tm, tn) of slot s are in acc (the end of
+    // The first steps of tile u (slot s) are in acc (the end of
     // the range): add the last steps' partial once published, row by row,
     // and store C; or publish the first steps when the last are not done.
-    auto finish_head = [&](int s, int tm, int tn) {
+    auto finish_head = [&](int s, const SkTile &u) {
         int v = 0;
         if (tid == 0)
             v = ops.flag_load(p.flags + s);
@@ -382,18 +404,18 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
 #pragma unroll
             for (int j = 0; j < FN; ++j)
                 acc[i][j] = acc[i][j] + ops.buf_load4_dev(r, p_lane + j * 1024, i * FN * 1024);
-            store_c_row(tm, tn, i);
+            store_c_row(u, i);
             ops.fence();
         }
         if (tid == 0)
             ops.flag_store(p.flags + s, 0);
     };
     // Both partials of slot s are published (this workgroup's last steps
-    // counted in second): C of the tile (tm, tn) is their sum, read back
+    // counted in second): C of tile u is their sum, read back
     // (the same sum as finish_head's: fp32 addition commutes).
-    auto combine = [&](int s, int tm, int tn) {
+    auto combine = [&](int s, const SkTile &u) {
         const auto r0 = part_rsrc(s, 0), r1 = part_rsrc(s, 1);
-        const auto rc = ops.rsrc(p.C + (int64_t)(tm * BM + wm * TM) * p.ldc + tn * BN + wn * TN);
+        const auto rc = ops.rsrc(c_base(u));
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
 #pragma unroll
@@ -449,11 +471,11 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
     // (flush), and the last step of a range stores its whole tile.  The
     // range's tail (if any) and its head are handed over between passes and
     // after the last.
-    bool flush = false;   // the tile (ftm, ftn) is stored under the next step
-    int ftm = 0, ftn = 0;
+    bool flush = false;   // the tile f is stored under the next step
+    SkTile f{0, 0, 0};
     int kfirst = cc.k;    // K step the current unit started at
     bool tail_combine = false;
-    int ttm = 0, ttn = 0;
+    SkTile tt{0, 0, 0};   // the tail's tile
     // two passes: up to the end of the tail (if any), then the rest
 #pragma nounroll
     for (int pass = tail_end > 0 ? 0 : 1; pass < 2; ++pass) {
@@ -468,7 +490,7 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
                 for (; n > 0; --n) {
                     s.a += BK;
                     s.b += (int64_t)BK * ldb;
-                    kstep(cc.g, false, 0, 0, s);
+                    kstep(cc.g, false, f, s);
                     ++cc.g;
                     ++cc.k;
                 }
@@ -482,16 +504,15 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
             flush = false;
             if (lc.g + 1 < L.G)
                 advance(lc);   // step g + 2, or the last step again
-            kstep(cc.g, fl, ftm, ftn, src_of(lc));
+            kstep(cc.g, fl, f, src_of(lc));
             if (kfirst == 0 && cc.k == p.kt - 1) {
                 if (cc.g + 1 < L.G) {
                     flush = true;
-                    ftm = cc.tm;
-                    ftn = cc.tn;
+                    f = cc.u;
                 } else {
 #pragma unroll
                     for (int i = 0; i < FM; ++i)
-                        store_c_row(cc.tm, cc.tn, i);
+                        store_c_row(cc.u, i);
                     clear_acc();
                 }
             }
@@ -503,7 +524,7 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
             tail_combine = publish(lw, 1) == 1;
             int t, k;
             sk_locate(p, rg, lw, tail_end - 1, t, k);
-            logical_tile(t, p.tiles_m, p.tiles_n, p.group_m, ttm, ttn);
+            tt = sk_tile_of(p, t);
             clear_acc();
         }
     }
@@ -511,13 +532,12 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
     // A range ending inside a tile ends with that tile's first steps (split
     // with range lw + 1, slot lw + 1).
     if (L.G > 0 && (rg.s1 > rg.s0) && rg.s1 % p.kt != 0) {
-        int t, k, tm, tn;
+        int t, k;
         sk_locate(p, rg, lw, L.G - 1, t, k);
-        logical_tile(t, p.tiles_m, p.tiles_n, p.group_m, tm, tn);
-        finish_head(lw + 1, tm, tn);
+        finish_head(lw + 1, sk_tile_of(p, t));
     }
     if (tail_combine)
-        combine(lw, ttm, ttn);
+        combine(lw, tt);
 }
 
 template <int BM, int BN, int BK, int WGM, int WGN, int DT>

@@ -224,13 +224,13 @@ struct BandPlan {
 // Other partial rounds stay with the band plans: there the shared ranges
 // start at many different K offsets, so the tiles an XCD runs at one time
 // share no operand rows in its L2 (6144^3: 404 against 357 us).
-bool use_persistent(int64_t M, int64_t N, int64_t K, int cu_count, const xgemm_config &whole)
+bool use_persistent(int64_t M, int64_t N, int64_t K, int cu_count, const xgemm_config &whole, int64_t batch = 1)
 {
     const TileShape &t = kTiles[XGEMM_TILE_256x256];
     if (whole.tile != XGEMM_TILE_256x256 || whole.split_k != 1 || M % t.bm || N % t.bn || K % t.bk ||
         cu_count < 1 || cu_count >= kMaxSkGrid)
         return false;
-    const int64_t tiles = (M / t.bm) * (N / t.bn), rounds = tiles / cu_count, rem = tiles % cu_count;
+    const int64_t tiles = (M / t.bm) * (N / t.bn) * batch, rounds = tiles / cu_count, rem = tiles % cu_count;
     return rem == 0 ? rounds >= 4 : (2 * rem == cu_count && rounds >= 3);
 }
 
@@ -503,6 +503,33 @@ int trim_split(int64_t K, int split, int bk, int64_t *kc)
     return split;
 }
 
+// The persistent kernel's schedule of `tiles` tiles of kt K steps over
+// `grid` workgroups (one per CU): whole rounds, then the K steps of the last
+// partial round and one more round shared out as equal ranges (each at least
+// a tile's steps, so a tile is split between at most two ranges).  Returns
+// false, leaving g unchanged, where the schedule does not apply; the
+// workspace it needs (two partial sums per slot, none without shared tiles)
+// is sk_workspace(g).
+bool sk_schedule(Segment &g, int64_t tiles, int64_t kt, int grid)
+{
+    if (kt < 1 || grid < 1 || grid >= kMaxSkGrid || tiles < grid || tiles * kt >= 0x7fffffff)
+        return false;
+    const int64_t rounds = tiles / grid, rem = tiles % grid;
+    g.sk = true;
+    g.grid = grid;
+    g.kt = (int)kt;
+    g.dp_rounds = (int)(rem == 0 ? rounds : rounds - 1);
+    g.sk_tiles = (int)(rem == 0 ? 0 : rem + grid);
+    return true;
+}
+
+size_t sk_workspace(const Segment &g)
+{
+    return g.sk && g.sk_tiles > 0 ? (size_t)2 * g.grid * kTiles[XGEMM_TILE_256x256].bm *
+                                        kTiles[XGEMM_TILE_256x256].bn * sizeof(float)
+                                  : 0;
+}
+
 // Plan a call for K > 0 and M, N > 0 with configuration cfg on a device
 // with cu_count CUs.  Device pointers are only inspected for alignment.
 int make_plan_with(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, const void *B, int64_t ldb,
@@ -626,20 +653,10 @@ int make_plan_with(int64_t M, int64_t N, int64_t K, const void *A, int64_t lda, 
     // with 256 of its rows within 4 GiB
     if (cfg.stream_k > 0 && cfg.tile == XGEMM_TILE_256x256 && !pk.a && !pk.b) {
         Segment &g = out->seg[0];
-        const int grid = cfg.stream_k == 1 ? cu_count : cfg.stream_k;
-        const int64_t kt = K / t.bk;
-        if (g.dma && M % t.bm == 0 && N % t.bn == 0 && K % t.bk == 0 && kt >= 1 && grid >= 1 &&
-            grid < kMaxSkGrid && tiles >= grid && tiles * kt < 0x7fffffff && g.p.vec_c &&
-            (int64_t)t.bm * ldc * 4 < ((int64_t)1 << 32)) {
-            const int64_t rounds = tiles / grid, rem = tiles % grid;
-            g.sk = true;
-            g.grid = grid;
-            g.kt = (int)kt;
-            g.dp_rounds = (int)(rem == 0 ? rounds : rounds - 1);
-            g.sk_tiles = (int)(rem == 0 ? 0 : rem + grid);
-            // two partial sums per slot (a slot per workgroup)
-            out->ws = g.sk_tiles > 0 ? (size_t)2 * grid * t.bm * t.bn * sizeof(float) : 0;
-        }
+        if (g.dma && M % t.bm == 0 && N % t.bn == 0 && K % t.bk == 0 && g.p.vec_c &&
+            (int64_t)t.bm * ldc * 4 < ((int64_t)1 << 32))
+            if (sk_schedule(g, tiles, K / t.bk, cfg.stream_k == 1 ? cu_count : cfg.stream_k))
+                out->ws = sk_workspace(g);
     }
     return finish();
 }
@@ -870,6 +887,10 @@ xgemm_dev::SkParams sk_params(const Segment &g, int *flags, float *part)
     q.tiles_m = g.p.tiles_m;
     q.tiles_n = g.p.tiles_n;
     q.group_m = g.p.group_m;
+    q.tiles_per = g.p.tiles_m * g.p.tiles_n;
+    q.stride_a = g.p.batch > 1 ? g.p.stride_a : 0;
+    q.stride_b = g.p.batch > 1 ? g.p.stride_b : 0;
+    q.stride_c = g.p.batch > 1 ? g.p.stride_c : 0;
     q.kt = g.kt;
     q.grid = (int)g.grid;
     q.dp_rounds = g.dp_rounds;
@@ -1045,6 +1066,28 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
     g.p.vec_ab = g.p.vec_ab && (sa % 8 == 0) && (sb % 8 == 0);
     g.p.vec_c = g.p.vec_c && (sc % 4 == 0);
     g.dma = dma_eligible(g.p, kTiles[plan.tile].bm, pk.b);
+    // the persistent kernel over the tiles of all problems, as xgemm_run
+    // takes it for one problem with as many tiles
+    const TileShape &t256 = kTiles[XGEMM_TILE_256x256];
+    if (!pk.a && !pk.b && g.dma && g.p.vec_c && use_persistent(M, N, K, h->cu_count, cfg, batch) &&
+        (int64_t)t256.bm * ldc * 4 < ((int64_t)1 << 32) &&
+        sk_schedule(g, (M / t256.bm) * (N / t256.bn) * batch, K / t256.bk, h->cu_count)) {
+        const size_t ws = sk_workspace(g);
+        if (ws > 0 && (rc = acquire_workspace(h, ws, s)) != XGEMM_OK)
+            return rc;
+        char *const base = ws > 0 ? (char *)h->workspace : nullptr;
+        e = launch_sk(dtype, sk_params(g, (int *)base, base ? (float *)ws_data(base) : nullptr), s);
+        rc = XGEMM_OK;
+        if (e != hipSuccess) {
+            set_error(h, "gemm launch", e);
+            rc = XGEMM_ERR_HIP;
+        }
+        if (ws > 0) {
+            const int rc2 = release_workspace(h, s);
+            rc = rc == XGEMM_OK ? rc2 : rc;
+        }
+        return rc;
+    }
     e = launch_tile(plan.tile, g.dma, dtype, g.p, (int)(g.grid * batch), s);
     rc = XGEMM_OK;
     if (e != hipSuccess) {

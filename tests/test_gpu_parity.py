@@ -883,6 +883,46 @@ def test_strided_batched_shared_a_and_padding():
         assert np.all(Ch[b * sc + M * ldc:(b + 1) * sc] == 777.0)
 
 
+@pytest.mark.parametrize("L", [64, 56], ids=["4rounds", "3.5rounds"])
+def test_strided_batched_persistent(L):
+    """Enough 256 x 256 tiles over the problems for the persistent kernel:
+    64 problems of 1024 x 1024 (16 tiles each) are four whole rounds on 256
+    CUs; 56 are three and a half, with tiles shared between workgroups (one
+    problem's tile may be split between two of them) and their partial sums
+    in the workspace.  C has padded rows and a padded batch stride, which
+    stay untouched; every problem is checked against the oracle."""
+    M = N = 1024
+    K = 512
+    cu = torch.cuda.get_device_properties(0).multi_processor_count
+    if cu != 256:
+        pytest.skip("the case is sized for 256 CUs")
+    As, Bs = _batched_case(L, M, N, K, "bf16", seed=L)
+    A = torch.stack([to_device(a, "bf16") for a in As])
+    B = torch.stack([to_device(b, "bf16") for b in Bs])
+    ldc, sc = N + 4, (M + 1) * (N + 4)
+    Cbuf = torch.full((L * sc,), 777.0, dtype=torch.float32, device="cuda")
+    h = xg.handle()
+    rc = xg.xgemm_run_strided_batched(h, L, M, N, K, A.data_ptr(), K, M * K, B.data_ptr(), N, K * N,
+                                      Cbuf.data_ptr(), ldc, sc, xg.XGEMM_BF16,
+                                      torch.cuda.current_stream().cuda_stream)
+    assert rc == xg.XGEMM_OK, xg.xgemm_last_error(h)
+    torch.cuda.synchronize()
+    Ch = Cbuf.cpu().numpy()
+    for b in range(L):
+        C_ref, S = oracle.gemm(As[b], Bs[b], "bf16")
+        blk = Ch[b * sc:b * sc + M * ldc].reshape(M, ldc)
+        check_close(blk[:, :N], C_ref, S, "persistent batch %d of %d" % (b, L))
+        assert np.all(blk[:, N:] == 777.0)
+        assert np.all(Ch[b * sc + M * ldc:(b + 1) * sc] == 777.0)
+    # the same call again gives the same bits (the counters were left zero)
+    Cbuf2 = torch.full((L * sc,), 777.0, dtype=torch.float32, device="cuda")
+    assert xg.xgemm_run_strided_batched(h, L, M, N, K, A.data_ptr(), K, M * K, B.data_ptr(), N, K * N,
+                                        Cbuf2.data_ptr(), ldc, sc, xg.XGEMM_BF16,
+                                        torch.cuda.current_stream().cuda_stream) == xg.XGEMM_OK
+    torch.cuda.synchronize()
+    assert np.array_equal(Cbuf2.cpu().numpy(), Ch)
+
+
 def test_strided_batched_integer_exact_and_single():
     L, M, N, K = 2, 256, 256, 512
     As, Bs = [], []
