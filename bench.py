@@ -8,11 +8,13 @@ One step is one call of xgemm_run on the 8192 x 8192 x 8192 bf16 workload
 (entries uniform on [-1, 1], seed 2), inputs already resident in HBM.  Prints
 one JSON line.  ``value`` is the whole-job throughput over the K timed steps,
 bracketed by device synchronisation; ``roofline.achieved`` uses the average
-duration of the GEMM kernel from HIP events recorded on the stream the kernel
-is launched on (for a call the selector cuts into a body and a band of C,
-both launches: ``config.band`` then describes the band).  The paper's own
+duration of the GEMM kernel from two HIP events recorded on the stream the
+kernel is launched on around the K steps, during which the stream runs the
+kernels back to back (for a call the selector cuts into a body and a band of
+C, both launches: ``config.band`` then describes the band).  The paper's own
 protocol (5 warm-up + 100 timed iterations, mean of the inter-quartile range;
-Section 6) is reported beside it.  Before the warm-up steps, untimed calls
+Section 6) is reported beside it, from a second sample of max(K, 100) calls
+with events around each call.  Before the warm-up steps, untimed calls
 run for --settle seconds (at least 64 calls): from idle, the GPU's power
 controller takes tens of calls to settle, and the first ones run 10-35%
 slower than the sustained rate that the timed steps are meant to measure
@@ -20,7 +22,7 @@ slower than the sustained rate that the timed steps are meant to measure
 ``roofline.traffic`` are not measured by this run: they come from the
 committed rocprofv3 summary of the same kernel sources, taken on another box.
 
-Usage: python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--settle 0.5] [--workload NAME]
+Usage: python bench.py [--gpus 1] [--steps 100] [--warmup 5] [--settle 0.5] [--workload NAME] [--no-persistent]
        [--no-cpu-baseline] [--no-comparator] [--copy-calibration BYTES]
        python bench.py --sweep M,N,K [M,N,K ...] [--dtype bf16] [--rounds 5]
        python bench.py --summarize-counters DIR [--workload NAME]   (CPU only)
@@ -201,6 +203,47 @@ def settle(step, seconds: float, min_calls: int = 64) -> dict:
     return {"calls": n, "seconds": round(time.perf_counter() - t0, 3)}
 
 
+def timed_region(step, steps: int, stream):
+    """Exactly `steps` calls, bracketed by device synchronisation: the wall
+    time, and the time between two HIP events recorded on the launch stream
+    around them (the GPU is busy with the calls back to back in between, so
+    that time over `steps` is the average duration of one call's kernels).
+    Events between the calls would cost time of their own (0.8% at 8192^3,
+    8% at 4096^3), so they are left to the per-call sample below."""
+    import torch
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall, e0.elapsed_time(e1) * 1e-3
+
+
+def per_call_times(step, calls: int, stream) -> np.ndarray:
+    """Durations (s) of `calls` more calls, each between two HIP events: the
+    sample of the paper's protocol (mean of the inter-quartile range)."""
+    import torch
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(calls)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(calls)]
+    torch.cuda.synchronize()
+    for i in range(calls):
+        starts[i].record(stream)
+        step()
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    return np.array([a.elapsed_time(b) for a, b in zip(starts, ends)]) * 1e-3
+
+
+def iqr_mean(per: np.ndarray) -> float:
+    srt = np.sort(per)
+    q = len(srt) // 4
+    return float(srt[q:len(srt) - q].mean()) if len(srt) >= 4 else float(srt.mean())
+
+
 def cpu_model() -> str:
     """The host CPU's model name (/proc/cpuinfo), for the baseline's record."""
     try:
@@ -280,22 +323,12 @@ def bench_gemv(args, w):
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        starts[i].record(stream)
-        step()
-        ends[i].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)]) * 1e-3
+    wall, ev = timed_region(step, args.steps, stream)
+    per = per_call_times(step, max(args.steps, 100), stream)
     value = w.flops * args.steps / wall / 1e12
-    achieved_gbs = w.alg_bytes / float(per.mean()) / 1e9
+    achieved_gbs = w.alg_bytes / (ev / args.steps) / 1e9
     peak_tflops = PEAK_HBM_GBS * 1e9 * 2 / 4 / 1e12
-    srt = np.sort(per)
-    q = len(srt) // 4
-    iqr_mean = float(srt[q:len(srt) - q].mean()) if len(srt) >= 4 else float(srt.mean())
+    iqr = iqr_mean(per)
     if args.copy_calibration:
         n = args.copy_calibration // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -334,7 +367,7 @@ def bench_gemv(args, w):
         "data": "synthetic (seeded uniform[-1,1], seed %d)" % w.seed,
         "config": {"workload": w.name, "M": w.M, "K": w.K, "rows": cfg.rows, "unroll": cfg.unroll},
         "pct_of_peak": round(100.0 * value / peak_tflops, 2),
-        "paper_protocol_iqr_mean_tflops": round(w.flops / iqr_mean / 1e12, 4),
+        "paper_protocol_iqr_mean_tflops": round(w.flops / iqr / 1e12, 4),
         "roofline": {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": round(achieved_gbs / PEAK_HBM_GBS, 4),
                      "traffic": None if counters is None else counters.get("hbm_bytes_per_launch")},
@@ -448,6 +481,9 @@ def main():
     ap.add_argument("--workload", default="gemm8192_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-comparator", action="store_true")
+    ap.add_argument("--no-persistent", action="store_true",
+                    help="switch the persistent kernel off for the bench handle (xgemm_set_persistent): the plan "
+                         "xgemm_run takes without it, to compare the two")
     ap.add_argument("--copy-calibration", type=int, default=0,
                     help="also run a plain device copy of this many bytes (counter calibration)")
     ap.add_argument("--batch", type=int, default=0,
@@ -493,8 +529,11 @@ def main():
     C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
     h = xg.handle(0, stream)
+    if args.no_persistent and xg.xgemm_set_persistent(h, 0) != xg.XGEMM_OK:
+        raise SystemExit("xgemm_set_persistent failed")
     code = xg.XGEMM_BF16 if w.dtype == "bf16" else xg.XGEMM_FP16
-    plan = xg.xgemm_select_band(w.M, w.N, w.K, code, torch.cuda.get_device_properties(dev).multi_processor_count)
+    plan = xg.xgemm_select_plan(w.M, w.N, w.K, code, torch.cuda.get_device_properties(dev).multi_processor_count,
+                                0 if args.no_persistent else 1)
     cfg = plan.body  # the whole call's configuration, or the body's when C is cut in two
     kernel_family = xg.xgemm_kernel_family(w.M, w.N, w.K, A.data_ptr(), w.K, B.data_ptr(), w.N, cfg)
 
@@ -542,29 +581,18 @@ def main():
     print("bench: settled (%d calls, %.2f s), warmup done" % (settled["calls"], settled["seconds"]),
           file=sys.stderr, flush=True)
 
-    # timed region: exactly K steps, bracketed by synchronisation; per-step
-    # HIP events on the launch stream give the kernel durations
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        starts[i].record(stream)
-        step()
-        ends[i].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    per = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)]) * 1e-3  # seconds
+    # timed region: exactly K steps, bracketed by synchronisation, with two
+    # HIP events on the launch stream around them (the kernels' average
+    # duration); then a per-call sample for the paper's protocol
+    wall, ev = timed_region(step, args.steps, stream)
     print("bench: timed %d steps in %.3f s" % (args.steps, wall), file=sys.stderr, flush=True)
+    per = per_call_times(step, max(args.steps, 100), stream)
 
     flops = float(w.flops)
     ms_per_step = wall / args.steps * 1e3
     value = flops * args.steps / wall / 1e12
-    avg_kernel = float(per.mean())
-    achieved = flops / avg_kernel / 1e12
-    srt = np.sort(per)
-    q = len(srt) // 4
-    iqr_mean = float(srt[q:len(srt) - q].mean()) if len(srt) >= 4 else float(srt.mean())
+    achieved = flops / (ev / args.steps) / 1e12
+    iqr = iqr_mean(per)
     peak = PEAK_TFLOPS[w.dtype]
 
     if args.copy_calibration:
@@ -619,7 +647,7 @@ def main():
                            "body_extent": plan.extent, "tile": plan.band.tile,
                            "split_k": plan.band.split_k}})),
         "pct_of_peak": round(100.0 * value / peak, 2),
-        "paper_protocol_iqr_mean_tflops": round(flops / iqr_mean / 1e12, 2),
+        "paper_protocol_iqr_mean_tflops": round(flops / iqr / 1e12, 2),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4),
                      "traffic": traffic},

@@ -110,6 +110,17 @@ int xgemm_destroy(xgemm_handle_t h);
 int xgemm_set_workspace_limit(xgemm_handle_t h, size_t bytes);
 
 /*
+ * enable = 0: the plans this handle selects (xgemm_run, xgemm_run_noalloc,
+ * xgemm_run_strided_batched) never use the persistent kernel, and take the
+ * plan they would take without it (banded or not); enable = 1 (the
+ * default): they use it where xgemm_select_band says.  For callers that
+ * budget workspace (the persistent kernel's shared tiles need 2 x 256 KiB of
+ * partial sums per CU) or compare plans.  xgemm_run_config is not affected.
+ * XGEMM_ERR_INVALID_ARG for a NULL handle or another value of enable.
+ */
+int xgemm_set_persistent(xgemm_handle_t h, int enable);
+
+/*
  * C = A * B, row-major, enqueued asynchronously on `stream` (a hipStream_t;
  * NULL means the default stream).  C is complete once the stream has been
  * synchronized.  Arguments:
@@ -131,12 +142,14 @@ int xgemm_set_workspace_limit(xgemm_handle_t h, size_t bytes);
  * to M, N, K < 2^31 with every matrix addressable in 64-bit element offsets.  A handle holds one workspace
  * (split-k partials and operand copies), grown on demand with hipMalloc
  * (XGEMM_ERR_ALLOC if that fails).  Calls that share a handle may be
- * enqueued on different streams: a call that uses the workspace first makes
- * its stream wait for the last such call on another stream (an event the
- * handle records), so calls sharing a handle never overlap on the
- * workspace, and a buffer being grown is freed only after its last user has
- * completed.  Calls on different streams run concurrently only with one
- * handle per stream.  A handle must not be used by two host threads at
+ * enqueued on different streams, and never overlap on the workspace: while
+ * all of a handle's workspace users come on one stream its order suffices;
+ * the first such call on another stream waits on the host for the device to
+ * finish its work (hipDeviceSynchronize, so not inside a graph capture);
+ * from then on each such call records an event on its stream and the next
+ * one on another stream makes its stream wait for it.  A buffer being grown
+ * is freed only after its last user has completed.  Calls on different
+ * streams run concurrently only with one handle per stream.  A handle must not be used by two host threads at
  * once.  The configuration comes from the problem shape and the
  * device's CU count (xgemm_select_band: one plan, or a body and a band of C
  * launched one after the other).
@@ -249,6 +262,14 @@ typedef struct xgemm_band {
  * negative sizes, an unknown dtype, cu_count < 1 or out == NULL.
  */
 int xgemm_select_band(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, xgemm_band *out);
+
+/*
+ * As xgemm_select_band, for a handle whose persistent kernel is switched on
+ * (persistent = 1: the same as xgemm_select_band) or off (0, see
+ * xgemm_set_persistent).  XGEMM_ERR_INVALID_ARG as xgemm_select_band, or for
+ * another value of persistent.
+ */
+int xgemm_select_plan(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, int persistent, xgemm_band *out);
 
 /*
  * Workgroup tile of a tile id: rows (bm), columns (bn), K step (bk) and

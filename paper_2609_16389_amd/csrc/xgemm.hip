@@ -40,15 +40,22 @@ struct xgemm_ctx {
     int cu_count;
     void *workspace;
     size_t ws_bytes;
-    // Every call that touches the workspace records ws_event on its stream
-    // after its last launch; a call on another stream first makes its stream
-    // wait for that event, so that calls sharing the workspace never overlap,
-    // whichever streams they are enqueued on.  The workspace is only freed
-    // (to grow it) once the event has completed.
+    // Calls that share the workspace never overlap, whichever streams they
+    // are enqueued on.  While a handle's calls all come on one stream, the
+    // stream's order is enough and nothing is recorded (an event record
+    // between two GEMMs leaves the GPU idle for about 10 us).  The first
+    // call on another stream waits for the device to drain (the previous
+    // stream may no longer exist), and from then on every call records
+    // ws_event on its stream after its last launch, and a call on another
+    // stream makes its stream wait for that event.  The workspace is only
+    // freed (to grow it) once its last user has completed.
     hipEvent_t ws_event;
-    hipStream_t ws_stream;  // stream of the last recorded ws_event
-    bool ws_recorded;
+    hipStream_t ws_stream;  // stream of the last call that used the workspace
+    bool ws_used;           // ws_stream is set
+    bool ws_recorded;       // ws_event follows the last use on ws_stream
+    bool ws_multi;          // calls have come on more than one stream
     size_t ws_limit;        // largest workspace the handle may allocate (0: no limit)
+    bool persistent;        // the selected plans may use the persistent kernel
     void *scratch;          // this device's `scratch` array (xgemm_run_noalloc)
     char last_error[256];
 };
@@ -677,19 +684,24 @@ int acquire_workspace(xgemm_ctx *h, size_t bytes, hipStream_t s)
                  bytes, h->ws_limit);
         return XGEMM_ERR_ALLOC;
     }
-    if (h->ws_recorded && h->ws_stream != s) {
-        e = hipStreamWaitEvent(s, h->ws_event, 0);
+    if (h->ws_used && h->ws_stream != s) {
+        // the last user is on another stream: wait for its event, or (the
+        // first switch of streams, nothing recorded) for the whole device
+        e = h->ws_recorded ? hipStreamWaitEvent(s, h->ws_event, 0) : hipDeviceSynchronize();
         if (e != hipSuccess) {
-            set_error(h, "hipStreamWaitEvent", e);
+            set_error(h, h->ws_recorded ? "hipStreamWaitEvent" : "hipDeviceSynchronize", e);
             return XGEMM_ERR_HIP;
         }
+        h->ws_multi = true;
     }
     if (bytes <= h->ws_bytes)
         return XGEMM_OK;
     if (h->workspace) {
-        e = h->ws_recorded ? hipEventSynchronize(h->ws_event) : hipSuccess;
+        // the last user completes before the buffer goes: its event, or this
+        // stream (the last user was on it, or the device has drained)
+        e = h->ws_recorded ? hipEventSynchronize(h->ws_event) : hipStreamSynchronize(s);
         if (e != hipSuccess) {
-            set_error(h, "hipEventSynchronize", e);
+            set_error(h, "workspace drain", e);
             return XGEMM_ERR_HIP;
         }
         (void)hipFree(h->workspace);
@@ -720,12 +732,16 @@ char *ws_data(void *ws) { return (char *)ws + kWsPrefix; }
 // Mark the end of the workspace users just enqueued on stream s.
 int release_workspace(xgemm_ctx *h, hipStream_t s)
 {
+    h->ws_stream = s;
+    h->ws_used = true;
+    h->ws_recorded = false;
+    if (!h->ws_multi)
+        return XGEMM_OK;
     const hipError_t e = hipEventRecord(h->ws_event, s);
     if (e != hipSuccess) {
         set_error(h, "hipEventRecord", e);
         return XGEMM_ERR_HIP;
     }
-    h->ws_stream = s;
     h->ws_recorded = true;
     return XGEMM_OK;
 }
@@ -853,7 +869,7 @@ int run(xgemm_ctx *h, int64_t M, int64_t N, int64_t K, const void *A, int64_t ld
     if (K == 0)
         return launch_zero(h, M, N, C, ldc, s);
     CallPlan cp;
-    rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, forced, &cp);
+    rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, forced, &cp, forced || h->persistent);
     if (rc != XGEMM_OK)
         return rc;
     if (cp.ws > 0 && (rc = acquire_workspace(h, cp.ws, s)) != XGEMM_OK)
@@ -1069,7 +1085,7 @@ int run_batched(xgemm_ctx *h, int64_t batch, int64_t M, int64_t N, int64_t K, co
     // the persistent kernel over the tiles of all problems, as xgemm_run
     // takes it for one problem with as many tiles
     const TileShape &t256 = kTiles[XGEMM_TILE_256x256];
-    if (!pk.a && !pk.b && g.dma && g.p.vec_c && use_persistent(M, N, K, h->cu_count, cfg, batch) &&
+    if (h->persistent && !pk.a && !pk.b && g.dma && g.p.vec_c && use_persistent(M, N, K, h->cu_count, cfg, batch) &&
         (int64_t)t256.bm * ldc * 4 < ((int64_t)1 << 32) &&
         sk_schedule(g, (M / t256.bm) * (N / t256.bn) * batch, K / t256.bk, h->cu_count)) {
         const size_t ws = sk_workspace(g);
@@ -1478,8 +1494,11 @@ int xgemm_create(xgemm_handle_t *out)
     h->workspace = nullptr;
     h->ws_bytes = 0;
     h->ws_stream = nullptr;
+    h->ws_used = false;
     h->ws_recorded = false;
+    h->ws_multi = false;
     h->ws_limit = 0;
+    h->persistent = true;
     h->last_error[0] = '\0';
     h->scratch = nullptr;
     if (dev >= 0 && dev < kMaxDevices) {
@@ -1538,6 +1557,14 @@ int xgemm_set_workspace_limit(xgemm_handle_t h, size_t bytes)
     return XGEMM_OK;
 }
 
+int xgemm_set_persistent(xgemm_handle_t h, int enable)
+{
+    if (!h || (enable != 0 && enable != 1))
+        return XGEMM_ERR_INVALID_ARG;
+    h->persistent = enable == 1;
+    return XGEMM_OK;
+}
+
 int xgemm_run(xgemm_handle_t h, int64_t M, int64_t N, int64_t K, const void *A, int64_t lda,
               const void *B, int64_t ldb, float *C, int64_t ldc, int dtype, void *stream)
 {
@@ -1561,7 +1588,7 @@ int xgemm_run_noalloc(xgemm_handle_t h, int64_t M, int64_t N, int64_t K, const v
     if (K == 0)
         return launch_zero(h, M, N, C, ldc, s);
     CallPlan cp;
-    rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, nullptr, &cp);
+    rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, nullptr, &cp, h->persistent);
     if (rc == XGEMM_OK && cp.ws + kWsPrefix > kScratchBytes)   // a persistent plan's partials may not fit
         rc = plan_call(h->cu_count, M, N, K, A, lda, B, ldb, C, ldc, nullptr, &cp, false);
     if (rc != XGEMM_OK)
@@ -1599,22 +1626,28 @@ int xgemm_select_config(int64_t M, int64_t N, int64_t K, int dtype, int cu_count
     return XGEMM_OK;
 }
 
-int xgemm_select_band(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, xgemm_band *out)
+int xgemm_select_plan(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, int persistent, xgemm_band *out)
 {
-    if (!out || M < 0 || N < 0 || K < 0 || cu_count < 1 || (dtype != XGEMM_BF16 && dtype != XGEMM_FP16))
+    if (!out || M < 0 || N < 0 || K < 0 || cu_count < 1 || (dtype != XGEMM_BF16 && dtype != XGEMM_FP16) ||
+        (persistent != 0 && persistent != 1))
         return XGEMM_ERR_INVALID_ARG;
     *out = xgemm_band{};
     if (M == 0 || N == 0 || K == 0 || M >= kMaxDim || N >= kMaxDim || K >= kMaxDim) {
         select_config(M, N, K, cu_count, &out->body);
         return XGEMM_OK;
     }
-    const BandPlan b = select_band(M, N, K, cu_count);
+    const BandPlan b = select_band(M, N, K, cu_count, persistent == 1);
     out->axis = b.axis;
     out->extent = b.extent;
     out->body = b.body;
     if (b.axis != XGEMM_BAND_NONE)
         out->band = b.band;
     return XGEMM_OK;
+}
+
+int xgemm_select_band(int64_t M, int64_t N, int64_t K, int dtype, int cu_count, xgemm_band *out)
+{
+    return xgemm_select_plan(M, N, K, dtype, cu_count, 1, out);
 }
 
 int xgemm_tile_info(int tile, int *bm, int *bn, int *bk, int *threads)

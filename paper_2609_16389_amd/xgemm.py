@@ -122,6 +122,8 @@ lib.xgemm_destroy.argtypes = [_handle_t]
 lib.xgemm_destroy.restype = _i32
 lib.xgemm_set_workspace_limit.argtypes = [_handle_t, ctypes.c_size_t]
 lib.xgemm_set_workspace_limit.restype = _i32
+lib.xgemm_set_persistent.argtypes = [_handle_t, _i32]
+lib.xgemm_set_persistent.restype = _i32
 lib.xgemm_run.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p]
 lib.xgemm_run.restype = _i32
 lib.xgemm_run_noalloc.argtypes = [_handle_t, _i64, _i64, _i64, _p, _i64, _p, _i64, _p, _i64, _i32, _p]
@@ -135,6 +137,8 @@ lib.xgemm_run_strided_batched.restype = _i32
 lib.xgemm_select_config.argtypes = [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(xgemm_config)]
 lib.xgemm_select_config.restype = _i32
 lib.xgemm_select_band.argtypes = [_i64, _i64, _i64, _i32, _i32, ctypes.POINTER(xgemm_band)]
+lib.xgemm_select_plan.argtypes = [_i64, _i64, _i64, _i32, _i32, _i32, ctypes.POINTER(xgemm_band)]
+lib.xgemm_select_plan.restype = _i32
 lib.xgemm_select_band.restype = _i32
 lib.xgemm_tile_info.argtypes = [_i32] + [ctypes.POINTER(ctypes.c_int)] * 4
 lib.xgemm_tile_info.restype = _i32
@@ -191,6 +195,10 @@ def xgemm_set_workspace_limit(h, nbytes) -> int:
     return lib.xgemm_set_workspace_limit(h, nbytes)
 
 
+def xgemm_set_persistent(h, enable) -> int:
+    return lib.xgemm_set_persistent(h, enable)
+
+
 def xgemm_run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream) -> int:
     return lib.xgemm_run(h, M, N, K, A, lda, B, ldb, C, ldc, dtype, stream)
 
@@ -224,6 +232,14 @@ def xgemm_select_config(M, N, K, dtype, cu_count) -> xgemm_config:
 def xgemm_select_band(M, N, K, dtype, cu_count) -> xgemm_band:
     out = xgemm_band()
     rc = lib.xgemm_select_band(M, N, K, dtype, cu_count, ctypes.byref(out))
+    if rc != XGEMM_OK:
+        raise XgemmError(rc)
+    return out
+
+
+def xgemm_select_plan(M, N, K, dtype, cu_count, persistent) -> xgemm_band:
+    out = xgemm_band()
+    rc = lib.xgemm_select_plan(M, N, K, dtype, cu_count, persistent, ctypes.byref(out))
     if rc != XGEMM_OK:
         raise XgemmError(rc)
     return out

@@ -28,6 +28,7 @@ def test_null_handle_is_invalid_argument():
     assert xg.xgemm_destroy(None) == xg.XGEMM_OK
     assert xg.xgemm_last_error(None) == "no handle"
     assert xg.lib.xgemm_create(None) == xg.XGEMM_ERR_INVALID_ARG
+    assert xg.xgemm_set_persistent(None, 0) == xg.XGEMM_ERR_INVALID_ARG
 
 
 def test_tile_info():
@@ -314,6 +315,18 @@ def test_band_selection_on_workloads():
     # the rule is in whole rounds of the device's CUs: 8192^3 on 304 CUs is
     # 3.37 rounds
     assert _band(8192, 8192, 8192, xg.XGEMM_BF16, 304).body.stream_k == 0
+    # without the persistent kernel: the one-launch plan, or the band plan
+    b = xg.xgemm_select_plan(8192, 8192, 8192, xg.XGEMM_BF16, 256, 0)
+    assert (b.axis, b.body.tile, b.body.split_k, b.body.stream_k) == (xg.XGEMM_BAND_NONE, 0, 1, 0)
+    b = xg.xgemm_select_plan(4096, 14336, 4096, xg.XGEMM_FP16, 256, 0)
+    assert (b.axis, b.extent, b.body.tile, b.body.stream_k) == (xg.XGEMM_BAND_COLUMNS, 12288, 0, 0)
+    assert (b.band.tile, b.band.split_k) == (1, 1)
+    for shape in [(4096, 14336, 4096), (6144, 6144, 6144), (1024, 1024, 65536)]:
+        a, b = _band(*shape), xg.xgemm_select_plan(*shape, xg.XGEMM_BF16, 256, 1)
+        assert (a.axis, a.extent, a.body.tile, a.body.split_k, a.body.stream_k) == \
+               (b.axis, b.extent, b.body.tile, b.body.split_k, b.body.stream_k)
+    with pytest.raises(xg.XgemmError):
+        xg.xgemm_select_plan(64, 64, 64, xg.XGEMM_BF16, 256, 2)
     # a band of rows
     b = _band(9472, 2048, 1000)
     assert (b.axis, b.extent) == (xg.XGEMM_BAND_ROWS, 8192)

@@ -923,6 +923,48 @@ def test_strided_batched_persistent(L):
     assert np.array_equal(Cbuf2.cpu().numpy(), Ch)
 
 
+def test_persistent_switch():
+    """xgemm_set_persistent(h, 0): the handle's selected plans leave out the
+    persistent kernel (8192 x 8192 x 2048 bf16 is four whole rounds of 256 x
+    256 tiles; with the switch off it runs one workgroup per tile, the same
+    sums in the same order for whole tiles, so the same bits); other values
+    are rejected; forced configurations are unaffected."""
+    M, N, K = 8192, 8192, 2048
+    cu = torch.cuda.get_device_properties(0).multi_processor_count
+    if cu != 256:
+        pytest.skip("the case is sized for 256 CUs")
+    assert xg.xgemm_select_band(M, N, K, xg.XGEMM_BF16, cu).body.stream_k == 1
+    A, B = wl.make_inputs(M, N, K, "bf16", "uniform", seed=91)
+    dA, dB = to_device(A, "bf16"), to_device(B, "bf16")
+    s = torch.cuda.current_stream().cuda_stream
+    h = xg.xgemm_create()
+    try:
+        outs = []
+        for enable in (1, 0):
+            assert xg.xgemm_set_persistent(h, enable) == xg.XGEMM_OK
+            C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+            assert xg.xgemm_run(h, M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, C.data_ptr(), N,
+                                xg.XGEMM_BF16, s) == xg.XGEMM_OK, xg.xgemm_last_error(h)
+            torch.cuda.synchronize()
+            outs.append(C.cpu().numpy())
+        assert np.array_equal(outs[0], outs[1])
+        rows = np.array([0, 1, 255, 256, 4097, 8191])
+        C_ref, S = oracle.gemm_rows(A, B, "bf16", rows)
+        check_close(outs[1][rows], C_ref, S, "persistent switch off")
+        assert xg.xgemm_set_persistent(h, 2) == xg.XGEMM_ERR_INVALID_ARG
+        # a forced persistent configuration still runs it
+        assert xg.xgemm_set_persistent(h, 0) == xg.XGEMM_OK
+        C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        cfg = xg.xgemm_config(tile=0, split_k=1, group_m=4, stream_k=1)
+        assert xg.xgemm_run_config(h, M, N, K, dA.data_ptr(), K, dB.data_ptr(), N, C.data_ptr(), N,
+                                   xg.XGEMM_BF16, s, cfg) == xg.XGEMM_OK
+        torch.cuda.synchronize()
+        assert np.array_equal(C.cpu().numpy(), outs[0])
+    finally:
+        torch.cuda.synchronize()
+        xg.xgemm_destroy(h)
+
+
 def test_strided_batched_integer_exact_and_single():
     L, M, N, K = 2, 256, 256, 512
     As, Bs = [], []
