@@ -329,17 +329,21 @@ def test_persistent_kernel_falls_back(shape):
     check_close(run_gpu(A, B, "bf16", config=cfg), C_ref, S, "fallback %s" % (shape,))
 
 
-SK_BIG = ["gemm4096_bf16", "gemm8192_bf16", "proj16384x5120x4096_fp16", "proj4096x14336x4096_fp16"]
+SK_BIG = [("gemm4096_bf16", 1), ("gemm8192_bf16", 1), ("proj16384x5120x4096_fp16", 1),
+          ("proj4096x14336x4096_fp16", 1),
+          # 16 tiles of K = 65536 on 12 workgroups: ranges of 1.33 tiles (1365 K steps)
+          ("skinny1024x1024x65536_bf16", 12)]
 
 
-@pytest.mark.parametrize("name", SK_BIG)
-def test_persistent_kernel_full_size_sampled(name):
-    """The full-size workloads through the persistent kernel on every CU:
-    sampled rows, columns and entries, plus every element of up to three
-    split tiles (their two pieces meet in the hand-over) and of the first
-    and last tile."""
+@pytest.mark.parametrize("name,grid", SK_BIG, ids=lambda v: str(v))
+def test_persistent_kernel_full_size_sampled(name, grid):
+    """The full-size workloads through the persistent kernel on every CU (the
+    skinny one, with fewer tiles than CUs, on 12 workgroups): sampled rows,
+    columns and entries, plus every element of up to three split tiles
+    (their two pieces meet in the hand-over) and of the first and last
+    tile."""
     w = wl.WORKLOADS[name]
-    cfg = _sk_cfg(1)
+    cfg = _sk_cfg(grid)
     info = _sk_info(w.M, w.N, w.K, cfg)
     assert info.family == xg.XGEMM_KERNEL_PERSISTENT
     A, B = wl.workload_inputs(w)
