@@ -14,11 +14,15 @@
 //     of steps, so a tile is split between at most two neighbouring ranges:
 //     the first steps (from k = 0) at the end of range lw, the rest at the
 //     start of range lw + 1.
+// The tiles may belong to the problems of a strided batch (tile t is tile
+// t % tiles_per of problem t / tiles_per).
 // The LDS pipeline runs across tile boundaries: during a tile's last K
 // steps the loads of the next tile's first steps are already in flight, and
 // a finished tile's C stores (streaming stores) are issued at the start of
-// the next tile's first step, whose MFMAs start from zero, so the stores
-// drain under the next tile's work.
+// the next tile's first step, whose MFMAs start from zero, so no second set
+// of accumulators is needed.  That step waits while the memory side takes
+// the stores (all workgroups of a round store at once); the other steps of
+// the next tile, and the prologue of none, follow without a gap.
 //
 // A tile split between ranges lw and lw + 1 (its slot is lw + 1) is
 // finished by whichever of its two pieces completes second, without any
