@@ -21,8 +21,8 @@
 // a finished tile's C stores (streaming stores) are issued at the start of
 // the next tile's first step, whose MFMAs start from zero, so no second set
 // of accumulators is needed.  That step waits while the memory side takes
-// the stores (all workgroups of a round store at once); the other steps of
-// the next tile, and the prologue of none, follow without a gap.
+// the stores (all workgroups of a round store at once); no tile after a
+// workgroup's first has a prologue of its own.
 //
 // A tile split between ranges lw and lw + 1 (its slot is lw + 1) is
 // finished by whichever of its two pieces completes second, without any
