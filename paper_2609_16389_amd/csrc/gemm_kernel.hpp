@@ -584,6 +584,31 @@ struct DeviceOps {
     {
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, voff, soff, 0);
     }
+    // Two 16 x 16 accumulator blocks of one block row (block columns 2p and
+    // 2p + 1; lane l holds row l % 16, columns 4 (l / 16) .. +3 of each),
+    // rearranged so that each holds 8 whole rows of their 32 columns: b0
+    // rows 0-7, b1 rows 8-15, lane l holding row l % 8 (+ 8 in b1), columns
+    // 16 ((l % 16) / 8) + 4 (l / 16) .. +3.  One 16-byte store per lane then
+    // writes 8 rows of 128 bytes, whole lines, where the plain layout writes
+    // 16 half lines (the memory side counted 1.2-1.37x the bytes of C for
+    // half-line streaming stores).  Lanes 8-15 of each row of 16 trade with
+    // lanes 0-7 (DPP row rotation by 8, bank masks select the halves).  The
+    // elements are copied out before the bit casts (a bit cast of a vector
+    // element in place read element 0 for every element).
+    __device__ __forceinline__ void line_pair(f32x4 &b0, f32x4 &b1) const
+    {
+        f32x4 r0, r1;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float a = b0[e], b = b1[e];
+            const int ia = __builtin_bit_cast(int, a), ib = __builtin_bit_cast(int, b);
+            const int t = __builtin_amdgcn_mov_dpp(ia, 0x128, 0xF, 0xF, false);   // row_ror:8
+            r0[e] = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(ia, ib, 0x128, 0xF, 0xC, false));
+            r1[e] = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(ib, t, 0xE4, 0xF, 0x3, false));
+        }
+        b0 = r0;
+        b1 = r1;
+    }
     // streaming store (nt): the XCD's L2 does not keep the line for reuse
     __device__ __forceinline__ void buf_store4_nt(Rsrc r, uint32_t voff, uint32_t soff, f32x4 v) const
     {

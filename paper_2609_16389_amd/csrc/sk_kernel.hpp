@@ -241,22 +241,32 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
     // --- stores ---
     // Buffer accesses: a descriptor of a uniform base, a 32-bit per-lane
     // byte offset and a uniform byte offset (the host keeps 256 rows of C
-    // within 4 GiB and C 16-byte aligned).  Lane l owns row lr, columns
-    // 4 kg .. 4 kg + 3 of each 16 x 16 block.
-    const uint32_t c_lane = (uint32_t)((lr * p.ldc + kg * 4) * 4);
+    // within 4 GiB and C 16-byte aligned).  Lane l's accumulators hold row
+    // lr, columns 4 kg .. 4 kg + 3 of each 16 x 16 block.
     // this wave's block of C in tile u
     auto c_base = [&](const SkTile &u) {
         return p.C + u.b * p.stride_c + (int64_t)(u.m * BM + wm * TM) * p.ldc + u.n * BN + wn * TN;
     };
     // C of tile u, block row i (FN 16-byte stores per lane): streaming
     // stores, whose lines an XCD's L2 does not keep, so that they take no L2
-    // space from the operands of the tiles that follow
+    // space from the operands of the tiles that follow.  Pairs of blocks are
+    // first rearranged into whole 128-byte rows (line_pair: lane l then
+    // writes row l % 8, or 8 + l % 8, at column 16 ((l % 16) / 8) + 4 (l / 16)
+    // of the pair).  Measured 712 against 748 us at 8192^3 (3-9% on the
+    // persistent kernel's shapes) over storing the blocks as they are.
+    const uint32_t c_line = (uint32_t)(((lr & 7) * p.ldc + (lr >> 3) * 16 + kg * 4) * 4);
+    static_assert(FN % 2 == 0, "pairs of block columns");
+    auto store_pair = [&](typename Ops::Rsrc r, uint32_t soff, int j, accT &b0, accT &b1) {
+        ops.line_pair(b0, b1);
+        ops.buf_store4_nt(r, c_line + j * MI * 4, soff, b0);
+        ops.buf_store4_nt(r, c_line + j * MI * 4, soff + (uint32_t)(8 * p.ldc * 4), b1);
+    };
     auto store_c_row = [&](const SkTile &u, int i) {
         const auto r = ops.rsrc(c_base(u));
         const uint32_t soff = (uint32_t)(i * MI * p.ldc * 4);
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-            ops.buf_store4_nt(r, c_lane + j * MI * 4, soff, acc[i][j]);
+        for (int j = 0; j < FN; j += 2)
+            store_pair(r, soff, j, acc[i][j], acc[i][j + 1]);
     };
     // partial sums of slot s, piece 0 (first steps) or 1 (last steps): block
     // (i, j) of wave w is 64 lanes x 16 bytes, contiguous, in the
@@ -423,10 +433,12 @@ __host__ __device__ __forceinline__ void sk_tile(const Ops &ops, const SkParams 
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
 #pragma unroll
-            for (int j = 0; j < FN; ++j) {
-                const accT x = ops.buf_load4_dev(r0, p_lane + j * 1024, i * FN * 1024) +
-                               ops.buf_load4_dev(r1, p_lane + j * 1024, i * FN * 1024);
-                ops.buf_store4_nt(rc, c_lane + j * MI * 4, (uint32_t)(i * MI * p.ldc * 4), x);
+            for (int j = 0; j < FN; j += 2) {
+                accT x0 = ops.buf_load4_dev(r0, p_lane + j * 1024, i * FN * 1024) +
+                          ops.buf_load4_dev(r1, p_lane + j * 1024, i * FN * 1024);
+                accT x1 = ops.buf_load4_dev(r0, p_lane + (j + 1) * 1024, i * FN * 1024) +
+                          ops.buf_load4_dev(r1, p_lane + (j + 1) * 1024, i * FN * 1024);
+                store_pair(rc, (uint32_t)(i * MI * p.ldc * 4), j, x0, x1);
             }
             ops.fence();
         }

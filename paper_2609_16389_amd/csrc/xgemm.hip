@@ -1373,6 +1373,8 @@ struct TraceOps {
         push(XGEMM_TRACE_STORE, 16, 0, (int64_t)(uintptr_t)(r + voff + soff));
     }
     void buf_store4_nt(Rsrc r, uint32_t voff, uint32_t soff, xgemm_dev::f32x4 v) const { buf_store4(r, voff, soff, v); }
+    // a register exchange between lanes: no memory access, nothing to record
+    void line_pair(xgemm_dev::f32x4 &, xgemm_dev::f32x4 &) const {}
     void buf_store4_dev(Rsrc r, uint32_t voff, uint32_t soff, xgemm_dev::f32x4 v) const { buf_store4(r, voff, soff, v); }
     xgemm_dev::f32x4 buf_load4_dev(Rsrc r, uint32_t voff, uint32_t soff) const
     {
