@@ -682,19 +682,25 @@ constexpr int dma_lds_bytes()
 // K step from the same LDS bytes.  On random data the GPU is power-capped;
 // there the 16 x 16 shape sustains more flops (MFMA-only, about 2100
 // against 1840 TFLOP/s, with the accumulators in VGPRs or AGPRs alike).
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, int MI, class Ops>
+//
+// KW is the number of waves along K: with 2, two waves own each (BM/WGM) x
+// (BN/WGN) block of C, each multiplying one of the two MFMA sub-steps of
+// every K step, and their sums are added at the end.
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, int MI, int KW, class Ops>
 __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmParams &p_in, int block, int nblocks,
                                                   int tid)
 {
     static_assert(MI == 16 || MI == 32, "MFMA block");
-    constexpr int NW = WGM * WGN;
+    static_assert(KW == 1 || KW == 2, "waves along K");
+    constexpr int NMN = WGM * WGN;               // waves along M and N
+    constexpr int NW = NMN * KW;
     constexpr int TM = BM / WGM, TN = BN / WGN;
     constexpr int FM = TM / MI, FN = TN / MI;   // MFMA blocks per wave
     constexpr int KI = 512 / MI;                 // k per MFMA
     constexpr int KS = BK / KI;                  // MFMA k sub-steps per K step
     constexpr int NG = 64 / MI;                  // lane groups along k, 8 values each
     constexpr int AE = MI * MI / 64;             // accumulators per lane and block
-    constexpr bool TWO_PER_SIMD = NW == 8;       // the two-waves-per-SIMD schedule below
+    constexpr bool TWO_PER_SIMD = NW == 8 && KW == 1;   // the two-waves-per-SIMD schedule below
     typedef float accT __attribute__((ext_vector_type(AE)));
     constexpr int A_ROWB = BK * 2;
     constexpr int B_ROWB = BN * 2;
@@ -729,7 +735,8 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
 
     const int lane = tid & 63;
     const int wave = ops.uniform(tid >> 6);
-    const int wm = wave % WGM, wn = wave / WGM;
+    const int wmn = wave % NMN, wk = wave / NMN;
+    const int wm = wmn % WGM, wn = wmn / WGM;
     const int64_t lda = p.lda, ldb = p.ldb;
     char *const smem = ops.lds();
 
@@ -1061,6 +1068,145 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
             kstep_pair.template operator()<false, 0>(nk - 2);
             kstep_pair.template operator()<false, -1>(nk - 1);
         }
+    } else if constexpr (KW == 2) {
+        // Two waves per SIMD on a tile too narrow for two 128 x 64 blocks
+        // per SIMD: the waves of a pair own the same 128 x 64 block and
+        // split every K step, wave wk multiplying sub-step wk (32 of the 64
+        // k).  Each wave thus reads the LDS bytes per flop of a 128 x 64
+        // block, and the other wave of its SIMD covers its barrier and load
+        // waits.  Three stages: the loads of step t+3 go into the stage that
+        // step t's barrier frees (its fragments were read during step t-1)
+        // and have two steps to land.  A wave's fragments of step t+1 are
+        // read during step t into the other register buffer, so the buffer
+        // alternates with the step's parity (a template argument: register
+        // arrays are not indexed at run time).
+        constexpr int R = 1;                      // rows of a step issued before its barrier
+        static_assert(MI == 16 && STAGES == 3 && KS == 2 && FN <= FM - R && FM % 2 == 0, "K-pair schedule shape");
+        constexpr int LSTEP = ((FM - R) * FN) / LD > 0 ? ((FM - R) * FN) / LD : 1;
+        static_assert(LSTEP * (LD - 1) < (FM - R) * FN, "load spacing");
+        u32x4 ga[2][FM], gb[2][FN];
+        // One K step t in buffer BUF (t's parity).  LOAD: issue the loads of
+        // step t+3 into stage t % 3.  WAIT: this wave's load groups allowed
+        // in flight once step t+1 has landed (-1: t is the last step).
+        auto kstep_k = [&]<int BUF, bool LOAD, int WAIT>(int t) {
+            const int stage = t % 3;
+            const int next = stage == 2 ? 0 : stage + 1;
+#pragma unroll
+            for (int i = 0; i < R; ++i) {
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    acc[i][j] = ops.template mfma<DT>(gb[BUF][j], ga[BUF][i], acc[i][j]);
+                ops.fence();
+            }
+            // stage t fully read by every wave; step t+1 landed for this wave
+            ops.wait_lgkm0();
+            if constexpr (WAIT >= 0)
+                ops.template wait_vm<WAIT * LD>();
+            ops.barrier();
+            ops.fence();
+            ops.template priority<1>();
+            if constexpr (WAIT >= 0) {
+#pragma unroll
+                for (int i = 0; i < R; ++i)
+                    ga[BUF ^ 1][i] = frag_A(next, wk, i);
+            }
+#pragma unroll
+            for (int i = R; i < FM; ++i) {
+#pragma unroll
+                for (int j = 0; j < FN; ++j) {
+                    acc[i][j] = ops.template mfma<DT>(gb[BUF][j], ga[BUF][i], acc[i][j]);
+                    const int g = (i - R) * FN + j;
+                    if constexpr (LOAD) {
+                        if (g % LSTEP == 0 && g / LSTEP < LD)
+                            load_j(t + 3, stage, g / LSTEP);
+                    }
+                }
+                if constexpr (WAIT >= 0) {
+                    ga[BUF ^ 1][i] = frag_A(next, wk, i);
+                    if (i - R < FN)
+                        gb[BUF ^ 1][i - R] = frag_B(next, wk, i - R);
+                }
+                ops.fence();
+            }
+            ops.template priority<0>();
+        };
+        // the last three steps: no more loads, then exact waits
+        auto last3 = [&]<int BUF>(int t) {
+            kstep_k.template operator()<BUF, false, 1>(t);
+            kstep_k.template operator()<BUF ^ 1, false, 0>(t + 1);
+            kstep_k.template operator()<BUF, false, -1>(t + 2);
+        };
+        // Add the pair's sums through LDS (every stage is free once every
+        // wave is past the last step's barrier, which follows its last
+        // fragment reads): wave WK keeps block rows
+        // [WK FM/2, WK FM/2 + FM/2), hands the other half to its partner and
+        // moves the kept rows to acc[0 .. FM/2).  Sub-step 0's sum is the
+        // first operand of every addition.  WK is the wave's wk as a template
+        // argument, so that the halves are chosen at compile time (a run-time
+        // choice keeps both live).
+        constexpr int FH = FM / 2;
+        static_assert(NW * FH * FN * 1024 <= STAGES * STAGE, "exchange fits the stages");
+        char *const give = smem + (wmn * KW + wk) * FH * FN * 1024 + lane * 16;
+        const char *const take = smem + (wmn * KW + (wk ^ 1)) * FH * FN * 1024 + lane * 16;
+        auto exchange = [&]<int WK>() {
+            constexpr int GIVE = WK ? 0 : FH, KEEP = WK ? FH : 0;
+#pragma unroll
+            for (int h = 0; h < FH; ++h)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    ops.lds_write16(give + (h * FN + j) * 1024, __builtin_bit_cast(u32x4, acc[GIVE + h][j]));
+            ops.wait_lgkm0();
+            ops.barrier();
+#pragma unroll
+            for (int h = 0; h < FH; ++h)
+#pragma unroll
+                for (int j = 0; j < FN; ++j) {
+                    const accT other = __builtin_bit_cast(accT, ops.read16(take + (h * FN + j) * 1024));
+                    acc[h][j] = WK ? other + acc[KEEP + h][j] : acc[KEEP + h][j] + other;
+                }
+        };
+        // Steps 0 .. nk-4 issue loads.  The whole K loop and the exchange
+        // are instantiated per parity P of their number, and per wk: the
+        // fragment buffers alternate with the step, and paths that joined
+        // before the last step would keep both buffers live.  With P = 1
+        // step 0 runs from buffer 1, so the loop always starts from buffer 0.
+        auto k_loop = [&]<int P, int WK>() {
+            const int nl = nk - 3;
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                ga[P][i] = frag_A(0, wk, i);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                gb[P][j] = frag_B(0, wk, j);
+            int t = 0;
+            if constexpr (P == 1) {
+                kstep_k.template operator()<1, true, 1>(0);
+                t = 1;
+            }
+            for (; t + 2 <= nl; t += 2) {
+                kstep_k.template operator()<0, true, 1>(t);
+                kstep_k.template operator()<1, true, 1>(t + 1);
+            }
+            last3.template operator()<0>(t);
+            exchange.template operator()<WK>();
+        };
+        if (nk >= 3) {
+            issue_loads(0, 0);
+            issue_loads(1, 1);
+            issue_loads(2, 2);
+            ops.template wait_vm<2 * LD>();
+            ops.barrier();
+            zero_partial();
+            const int sel = ((nk - 3) & 1) * 2 + (wk & 1);
+            if (sel == 0)
+                k_loop.template operator()<0, 0>();
+            else if (sel == 1)
+                k_loop.template operator()<0, 1>();
+            else if (sel == 2)
+                k_loop.template operator()<1, 0>();
+            else
+                k_loop.template operator()<1, 1>();
+        }
     } else if (nk >= STAGES) {
         // prologue: fill every stage, wait for stage 0
 #pragma unroll
@@ -1095,9 +1241,11 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     float *Cb = ov.base;
     const int64_t ldc = ov.ld;
     const bool vec_store = p.vec_c && (m0 + BM <= p.M) && (n0 + BN <= p.N);
+    // with two waves along K, each stores its FM / 2 kept block rows
+    constexpr int FO = FM / KW;
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int row = m0 + wm * TM + i * MI + lr;
+    for (int i = 0; i < FO; ++i) {
+        const int row = m0 + wm * TM + (wk * FO + i) * MI + lr;
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
 #pragma unroll
@@ -1121,8 +1269,8 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
     }
 }
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, int MI>
-__global__ void __launch_bounds__(WGM * WGN * 64, 1)
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int DT, int MI, int KW>
+__global__ void __launch_bounds__(WGM * WGN * KW * 64, 1)
 gemm_kernel_dma(GemmParams p_in)
 {
     __shared__ __attribute__((aligned(1024))) char smem[dma_lds_bytes<BM, BN, BK, STAGES>()];
@@ -1130,7 +1278,7 @@ gemm_kernel_dma(GemmParams p_in)
     if (w >= p_in.grid)
         return;
     const DeviceOps ops{smem};
-    dma_tile<BM, BN, BK, STAGES, WGM, WGN, DT, MI>(ops, p_in, w, p_in.grid, threadIdx.x);
+    dma_tile<BM, BN, BK, STAGES, WGM, WGN, DT, MI, KW>(ops, p_in, w, p_in.grid, threadIdx.x);
 }
 
 // C[i][j] = sum over p of W[p][i][j], p ascending (a fixed order, so the

@@ -124,7 +124,7 @@ struct TileCost {
 };
 constexpr TileCost kTileCost[XGEMM_TILE_COUNT] = {
     {9.78, 1.487, 1.487},  // 256 x 256: 8 waves, one workgroup per CU
-    {6.29, 0.852, 0.852},  // 256 x 128: 4 waves, one workgroup per CU
+    {6.29, 0.852, 0.852},  // 256 x 128: 8 waves (pairs split K), one workgroup per CU
     {3.22, 0.585, 1.050},  // 128 x 128: 4 waves, one or two workgroups per CU
 };
 
@@ -337,16 +337,16 @@ hipError_t launch_gemm(int dtype, GemmParams p, int grid, hipStream_t s)
     return hipGetLastError();
 }
 
-template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int MI>
+template <int BM, int BN, int BK, int STAGES, int WGM, int WGN, int MI, int KW>
 hipError_t launch_dma(int dtype, GemmParams p, int grid, hipStream_t s)
 {
     p.grid = grid;
     if (dtype == XGEMM_BF16)
-        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 0, MI>), grid_of(grid),
-                           dim3(WGM * WGN * 64), 0, s, p);
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 0, MI, KW>), grid_of(grid),
+                           dim3(WGM * WGN * KW * 64), 0, s, p);
     else
-        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 1, MI>), grid_of(grid),
-                           dim3(WGM * WGN * 64), 0, s, p);
+        hipLaunchKernelGGL((xgemm_dev::gemm_kernel_dma<BM, BN, BK, STAGES, WGM, WGN, 1, MI, KW>), grid_of(grid),
+                           dim3(WGM * WGN * KW * 64), 0, s, p);
     return hipGetLastError();
 }
 
@@ -373,6 +373,12 @@ constexpr int kDmaMinStages = 3;
 #define XGEMM_WGM_256x256 2
 #define XGEMM_WGN_256x256 4
 #endif
+// Waves along K of the 256 x 128 pipelined tile: 2 (eight waves, two per
+// SIMD, each pair splitting the K steps of one 128 x 64 block) or 1 (four
+// waves, one per SIMD).
+#ifndef XGEMM_KW_256x128
+#define XGEMM_KW_256x128 2
+#endif
 
 // The pipelined kernels need 16-byte aligned A and B with lda, ldb multiples
 // of 8, N and K multiples of 8 (whole 16-byte chunks of B rows and of A rows
@@ -392,9 +398,10 @@ bool dma_eligible(const GemmParams &p, int bm, bool b_padded = false)
 // columns, K step, LDS stages, waves along M and N, MFMA block).  Launches
 // and host traces both take them from here, so a trace follows the kernel
 // that runs.
-template <int BM_, int BN_, int STAGES_, int MI_, int WGM_ = 2, int WGN_ = 2>
+template <int BM_, int BN_, int STAGES_, int MI_, int WGM_ = 2, int WGN_ = 2, int KW_ = 1>
 struct DmaTile {
-    static constexpr int BM = BM_, BN = BN_, BK = kDmaBK, STAGES = STAGES_, WGM = WGM_, WGN = WGN_, MI = MI_;
+    static constexpr int BM = BM_, BN = BN_, BK = kDmaBK, STAGES = STAGES_, WGM = WGM_, WGN = WGN_, MI = MI_,
+                         KW = KW_;
 };
 
 template <class F>
@@ -402,7 +409,7 @@ auto with_dma_tile(int tile, F &&f)
 {
     switch (tile) {
     case XGEMM_TILE_256x256: return f(DmaTile<256, 256, kDmaStages256x256, XGEMM_MI_256x256, XGEMM_WGM_256x256, XGEMM_WGN_256x256>{});
-    case XGEMM_TILE_256x128: return f(DmaTile<256, 128, kDmaStages256x128, XGEMM_MI_256x128>{});
+    case XGEMM_TILE_256x128: return f(DmaTile<256, 128, kDmaStages256x128, XGEMM_MI_256x128, 2, 2, XGEMM_KW_256x128>{});
     default: return f(DmaTile<128, 128, kDmaStages128x128, XGEMM_MI_128x128>{});
     }
 }
@@ -428,7 +435,7 @@ auto with_general_tile(int tile, F &&f)
 int tile_threads(int tile, bool dma)
 {
     if (dma)
-        return with_dma_tile(tile, [](auto t) { return decltype(t)::WGM * decltype(t)::WGN * 64; });
+        return with_dma_tile(tile, [](auto t) { return decltype(t)::WGM * decltype(t)::WGN * decltype(t)::KW * 64; });
     return with_general_tile(tile, [](auto t) { return decltype(t)::WGM * decltype(t)::WGN * 64; });
 }
 
@@ -439,7 +446,7 @@ hipError_t launch_tile(int tile, bool dma, int dtype, const GemmParams &p, int g
     if (dma)
         return with_dma_tile(tile, [&](auto t) {
             using T = decltype(t);
-            return launch_dma<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, T::MI>(dtype, p, grid, s);
+            return launch_dma<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, T::MI, T::KW>(dtype, p, grid, s);
         });
     return with_general_tile(tile, [&](auto t) {
         using T = decltype(t);
@@ -1790,7 +1797,7 @@ int xgemm_trace_workgroup(int64_t M, int64_t N, int64_t K, const void *A, int64_
             return trace_threads(xgemm_dev::dma_lds_bytes<T::BM, T::BN, T::BK, T::STAGES>(),
                                  [&](const TraceOps &ops, int tid) {
                                      xgemm_dev::dma_tile<T::BM, T::BN, T::BK, T::STAGES, T::WGM, T::WGN, 0,
-                                                         T::MI>(ops, g.p, (int)block, (int)g.grid, tid);
+                                                         T::MI, T::KW>(ops, g.p, (int)block, (int)g.grid, tid);
                                  });
         });
     return with_general_tile(plan.tile, [&](auto t) {

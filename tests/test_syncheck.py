@@ -189,16 +189,19 @@ def stages(tile):
 
 @pytest.mark.parametrize("tile", [0, 1, 2])
 def test_kernel_trace_structure(tile):
-    """Per wave: one barrier after the prologue and one per K step, and the
-    direct loads of every K step exactly once."""
+    """Per wave: one barrier after the prologue and one per K step (one more
+    where two waves along K add their sums through LDS), and the direct
+    loads of every K step exactly once."""
     bm, bn, bk, threads = xg.xgemm_tile_info(tile)
     nk = stages(tile) + 3
     K = nk * bk
     ev, counts = sc.trace_workgroup(bm, bn, K, K, bn, bn, cfg(tile), 256, 0, 0, threads)
     waves = sc.wave_streams(ev, counts)
     loads_per_step = (bm + bn) * bk * 2 // 1024 // len(waves)
+    # the 256 x 128 tile: eight waves, two on each 128 x 64 block of C
+    exchange = 1 if tile == 1 and threads == 512 else 0
     for ws in waves:
-        assert (ws.op == sc.BARRIER).sum() == nk + 1
+        assert (ws.op == sc.BARRIER).sum() == nk + 1 + exchange
         assert (ws.op == sc.LDS_LOAD).sum() == nk * loads_per_step
     # every byte of every stage is loaded once per step that uses it
     base = np.concatenate([ws.lds[ws.op == sc.LDS_LOAD, 0] for ws in waves])
@@ -462,11 +465,17 @@ def partial_waves(tile):
 def test_partial_k_step_zero_fill_is_traced(tile):
     waves, lds = partial_waves(tile)
     assert sc.check_workgroup_lds(waves, lds) == []
+    # the 256 x 128 tile's wave pairs write half their sums to LDS after the
+    # second-to-last barrier (16 blocks of 16 x 16 each)
+    pair = tile == 1 and len(waves) == 8
     for ws in waves:
         # the zero fill: LDS writes between the first barrier and the second
         b0, b1 = nth(ws.op, sc.BARRIER, 0), nth(ws.op, sc.BARRIER, 1)
         assert (ws.op[b0:b1] == sc.LDS_WRITE).sum() > 0
-        assert (ws.op[b1:] == sc.LDS_WRITE).sum() == 0
+        nbar = int((ws.op == sc.BARRIER).sum())
+        end = nth(ws.op, sc.BARRIER, nbar - 2) if pair else len(ws.op)
+        assert (ws.op[b1:end] == sc.LDS_WRITE).sum() == 0
+        assert (ws.op[end:] == sc.LDS_WRITE).sum() == (16 if pair else 0)
 
 
 @pytest.mark.parametrize("tile", [0, 1])
@@ -476,6 +485,27 @@ def test_partial_k_step_missing_barrier_is_caught(tile):
     waves, lds = partial_waves(tile)
     mutated = [edit(ws, keep=lambda op: np.arange(len(op)) != nth(op, sc.BARRIER, 1)) for ws in waves]
     assert {v.kind for v in sc.check_workgroup_lds(mutated, lds)} & {"raw", "war", "waw"}
+
+
+@pytest.mark.parametrize("which", [-2, -1])
+def test_pair_exchange_barriers_are_needed(which):
+    """The 256 x 128 tile's wave pairs add their sums through LDS: without
+    the last K step's barrier, a wave's writes overwrite a stage that
+    another wave may still read; without the one between the writes and the
+    reads, a wave reads its partner's half before it is written."""
+    bm, bn, bk, threads = xg.xgemm_tile_info(1)
+    assert threads == 512
+    K = 6 * bk
+    ev, counts = sc.trace_workgroup(bm, bn, K, K, bn, bn, cfg(1), 256, 0, 0, threads)
+    waves = sc.wave_streams(ev, counts)
+    lds = xg.xgemm_trace_plan(bm, bn, K, sc.BASE_A, K, sc.BASE_B, bn, sc.BASE_C, bn, cfg(1), 256, 0).lds_bytes
+    assert sc.check_workgroup_lds(waves, lds) == []
+
+    def drop(ws):
+        n = int((ws.op == sc.BARRIER).sum())
+        return edit(ws, keep=lambda op: np.arange(len(op)) != nth(op, sc.BARRIER, n + which))
+    kinds = {v.kind for v in sc.check_workgroup_lds([drop(ws) for ws in waves], lds)}
+    assert kinds & ({"war", "waw"} if which == -2 else {"raw"})
 
 
 # ---------------------------------------------------------------------------
