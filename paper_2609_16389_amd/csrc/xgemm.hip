@@ -118,7 +118,10 @@ int64_t split_chunk(int64_t K, int split, int bk)
 // were fitted (least squares on log time) to 180 measured (tile, split)
 // timings over 21 shapes from 256^3 to 8192^3 and 1024 x 1024 x 65536; the
 // fit picks a configuration within 7% of the fastest measured one on every
-// shape, and the fastest on the five benchmark workloads.
+// shape, and the fastest on the five benchmark workloads.  Re-checked after
+// the 256 x 128 tile moved to eight waves: the fastest on 20 of 25 shapes,
+// within 4.6% on the others (refitting that tile alone made the large
+// shapes pick it, 10-20% slower).
 struct TileCost {
     double fixed_us, step_us, step_shared_us;
 };
