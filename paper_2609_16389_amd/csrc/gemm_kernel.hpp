@@ -1165,12 +1165,13 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
                     acc[h][j] = WK ? other + acc[KEEP + h][j] : acc[KEEP + h][j] + other;
                 }
         };
-        // Steps 0 .. nk-4 issue loads.  The whole K loop and the exchange
-        // are instantiated per parity P of their number, and per wk: the
-        // fragment buffers alternate with the step, and paths that joined
-        // before the last step would keep both buffers live.  With P = 1
-        // step 0 runs from buffer 1, so the loop always starts from buffer 0.
-        auto k_loop = [&]<int P, int WK>() {
+        // Steps 0 .. nk-4 issue loads.  The whole K loop is instantiated per
+        // parity P of their number: the fragment buffers alternate with the
+        // step, and paths that joined before the last step would keep both
+        // buffers live.  With P = 1 step 0 runs from buffer 1, so the loop
+        // always starts from buffer 0.  After the last step only the
+        // accumulators are live, and the exchange is instantiated per wk.
+        auto k_loop = [&]<int P>() {
             const int nl = nk - 3;
 #pragma unroll
             for (int i = 0; i < FM; ++i)
@@ -1188,7 +1189,6 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
                 kstep_k.template operator()<1, true, 1>(t + 1);
             }
             last3.template operator()<0>(t);
-            exchange.template operator()<WK>();
         };
         if (nk >= 3) {
             issue_loads(0, 0);
@@ -1197,15 +1197,14 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
             ops.template wait_vm<2 * LD>();
             ops.barrier();
             zero_partial();
-            const int sel = ((nk - 3) & 1) * 2 + (wk & 1);
-            if (sel == 0)
-                k_loop.template operator()<0, 0>();
-            else if (sel == 1)
-                k_loop.template operator()<0, 1>();
-            else if (sel == 2)
-                k_loop.template operator()<1, 0>();
+            if ((nk - 3) & 1)
+                k_loop.template operator()<1>();
             else
-                k_loop.template operator()<1, 1>();
+                k_loop.template operator()<0>();
+            if (wk)
+                exchange.template operator()<1>();
+            else
+                exchange.template operator()<0>();
         }
     } else if (nk >= STAGES) {
         // prologue: fill every stage, wait for stage 0
