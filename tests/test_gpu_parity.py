@@ -101,6 +101,20 @@ def test_partial_k_step(tile, shape):
                     "partial step tile %d %s %s" % (tile, dtype, shape))
 
 
+# The 256 x 128 tile's two waves per block split every K step, and its K
+# loop is instantiated per parity of the number of steps that issue loads
+# (nk - 3): every step count from the pipeline's minimum of 3 to 9, with and
+# without a partial last step, so both parities, the shortest loops and the
+# loop-free case all run.
+@pytest.mark.parametrize("K", [192, 256, 320, 384, 448, 512, 576, 200, 264, 328])
+def test_wave_pair_step_counts(K):
+    M, N = 300, 264
+    assert _family(M, N, K, config(1)) == xg.XGEMM_KERNEL_PIPELINED
+    for dtype in ("bf16", "fp16"):
+        A, B, C_ref, S = _case(M, N, K, dtype, seed=K + 7)
+        check_close(run_gpu(A, B, dtype, config=config(1)), C_ref, S, "wave pairs %s K=%d" % (dtype, K))
+
+
 @pytest.mark.parametrize("tile", TILES)
 @pytest.mark.parametrize("dtype", ["bf16", "fp16"])
 def test_partial_k_step_never_reads_past_k(tile, dtype):
