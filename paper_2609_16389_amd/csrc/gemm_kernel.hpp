@@ -1165,29 +1165,45 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
                     acc[h][j] = WK ? other + acc[KEEP + h][j] : acc[KEEP + h][j] + other;
                 }
         };
-        // Steps 0 .. nk-4 issue loads.  The whole K loop is instantiated per
-        // parity P of their number: the fragment buffers alternate with the
-        // step, and paths that joined before the last step would keep both
-        // buffers live.  With P = 1 step 0 runs from buffer 1, so the loop
-        // always starts from buffer 0.  After the last step only the
+        // Steps 0 .. nk-4 issue loads (nl of them).  The K loop is
+        // instantiated per parity of nl: the fragment buffers alternate with
+        // the step, and with an odd nl step 0 runs from buffer 1, so that the
+        // loop of two steps and the last three always start from buffer 0.
+        // The loop body runs at least once (nk = 3 and 4 are straight-line
+        // code of their own): a path that skipped it kept the first
+        // fragments live across it and spilled.  After the last step only the
         // accumulators are live, and the exchange is instantiated per wk.
-        auto k_loop = [&]<int P>() {
-            const int nl = nk - 3;
+        // (buffer 1 is read B first: the branches then begin differently, so
+        // the compiler does not hoist the common reads above them, where
+        // they would stay live across the loop)
+        auto first_frags = [&]<int P>() {
+            if constexpr (P == 1) {
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    gb[P][j] = frag_B(0, wk, j);
+            }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
                 ga[P][i] = frag_A(0, wk, i);
+            if constexpr (P == 0) {
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                gb[P][j] = frag_B(0, wk, j);
+                for (int j = 0; j < FN; ++j)
+                    gb[P][j] = frag_B(0, wk, j);
+            }
+        };
+        auto k_loop = [&]<int P>() {
+            const int nl = nk - 3;
+            first_frags.template operator()<P>();
             int t = 0;
             if constexpr (P == 1) {
                 kstep_k.template operator()<1, true, 1>(0);
                 t = 1;
             }
-            for (; t + 2 <= nl; t += 2) {
+            do {
                 kstep_k.template operator()<0, true, 1>(t);
                 kstep_k.template operator()<1, true, 1>(t + 1);
-            }
+                t += 2;
+            } while (t + 2 <= nl);
             last3.template operator()<0>(t);
         };
         if (nk >= 3) {
@@ -1197,10 +1213,18 @@ __host__ __device__ __forceinline__ void dma_tile(const Ops &ops, const GemmPara
             ops.template wait_vm<2 * LD>();
             ops.barrier();
             zero_partial();
-            if ((nk - 3) & 1)
+            if (nk == 3) {
+                first_frags.template operator()<0>();
+                last3.template operator()<0>(0);
+            } else if (nk == 4) {
+                first_frags.template operator()<1>();
+                kstep_k.template operator()<1, true, 1>(0);
+                last3.template operator()<0>(1);
+            } else if ((nk - 3) & 1) {
                 k_loop.template operator()<1>();
-            else
+            } else {
                 k_loop.template operator()<0>();
+            }
             if (wk)
                 exchange.template operator()<1>();
             else

@@ -368,3 +368,28 @@ def test_band_selection_rejects_bad_arguments():
     # empty problems: no band
     assert xg.lib.xgemm_select_band(0, 4096, 4096, 0, 256, ctypes.byref(out)) == xg.XGEMM_OK
     assert out.axis == xg.XGEMM_BAND_NONE
+
+
+def test_kernels_use_no_scratch(tmp_path):
+    """No kernel of libxgemm.so has a private (scratch) segment.  A kernel
+    that spills registers gets one, and the runtime then allocates scratch
+    memory at its first launch: xgemm_run_noalloc would allocate after all.
+    Reads the gfx950 code object's metadata (objcopy, the offload bundler and
+    llvm-readelf of this image)."""
+    import os
+    import re
+    import shutil
+    import subprocess
+    bundler = "/opt/rocm/llvm/bin/clang-offload-bundler"
+    readelf = "/opt/rocm/llvm/bin/llvm-readelf"
+    if not (shutil.which("objcopy") and os.path.exists(bundler) and os.path.exists(readelf)):
+        pytest.skip("objcopy / clang-offload-bundler / llvm-readelf not available")
+    fat, co = tmp_path / "fat.bin", tmp_path / "gfx950.co"
+    subprocess.run(["objcopy", "-O", "binary", "--only-section=.hip_fatbin", xg._LIB_PATH, str(fat)], check=True)
+    subprocess.run([bundler, "--unbundle", "--type=o", "--input=" + str(fat),
+                    "--targets=hipv4-amdgcn-amd-amdhsa--gfx950", "--output=" + str(co)], check=True)
+    notes = subprocess.run([readelf, "--notes", str(co)], check=True, capture_output=True, text=True).stdout
+    symbols = re.findall(r"\.symbol:\s+(\S+)\.kd", notes)
+    sizes = [int(v) for v in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", notes)]
+    assert len(sizes) == len(symbols) >= 20, (len(sizes), len(symbols))
+    assert all(v == 0 for v in sizes), [(n, v) for n, v in zip(symbols, sizes) if v]
