@@ -707,7 +707,7 @@ def test_full_size_8192_integer_exact_sampled():
 # (M, N, K, dtype): bands of columns, of rows, and one with both operands
 # copied (N and M odd)
 BANDED = [(2560, 6656, 1000, "bf16"), (3072, 5632, 1024, "fp16"), (9472, 2048, 1000, "bf16"),
-          (2047, 10239, 1000, "fp16")]
+          (2047, 10239, 1000, "fp16"), (4096, 6144, 1000, "bf16")]   # the last: a band of 256 x 128 wave-pair tiles
 
 
 def _band_or_skip(M, N, K, dtype):
